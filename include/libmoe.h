@@ -1,0 +1,175 @@
+/*
+ * libmoe: the Mixture-of-Experts layer forward on one GPU's share of the
+ * work, for AMD Instinct MI355X (gfx950).
+ *
+ * The paper (Sec. 2.1 and Sec. 3.1) runs the expert layer in two layouts:
+ *
+ *  - tensor parallel (TP): every rank holds one I/P slice of every expert,
+ *    W13 (E, 2I/P, H) and W2 (E, H, I/P); all tokens are present and the
+ *    rank's output is a partial sum that an all-reduce completes;
+ *  - expert parallel (EP): a rank holds E/P whole experts, W13 (E/P, 2I, H)
+ *    and W2 (E/P, H, I), and computes only the (token, expert) pairs routed
+ *    to them; a combine all-to-all completes the output.
+ *
+ * W13 stacks the gate projection (rows [0, I_s)) before the up projection
+ * (rows [I_s, 2*I_s)) of a SwiGLU MLP; I_s is the rank's intermediate width
+ * (I under EP, I/P under TP).  Both layouts compute the same function of the
+ * same weights (Sec. 1, Sec. 3), so one library serves both: a TP slice is
+ * expert_begin = 0, n_local_experts = E, I_s = I/P; an EP slice is
+ * expert_begin = r*E/P, n_local_experts = E/P, I_s = I.
+ *
+ * The forward is four calls on one stream:
+ *   moe_route -> moe_permute -> moe_grouped_ffn -> moe_combine
+ *
+ * Conventions for every call:
+ *  - Array arguments are DEVICE pointers owned by the caller, row-major and
+ *    contiguous.  bf16 tensors are passed as uint16_t bit patterns.
+ *  - The library never allocates, frees or synchronises; scratch memory is
+ *    the caller's `workspace` (sizes from the *_workspace_size queries).
+ *    Work is enqueued on `stream` (a hipStream_t; NULL = default stream) and
+ *    results are valid once that stream has been synchronised.  No call
+ *    reads device data back to the host, so the chain can be captured in a
+ *    HIP graph.
+ *  - Arguments are validated on the host before any HIP call; a rejected
+ *    call returns MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED or
+ *    MOE_ERR_WORKSPACE, enqueues nothing and leaves every buffer untouched.
+ *    A failed kernel launch returns MOE_ERR_HIP.  moe_last_error() gives a
+ *    message for the last non-OK status on the calling thread.
+ *  - Sizes: 1 <= E <= 1024, 1 <= k <= min(E, 16), T >= 0, T*k < 2^31,
+ *    H and I_s positive multiples of 8.
+ */
+#ifndef LIBMOE_H
+#define LIBMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum moe_status {
+    MOE_OK = 0,
+    MOE_ERR_INVALID_ARG = 1, /* null pointer, negative or inconsistent size */
+    MOE_ERR_UNSUPPORTED = 2, /* outside the documented limits */
+    MOE_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required */
+    MOE_ERR_HIP = 4          /* a HIP runtime call or kernel launch failed */
+} moe_status;
+
+#define MOE_MAX_TOPK 16
+#define MOE_MAX_EXPERTS 1024
+
+/* Static name of a status code ("MOE_OK", ...). */
+const char *moe_status_str(int status);
+
+/* Message for the last non-OK status returned on the calling thread. */
+const char *moe_last_error(void);
+
+/* Library interface version (incremented on any ABI change). */
+int moe_version(void);
+
+/*
+ * Gating.  The paper names sparse per-token expert selection (Sec. 1) but
+ * not the gating function; libmoe uses softmax top-k renormalised over the
+ * kept experts.  For each token t:
+ *   - topk_ids[t, 0..k-1]: the k experts with the largest logits, largest
+ *     first; equal logits order by ascending expert id, and -0.0 equals +0.0;
+ *   - topk_w[t, j] = exp(l_j - l_0) / sum_{i<k} exp(l_i - l_0), the softmax
+ *     over all E logits renormalised over the kept k (weights sum to 1).
+ * logits   [T, E] fp32, finite (NaN/Inf give unspecified ids and weights)
+ * topk_ids [T, k] int32 out;  topk_w [T, k] fp32 out.
+ */
+moe_status moe_route(const float *logits, int64_t T, int E, int k, int32_t *topk_ids,
+                     float *topk_w, void *stream);
+
+/*
+ * Permutation (token sort by expert).  Pair p = t*k + j is local when
+ * expert_begin <= topk_ids[t, j] < expert_begin + n_local_experts (an EP
+ * rank sees only the pairs routed to its experts, Sec. 2.1; a TP rank owns
+ * every expert).  Local pairs are ordered by local expert, then by
+ * ascending token; this order is unique, so every output is deterministic.
+ *   counts      [El]        int32 out: pairs per local expert
+ *   offsets     [El + 1]    int32 out: exclusive prefix sum of counts;
+ *                           offsets[El] = n, the number of local pairs
+ *   row_to_pair [T*min(k,El)] int32 out: rows [0, n) hold the pair index
+ *   pair_to_row [T*k]       int32 out: the pair's row, or -1 if not local
+ *   x [T, H] bf16 and x_perm [T*min(k,El), H] bf16: when x_perm is not
+ *   NULL, row r of x_perm is set to x[row_to_pair[r] / k] for r < n (x may
+ *   be NULL when x_perm is NULL).
+ * Rows at and beyond n of row_to_pair / x_perm are left untouched.
+ * workspace: at least moe_permute_workspace_size(T, k, n_local_experts)
+ * bytes, 256-byte aligned.
+ */
+size_t moe_permute_workspace_size(int64_t T, int k, int n_local_experts);
+moe_status moe_permute(const int32_t *topk_ids, int64_t T, int k, int E, int expert_begin,
+                       int n_local_experts, int32_t *counts, int32_t *offsets,
+                       int32_t *row_to_pair, int32_t *pair_to_row, const uint16_t *x, int H,
+                       uint16_t *x_perm, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Grouped SwiGLU expert FFN (Sec. 3.1 weight shapes).  For every local
+ * expert e and every row r in [offsets[e], offsets[e+1]):
+ *   g = x_perm[r] . W13[e, 0:I_s]^T,   u = x_perm[r] . W13[e, I_s:2*I_s]^T
+ *   h = silu(g) * u  (fp32, then rounded to bf16)
+ *   y[r] = h . W2[e]^T  (fp32 accumulation, rounded to bf16)
+ *   x_perm [cap_rows, H] bf16;  offsets [El + 1] int32 (as moe_permute
+ *   writes them; rows beyond cap_rows are never touched even if offsets
+ *   claim them);  w13 [El, 2*I_s, H] bf16;  w2 [El, H, I_s] bf16;
+ *   y [cap_rows, H] bf16 out (rows >= offsets[El] untouched).
+ * Experts with no rows read none of their weights.
+ * workspace: at least moe_ffn_workspace_size(cap_rows, El, H, I_s) bytes,
+ * 256-byte aligned (holds the bf16 intermediate h and the tile schedule).
+ */
+size_t moe_ffn_workspace_size(int64_t cap_rows, int n_local_experts, int H, int I_s);
+moe_status moe_grouped_ffn(const uint16_t *x_perm, const int32_t *offsets, int n_local_experts,
+                           int64_t cap_rows, int H, int I_s, const uint16_t *w13,
+                           const uint16_t *w2, uint16_t *y, void *workspace,
+                           size_t workspace_bytes, void *stream);
+
+/*
+ * Combine (unpermute and gate-weighted reduce).  For every token t:
+ *   out[t] = (accumulate ? out[t] : 0)
+ *          + (shared_begin <= t < shared_begin + shared_count ? shared_y[t - shared_begin] : 0)
+ *          + sum_{j=0..k-1, pair_to_row[t*k+j] >= 0} topk_w[t, j] * y[pair_to_row[t*k+j]]
+ * accumulated in fp32 in that order and rounded once to bf16.  The result
+ * is the rank's partial output: the TP partial sum before the all-reduce,
+ * or the EP partial before the combine all-to-all (Sec. 1); a token with no
+ * local pair gets 0 (or its prior value).  The optional shared term carries
+ * a shared expert's output for the rank's own data-parallel token share.
+ *   y [y_rows, H] bf16;  pair_to_row [T*k] int32 (rows >= y_rows are
+ *   skipped);  topk_w [T, k] fp32;  shared_y [shared_count, H] bf16 or
+ *   NULL;  out [T, H] bf16 in/out.
+ */
+moe_status moe_combine(const uint16_t *y, int64_t y_rows, const int32_t *pair_to_row,
+                       const float *topk_w, int64_t T, int k, int H, const uint16_t *shared_y,
+                       int64_t shared_begin, int64_t shared_count, int accumulate,
+                       uint16_t *out, void *stream);
+
+/*
+ * Per-kernel timing for measurement.  While enabled, every kernel the
+ * library launches is bracketed by HIP events on its own stream (this adds
+ * event records to the stream; it never synchronises).  moe_timing_read
+ * waits for the recorded events and returns, for one kernel kind, the summed
+ * duration in milliseconds and the number of launches since the last reset.
+ * Kinds: see enum moe_kernel_kind.  Enabling allocates nothing on the device.
+ */
+typedef enum moe_kernel_kind {
+    MOE_K_ROUTE = 0,
+    MOE_K_PERMUTE = 1,   /* count + scan + scatter */
+    MOE_K_GATHER = 2,    /* x_perm row gather */
+    MOE_K_SCHEDULE = 3,  /* grouped-FFN tile schedule */
+    MOE_K_GATE_UP = 4,   /* gate-up GEMM with the SwiGLU epilogue */
+    MOE_K_DOWN = 5,      /* down GEMM (and its split-K reduction) */
+    MOE_K_COMBINE = 6,
+    MOE_K_COUNT = 7
+} moe_kernel_kind;
+
+moe_status moe_timing_enable(int enable);
+moe_status moe_timing_reset(void);
+moe_status moe_timing_read(int kind, double *total_ms, int64_t *launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIBMOE_H */

@@ -20,14 +20,18 @@ The paper's workloads (Qwen3-235B weights, ShareGPT, DeepMath) are not
 available; these synthetic layers stand in for them, with the model shapes
 of Mixtral, Qwen-MoE and DeepSeek-V3.
 
-Random draws are keyed per (tensor, expert, 8-row chunk), so a TP or EP
+Random draws are keyed per (tensor, expert, chunk of rows), so a TP or EP
 slice of a weight is generated without generating the whole weight, and the
-slices of all P ranks concatenate to exactly the unsliced tensor.
+slices of all P ranks concatenate to exactly the unsliced tensor.  The chunk
+is 64 rows when I is a multiple of 512 and 8 rows otherwise; a TP slice
+width must be a multiple of it.
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 import dataclasses
 import math
+import os
 from typing import Optional
 
 import numpy as np
@@ -35,8 +39,12 @@ import numpy as np
 # Distinct stream tags for each drawn tensor.
 _TAG_X, _TAG_WR, _TAG_W1, _TAG_W3, _TAG_W2 = 11, 12, 13, 14, 15
 _TAG_SW1, _TAG_SW3, _TAG_SW2, _TAG_ZIPF, _TAG_Y, _TAG_W = 16, 17, 18, 19, 20, 21
-_CHUNK = 8  # rows (W1/W3) or columns (W2) drawn per generator stream
 EXPERT_STD = 0.02
+
+
+def weight_chunk(I: int) -> int:
+    """Rows (W1/W3) or columns (W2) drawn per generator stream."""
+    return 64 if I % 512 == 0 else 8
 
 
 @dataclasses.dataclass(frozen=True)
@@ -93,9 +101,9 @@ class MoeConfig:
         if self.layout == "ep":
             assert self.E % self.P == 0
         if self.layout == "tp":
-            assert self.I % self.P == 0 and (self.I // self.P) % _CHUNK == 0
+            assert self.I % self.P == 0 and (self.I // self.P) % weight_chunk(self.I) == 0
         assert 0 <= self.rank < self.P
-        assert self.H % _CHUNK == 0 and self.I % _CHUNK == 0
+        assert self.H % 8 == 0 and self.I % 8 == 0
 
     def with_(self, **kw) -> "MoeConfig":
         return dataclasses.replace(self, **kw)
@@ -144,21 +152,21 @@ def _normal_bf16(shape, std: float, *key: int) -> np.ndarray:
     return f32_to_bf16_bits(g)
 
 
-def _rows(tag: int, seed: int, e: int, r0: int, r1: int, H: int, std: float) -> np.ndarray:
-    """Rows [r0, r1) of a (rows, H) weight, drawn in 8-row chunks."""
-    assert r0 % _CHUNK == 0 and r1 % _CHUNK == 0
+def _rows(tag: int, seed: int, e: int, r0: int, r1: int, H: int, std: float, ch: int) -> np.ndarray:
+    """Rows [r0, r1) of a (rows, H) weight, drawn in chunks of ch rows."""
+    assert r0 % ch == 0 and r1 % ch == 0
     out = np.empty((r1 - r0, H), dtype=np.uint16)
-    for c in range(r0 // _CHUNK, r1 // _CHUNK):
-        out[c * _CHUNK - r0:(c + 1) * _CHUNK - r0] = _normal_bf16((_CHUNK, H), std, seed, tag, e, c)
+    for c in range(r0 // ch, r1 // ch):
+        out[c * ch - r0:(c + 1) * ch - r0] = _normal_bf16((ch, H), std, seed, tag, e, c)
     return out
 
 
-def _cols(tag: int, seed: int, e: int, c0: int, c1: int, H: int, std: float) -> np.ndarray:
-    """Columns [c0, c1) of an (H, I) weight, drawn in 8-column chunks."""
-    assert c0 % _CHUNK == 0 and c1 % _CHUNK == 0
+def _cols(tag: int, seed: int, e: int, c0: int, c1: int, H: int, std: float, ch: int) -> np.ndarray:
+    """Columns [c0, c1) of an (H, I) weight, drawn in chunks of ch columns."""
+    assert c0 % ch == 0 and c1 % ch == 0
     out = np.empty((H, c1 - c0), dtype=np.uint16)
-    for c in range(c0 // _CHUNK, c1 // _CHUNK):
-        out[:, c * _CHUNK - c0:(c + 1) * _CHUNK - c0] = _normal_bf16((H, _CHUNK), std, seed, tag, e, c)
+    for c in range(c0 // ch, c1 // ch):
+        out[:, c * ch - c0:(c + 1) * ch - c0] = _normal_bf16((H, ch), std, seed, tag, e, c)
     return out
 
 
@@ -205,16 +213,18 @@ def expert_weights(cfg: MoeConfig, e: int):
     (w13 [2*I_s, H], w2 [H, I_s])."""
     c0 = cfg.rank * cfg.I_s if cfg.layout == "tp" else 0
     c1 = c0 + cfg.I_s
-    g = _rows(_TAG_W1, cfg.seed, e, c0, c1, cfg.H, EXPERT_STD)
-    u = _rows(_TAG_W3, cfg.seed, e, c0, c1, cfg.H, EXPERT_STD)
-    w2 = _cols(_TAG_W2, cfg.seed, e, c0, c1, cfg.H, EXPERT_STD)
+    ch = weight_chunk(cfg.I)
+    g = _rows(_TAG_W1, cfg.seed, e, c0, c1, cfg.H, EXPERT_STD, ch)
+    u = _rows(_TAG_W3, cfg.seed, e, c0, c1, cfg.H, EXPERT_STD, ch)
+    w2 = _cols(_TAG_W2, cfg.seed, e, c0, c1, cfg.H, EXPERT_STD, ch)
     return np.concatenate([g, u], axis=0), w2
 
 
 def shared_weights(cfg: MoeConfig):
-    g = _rows(_TAG_SW1, cfg.seed, 0, 0, cfg.I, cfg.H, EXPERT_STD)
-    u = _rows(_TAG_SW3, cfg.seed, 0, 0, cfg.I, cfg.H, EXPERT_STD)
-    w2 = _cols(_TAG_SW2, cfg.seed, 0, 0, cfg.I, cfg.H, EXPERT_STD)
+    ch = weight_chunk(cfg.I)
+    g = _rows(_TAG_SW1, cfg.seed, 0, 0, cfg.I, cfg.H, EXPERT_STD, ch)
+    u = _rows(_TAG_SW3, cfg.seed, 0, 0, cfg.I, cfg.H, EXPERT_STD, ch)
+    w2 = _cols(_TAG_SW2, cfg.seed, 0, 0, cfg.I, cfg.H, EXPERT_STD, ch)
     return np.concatenate([g, u], axis=0)[None], w2[None]
 
 
@@ -226,8 +236,12 @@ def make_inputs(cfg: MoeConfig, with_weights: bool = True) -> MoeInputs:
     if with_weights:
         w13 = np.empty((El, 2 * Is, H), dtype=np.uint16)
         w2 = np.empty((El, H, Is), dtype=np.uint16)
-        for le in range(El):
+
+        def fill(le):
             w13[le], w2[le] = expert_weights(cfg, cfg.e0 + le)
+        workers = max(1, min(8, El, len(os.sched_getaffinity(0))))
+        with cf.ThreadPoolExecutor(workers) as ex:
+            list(ex.map(fill, range(El)))
     else:
         w13 = np.empty((El, 2 * Is, H), dtype=np.uint16)[:0]
         w2 = np.empty((El, H, Is), dtype=np.uint16)[:0]

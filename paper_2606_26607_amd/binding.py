@@ -1,0 +1,272 @@
+"""Thin ctypes binding over libmoe.so (the C ABI in include/libmoe.h).
+
+Each function takes torch tensors that already live on the GPU, checks
+dtype/shape/contiguity, and passes raw device pointers plus the current HIP
+stream to the library.  No arithmetic of the layer happens here: every step
+runs in the library's HIP kernels.  If libmoe.so is missing the import of a
+call raises; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmoe.so")
+
+MAX_TOPK = 16
+MAX_EXPERTS = 1024
+KERNEL_KINDS = {"route": 0, "permute": 1, "gather": 2, "schedule": 3, "gate_up": 4, "down": 5,
+                "combine": 6}
+
+
+class MoeError(RuntimeError):
+    """A libmoe call returned a non-OK status."""
+
+    def __init__(self, status: int, name: str, msg: str):
+        super().__init__(f"{name}: {msg}")
+        self.status = status
+        self.name = name
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"libmoe.so not found at {LIB_PATH}; build it with "
+                          "`python -m paper_2606_26607_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    i64, i32, vp, sz = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t
+    sigs = {
+        "moe_status_str": ([i32], ctypes.c_char_p),
+        "moe_last_error": ([], ctypes.c_char_p),
+        "moe_version": ([], i32),
+        "moe_route": ([vp, i64, i32, i32, vp, vp, vp], i32),
+        "moe_permute_workspace_size": ([i64, i32, i32], sz),
+        "moe_permute": ([vp, i64, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, vp, vp, sz, vp], i32),
+        "moe_ffn_workspace_size": ([i64, i32, i32, i32], sz),
+        "moe_grouped_ffn": ([vp, vp, i32, i64, i32, i32, vp, vp, vp, vp, sz, vp], i32),
+        "moe_combine": ([vp, i64, vp, vp, i64, i32, i32, vp, i64, i64, i32, vp, vp], i32),
+        "moe_timing_enable": ([i32], i32),
+        "moe_timing_reset": ([], i32),
+        "moe_timing_read": ([i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)], i32),
+    }
+    for name, (args, res) in sigs.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = L
+    return L
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        L = lib()
+        raise MoeError(status, L.moe_status_str(status).decode(), L.moe_last_error().decode())
+
+
+def _stream(stream=None) -> Optional[int]:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream or None
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else (t.data_ptr() or None)
+
+
+def _need(t: torch.Tensor, dtype, name: str, ndim: Optional[int] = None) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got {tuple(t.shape)}")
+
+
+# ------------------------------------------------------------- the 4 calls
+def route(logits: torch.Tensor, k: int, topk_ids: Optional[torch.Tensor] = None,
+          topk_w: Optional[torch.Tensor] = None, stream=None):
+    _need(logits, torch.float32, "logits", 2)
+    T, E = logits.shape
+    if topk_ids is None:
+        topk_ids = torch.empty((T, k), dtype=torch.int32, device=logits.device)
+    if topk_w is None:
+        topk_w = torch.empty((T, k), dtype=torch.float32, device=logits.device)
+    _check(lib().moe_route(_ptr(logits), T, E, k, _ptr(topk_ids), _ptr(topk_w), _stream(stream)))
+    return topk_ids, topk_w
+
+
+def permute_workspace_size(T: int, k: int, n_local: int) -> int:
+    return int(lib().moe_permute_workspace_size(T, k, n_local))
+
+
+def ffn_workspace_size(cap_rows: int, n_local: int, H: int, I_s: int) -> int:
+    return int(lib().moe_ffn_workspace_size(cap_rows, n_local, H, I_s))
+
+
+def permute(topk_ids: torch.Tensor, E: int, expert_begin: int, n_local: int,
+            x: Optional[torch.Tensor] = None, gather: bool = True, out: Optional[dict] = None,
+            workspace: Optional[torch.Tensor] = None, stream=None) -> dict:
+    _need(topk_ids, torch.int32, "topk_ids", 2)
+    T, k = topk_ids.shape
+    dev = topk_ids.device
+    cap = T * min(k, n_local)
+    o = dict(out or {})
+    o.setdefault("counts", torch.empty(n_local, dtype=torch.int32, device=dev))
+    o.setdefault("offsets", torch.empty(n_local + 1, dtype=torch.int32, device=dev))
+    o.setdefault("row_to_pair", torch.empty(max(cap, 1), dtype=torch.int32, device=dev))
+    o.setdefault("pair_to_row", torch.empty(max(T * k, 1), dtype=torch.int32, device=dev))
+    H = 0
+    if x is not None and gather:
+        _need(x, torch.bfloat16, "x", 2)
+        H = x.shape[1]
+        o.setdefault("x_perm", torch.empty((max(cap, 1), H), dtype=torch.bfloat16, device=dev))
+    else:
+        o["x_perm"] = None
+    if workspace is None:
+        workspace = torch.empty(permute_workspace_size(T, k, n_local), dtype=torch.uint8, device=dev)
+    _check(lib().moe_permute(_ptr(topk_ids), T, k, E, expert_begin, n_local, _ptr(o["counts"]),
+                             _ptr(o["offsets"]), _ptr(o["row_to_pair"]), _ptr(o["pair_to_row"]),
+                             _ptr(x) if o["x_perm"] is not None else None, H, _ptr(o["x_perm"]),
+                             _ptr(workspace), workspace.numel(), _stream(stream)))
+    return o
+
+
+def grouped_ffn(x_perm: torch.Tensor, offsets: torch.Tensor, w13: torch.Tensor, w2: torch.Tensor,
+                y: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                stream=None) -> torch.Tensor:
+    _need(x_perm, torch.bfloat16, "x_perm", 2)
+    _need(offsets, torch.int32, "offsets", 1)
+    _need(w13, torch.bfloat16, "w13", 3)
+    _need(w2, torch.bfloat16, "w2", 3)
+    cap, H = x_perm.shape
+    El = offsets.numel() - 1
+    I_s = w2.shape[2]
+    if tuple(w13.shape) != (El, 2 * I_s, H) or tuple(w2.shape) != (El, H, I_s):
+        raise ValueError(f"weight shapes {tuple(w13.shape)}, {tuple(w2.shape)} do not match "
+                         f"El={El}, H={H}, I_s={I_s}")
+    if y is None:
+        y = torch.empty((cap, H), dtype=torch.bfloat16, device=x_perm.device)
+    _need(y, torch.bfloat16, "y", 2)
+    if y.shape[0] < cap or y.shape[1] != H:
+        raise ValueError("y must be [cap_rows, H]")
+    if workspace is None:
+        workspace = torch.empty(ffn_workspace_size(cap, El, H, I_s), dtype=torch.uint8,
+                                device=x_perm.device)
+    _check(lib().moe_grouped_ffn(_ptr(x_perm), _ptr(offsets), El, cap, H, I_s, _ptr(w13), _ptr(w2),
+                                 _ptr(y), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return y
+
+
+def combine(y: torch.Tensor, pair_to_row: torch.Tensor, topk_w: torch.Tensor,
+            out: Optional[torch.Tensor] = None, shared_y: Optional[torch.Tensor] = None,
+            shared_begin: int = 0, accumulate: bool = False, stream=None) -> torch.Tensor:
+    _need(y, torch.bfloat16, "y", 2)
+    _need(topk_w, torch.float32, "topk_w", 2)
+    _need(pair_to_row, torch.int32, "pair_to_row")
+    T, k = topk_w.shape
+    H = y.shape[1]
+    if pair_to_row.numel() < T * k:
+        raise ValueError("pair_to_row must hold T*k entries")
+    if out is None:
+        out = torch.empty((T, H), dtype=torch.bfloat16, device=y.device)
+    _need(out, torch.bfloat16, "out", 2)
+    sc = 0
+    if shared_y is not None:
+        _need(shared_y, torch.bfloat16, "shared_y", 2)
+        sc = shared_y.shape[0]
+    _check(lib().moe_combine(_ptr(y), y.shape[0], _ptr(pair_to_row), _ptr(topk_w), T, k, H,
+                             _ptr(shared_y), shared_begin, sc, 1 if accumulate else 0, _ptr(out),
+                             _stream(stream)))
+    return out
+
+
+# ---------------------------------------------------------------- timing
+def timing_enable(on: bool = True) -> None:
+    _check(lib().moe_timing_enable(1 if on else 0))
+
+
+def timing_reset() -> None:
+    _check(lib().moe_timing_reset())
+
+
+def timing_read(kind: str):
+    """(total milliseconds, launches) for one kernel kind since the last reset."""
+    ms = ctypes.c_double()
+    n = ctypes.c_int64()
+    _check(lib().moe_timing_read(KERNEL_KINDS[kind], ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
+
+
+# ------------------------------------------------------------ the layer
+class MoeLayer:
+    """One GPU's share of an MoE layer forward with every buffer allocated
+    once (fixed addresses, so the four-call chain can be replayed from a HIP
+    graph).
+
+    w13 [El, 2*I_s, H], w2 [El, H, I_s]: this rank's routed-expert weights
+    (an EP slice of whole experts or a TP slice of every expert).  sw13/sw2:
+    an optional shared expert applied with weight 1 to tokens
+    [shared_begin, shared_begin + shared_count).
+    """
+
+    def __init__(self, T: int, E: int, k: int, expert_begin: int, w13: torch.Tensor,
+                 w2: torch.Tensor, sw13: Optional[torch.Tensor] = None,
+                 sw2: Optional[torch.Tensor] = None, shared_begin: int = 0, shared_count: int = 0):
+        dev = w13.device
+        self.T, self.E, self.k, self.e0 = T, E, k, expert_begin
+        self.El, two_is, self.H = w13.shape
+        self.I_s = two_is // 2
+        self.w13, self.w2 = w13, w2
+        self.cap = T * min(k, self.El)
+        cap1 = max(self.cap, 1)
+        self.topk_ids = torch.empty((T, k), dtype=torch.int32, device=dev)
+        self.topk_w = torch.empty((T, k), dtype=torch.float32, device=dev)
+        self.bufs = {
+            "counts": torch.empty(self.El, dtype=torch.int32, device=dev),
+            "offsets": torch.empty(self.El + 1, dtype=torch.int32, device=dev),
+            "row_to_pair": torch.empty(cap1, dtype=torch.int32, device=dev),
+            "pair_to_row": torch.empty(max(T * k, 1), dtype=torch.int32, device=dev),
+            "x_perm": torch.empty((cap1, self.H), dtype=torch.bfloat16, device=dev),
+        }
+        self.ws_perm = torch.empty(max(permute_workspace_size(T, k, self.El), 256), dtype=torch.uint8,
+                                   device=dev)
+        self.ws_ffn = torch.empty(ffn_workspace_size(cap1, self.El, self.H, self.I_s), dtype=torch.uint8,
+                                  device=dev)
+        self.y = torch.empty((cap1, self.H), dtype=torch.bfloat16, device=dev)
+        self.out = torch.empty((T, self.H), dtype=torch.bfloat16, device=dev)
+        self.sw13, self.sw2 = sw13, sw2
+        self.sb, self.sc = shared_begin, shared_count if sw13 is not None else 0
+        if self.sc:
+            sIs = sw2.shape[2]
+            self.s_offsets = torch.tensor([0, self.sc], dtype=torch.int32, device=dev)
+            self.s_y = torch.empty((self.sc, self.H), dtype=torch.bfloat16, device=dev)
+            self.ws_sh = torch.empty(ffn_workspace_size(self.sc, 1, self.H, sIs), dtype=torch.uint8,
+                                     device=dev)
+
+    def forward(self, x: torch.Tensor, logits: torch.Tensor, stream=None) -> torch.Tensor:
+        route(logits, self.k, self.topk_ids, self.topk_w, stream=stream)
+        permute(self.topk_ids, self.E, self.e0, self.El, x=x, out=self.bufs, workspace=self.ws_perm,
+                stream=stream)
+        grouped_ffn(self.bufs["x_perm"], self.bufs["offsets"], self.w13, self.w2, y=self.y,
+                    workspace=self.ws_ffn, stream=stream)
+        shared_y = None
+        if self.sc:
+            grouped_ffn(x[self.sb:self.sb + self.sc], self.s_offsets, self.sw13, self.sw2, y=self.s_y,
+                        workspace=self.ws_sh, stream=stream)
+            shared_y = self.s_y
+        combine(self.y, self.bufs["pair_to_row"], self.topk_w, out=self.out, shared_y=shared_y,
+                shared_begin=self.sb, stream=stream)
+        return self.out

@@ -1,0 +1,175 @@
+// libmoe C ABI: host-side argument validation, then kernel launches.
+// Validation happens before any HIP call, so a rejected call enqueues
+// nothing and touches no buffer.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "moe_internal.h"
+
+using namespace moe;
+
+namespace {
+
+thread_local char g_msg[512] = "no error";
+
+moe_status fail(moe_status st, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_msg, sizeof g_msg, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+moe_status hip_status(hipError_t err, const char *what)
+{
+    if (err == hipSuccess) return MOE_OK;
+    return fail(MOE_ERR_HIP, "%s: %s", what, hipGetErrorString(err));
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+moe_status check_topk(int64_t T, int E, int k)
+{
+    if (T < 0) return fail(MOE_ERR_INVALID_ARG, "T=%lld is negative", (long long)T);
+    if (E < 1) return fail(MOE_ERR_INVALID_ARG, "E=%d must be >= 1", E);
+    if (k < 1 || k > E) return fail(MOE_ERR_INVALID_ARG, "k=%d must be in [1, E=%d]", k, E);
+    if (E > MOE_MAX_EXPERTS) return fail(MOE_ERR_UNSUPPORTED, "E=%d exceeds %d", E, MOE_MAX_EXPERTS);
+    if (k > MOE_MAX_TOPK) return fail(MOE_ERR_UNSUPPORTED, "k=%d exceeds %d", k, MOE_MAX_TOPK);
+    if (T * (int64_t)k >= ((int64_t)1 << 31))
+        return fail(MOE_ERR_UNSUPPORTED, "T*k=%lld does not fit int32 indices", (long long)(T * k));
+    return MOE_OK;
+}
+
+moe_status check_width(const char *name, int v)
+{
+    if (v <= 0) return fail(MOE_ERR_INVALID_ARG, "%s=%d must be positive", name, v);
+    if (v % 8) return fail(MOE_ERR_UNSUPPORTED, "%s=%d is not a multiple of 8", name, v);
+    return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" const char *moe_status_str(int status)
+{
+    switch (status) {
+    case MOE_OK: return "MOE_OK";
+    case MOE_ERR_INVALID_ARG: return "MOE_ERR_INVALID_ARG";
+    case MOE_ERR_UNSUPPORTED: return "MOE_ERR_UNSUPPORTED";
+    case MOE_ERR_WORKSPACE: return "MOE_ERR_WORKSPACE";
+    case MOE_ERR_HIP: return "MOE_ERR_HIP";
+    default: return "MOE_ERR_UNKNOWN";
+    }
+}
+
+extern "C" const char *moe_last_error(void) { return g_msg; }
+
+extern "C" int moe_version(void) { return 1; }
+
+extern "C" moe_status moe_route(const float *logits, int64_t T, int E, int k, int32_t *topk_ids,
+                                float *topk_w, void *stream)
+{
+    moe_status st = check_topk(T, E, k);
+    if (st != MOE_OK) return st;
+    if (T > 0 && (!logits || !topk_ids || !topk_w))
+        return fail(MOE_ERR_INVALID_ARG, "moe_route: null pointer");
+    return hip_status(launch_route(logits, T, E, k, topk_ids, topk_w, (hipStream_t)stream),
+                      "moe_route launch");
+}
+
+extern "C" size_t moe_permute_workspace_size(int64_t T, int k, int n_local_experts)
+{
+    if (T < 0 || k < 1 || n_local_experts < 1) return 0;
+    return align256((size_t)(permute_chunks(T, k) + 1) * (size_t)n_local_experts * sizeof(int32_t));
+}
+
+extern "C" moe_status moe_permute(const int32_t *topk_ids, int64_t T, int k, int E, int expert_begin,
+                                  int n_local_experts, int32_t *counts, int32_t *offsets,
+                                  int32_t *row_to_pair, int32_t *pair_to_row, const uint16_t *x,
+                                  int H, uint16_t *x_perm, void *workspace, size_t workspace_bytes,
+                                  void *stream)
+{
+    moe_status st = check_topk(T, E, k);
+    if (st != MOE_OK) return st;
+    const int El = n_local_experts;
+    if (El < 1 || expert_begin < 0 || expert_begin + El > E)
+        return fail(MOE_ERR_INVALID_ARG, "local experts [%d, %d+%d) not inside [0, E=%d)",
+                    expert_begin, expert_begin, El, E);
+    if (!counts || !offsets) return fail(MOE_ERR_INVALID_ARG, "moe_permute: null counts/offsets");
+    if (T > 0 && (!topk_ids || !row_to_pair || !pair_to_row))
+        return fail(MOE_ERR_INVALID_ARG, "moe_permute: null index array");
+    if (x_perm) {
+        if ((st = check_width("H", H)) != MOE_OK) return st;
+        if (T > 0 && !x) return fail(MOE_ERR_INVALID_ARG, "moe_permute: x_perm given without x");
+        if (!aligned16(x) || !aligned16(x_perm))
+            return fail(MOE_ERR_INVALID_ARG, "moe_permute: x / x_perm not 16-byte aligned");
+    }
+    const size_t need = moe_permute_workspace_size(T, k, El);
+    if (!workspace || workspace_bytes < need)
+        return fail(MOE_ERR_WORKSPACE, "moe_permute: workspace %zu < %zu bytes", workspace_bytes, need);
+    const int64_t cap = T * (k < El ? k : El);
+    return hip_status(launch_permute(topk_ids, T, k, expert_begin, El, counts, offsets, row_to_pair,
+                                     pair_to_row, x, H, x_perm, cap, static_cast<int32_t *>(workspace),
+                                     (hipStream_t)stream),
+                      "moe_permute launch");
+}
+
+extern "C" size_t moe_ffn_workspace_size(int64_t cap_rows, int n_local_experts, int H, int I_s)
+{
+    if (cap_rows < 0 || n_local_experts < 1 || H <= 0 || I_s <= 0) return 0;
+    return ffn_workspace_bytes(cap_rows, n_local_experts, H, I_s);
+}
+
+extern "C" moe_status moe_grouped_ffn(const uint16_t *x_perm, const int32_t *offsets,
+                                      int n_local_experts, int64_t cap_rows, int H, int I_s,
+                                      const uint16_t *w13, const uint16_t *w2, uint16_t *y,
+                                      void *workspace, size_t workspace_bytes, void *stream)
+{
+    moe_status st;
+    if (n_local_experts < 1) return fail(MOE_ERR_INVALID_ARG, "n_local_experts=%d", n_local_experts);
+    if (n_local_experts > MOE_MAX_EXPERTS)
+        return fail(MOE_ERR_UNSUPPORTED, "n_local_experts=%d exceeds %d", n_local_experts, MOE_MAX_EXPERTS);
+    if (cap_rows < 0) return fail(MOE_ERR_INVALID_ARG, "cap_rows=%lld", (long long)cap_rows);
+    if (cap_rows >= ((int64_t)1 << 31)) return fail(MOE_ERR_UNSUPPORTED, "cap_rows too large");
+    if ((st = check_width("H", H)) != MOE_OK) return st;
+    if ((st = check_width("I_s", I_s)) != MOE_OK) return st;
+    if (!offsets) return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn: null offsets");
+    if (cap_rows > 0 && (!x_perm || !w13 || !w2 || !y))
+        return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn: null pointer");
+    if (!aligned16(x_perm) || !aligned16(w13) || !aligned16(w2) || !aligned16(y))
+        return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn: tensors must be 16-byte aligned");
+    const size_t need = moe_ffn_workspace_size(cap_rows, n_local_experts, H, I_s);
+    if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u))
+        return fail(MOE_ERR_WORKSPACE, "moe_grouped_ffn: workspace %zu < %zu bytes or misaligned",
+                    workspace_bytes, need);
+    return hip_status(launch_grouped_ffn(x_perm, offsets, n_local_experts, cap_rows, H, I_s, w13, w2,
+                                         y, workspace, (hipStream_t)stream),
+                      "moe_grouped_ffn launch");
+}
+
+extern "C" moe_status moe_combine(const uint16_t *y, int64_t y_rows, const int32_t *pair_to_row,
+                                  const float *topk_w, int64_t T, int k, int H,
+                                  const uint16_t *shared_y, int64_t shared_begin,
+                                  int64_t shared_count, int accumulate, uint16_t *out, void *stream)
+{
+    moe_status st;
+    if (T < 0 || y_rows < 0) return fail(MOE_ERR_INVALID_ARG, "negative T or y_rows");
+    if (k < 1) return fail(MOE_ERR_INVALID_ARG, "k=%d must be >= 1", k);
+    if (k > MOE_MAX_TOPK) return fail(MOE_ERR_UNSUPPORTED, "k=%d exceeds %d", k, MOE_MAX_TOPK);
+    if (T * (int64_t)k >= ((int64_t)1 << 31)) return fail(MOE_ERR_UNSUPPORTED, "T*k too large");
+    if ((st = check_width("H", H)) != MOE_OK) return st;
+    if (T > 0 && (!pair_to_row || !topk_w || !out))
+        return fail(MOE_ERR_INVALID_ARG, "moe_combine: null pointer");
+    if (y_rows > 0 && !y) return fail(MOE_ERR_INVALID_ARG, "moe_combine: null y with y_rows > 0");
+    if (shared_y) {
+        if (shared_begin < 0 || shared_count < 0 || shared_begin + shared_count > T)
+            return fail(MOE_ERR_INVALID_ARG, "shared rows [%lld, +%lld) outside [0, T)",
+                        (long long)shared_begin, (long long)shared_count);
+    }
+    if (!aligned16(y) || !aligned16(out) || !aligned16(shared_y))
+        return fail(MOE_ERR_INVALID_ARG, "moe_combine: tensors must be 16-byte aligned");
+    return hip_status(launch_combine(y, y_rows, pair_to_row, topk_w, T, k, H, shared_y,
+                                     shared_begin, shared_y ? shared_count : 0, accumulate ? 1 : 0,
+                                     out, (hipStream_t)stream),
+                      "moe_combine launch");
+}

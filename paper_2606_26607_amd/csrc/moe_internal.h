@@ -1,0 +1,70 @@
+// Internal declarations shared by the libmoe host API and its HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/libmoe.h"
+
+namespace moe {
+
+// ---------------------------------------------------------------- bf16
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b)
+{
+    return __uint_as_float((uint32_t)b << 16);
+}
+
+// fp32 -> bf16, round to nearest even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// Two packed bf16 (little-endian: low half first) <-> two floats.
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
+{
+    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+// ------------------------------------------------------------- timing
+// Record around every kernel launch when timing is enabled (see timing.cpp).
+struct KernelTimer {
+    int slot;
+    hipStream_t s;
+    KernelTimer(int kind, hipStream_t stream);
+    ~KernelTimer();
+};
+
+// ------------------------------------------------------------ launchers
+// Every launcher enqueues on `s` and returns hipGetLastError() of the launch.
+hipError_t launch_route(const float *logits, int64_t T, int E, int k, int32_t *ids, float *w,
+                        hipStream_t s);
+
+int64_t permute_chunks(int64_t T, int k);
+hipError_t launch_permute(const int32_t *ids, int64_t T, int k, int e0, int El, int32_t *counts,
+                          int32_t *offsets, int32_t *row_to_pair, int32_t *pair_to_row,
+                          const uint16_t *x, int H, uint16_t *x_perm, int64_t cap, int32_t *ws,
+                          hipStream_t s);
+
+size_t ffn_workspace_bytes(int64_t cap, int El, int H, int Is);
+hipError_t launch_grouped_ffn(const uint16_t *x_perm, const int32_t *offsets, int El, int64_t cap,
+                              int H, int Is, const uint16_t *w13, const uint16_t *w2, uint16_t *y,
+                              void *ws, hipStream_t s);
+
+hipError_t launch_combine(const uint16_t *y, int64_t y_rows, const int32_t *pair_to_row,
+                          const float *w, int64_t T, int k, int H, const uint16_t *shared_y,
+                          int64_t sb, int64_t sc, int accumulate, uint16_t *out, hipStream_t s);
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+}  // namespace moe

@@ -1,0 +1,191 @@
+// Permutation: stable counting sort of (token, slot) pairs by local expert.
+//
+// The T*k pairs are cut into chunks of 1024, one wavefront per chunk:
+//   1. count:   per-chunk histogram over local experts (LDS),
+//   2. scan:    per expert, exclusive prefix over chunks; per-expert totals
+//               and their exclusive prefix over experts give `offsets`, and
+//               each (chunk, expert) gets its first output row,
+//   3. scatter: each chunk walks its pairs in order, 64 at a time; lanes
+//               holding the same expert find each other with ballots over
+//               the bits of the expert index, so a pair's row is its chunk
+//               base + earlier pairs of that expert in the chunk + its rank
+//               among equal lanes.  No global atomics: the result is the
+//               unique stable order, identical on every run.
+//   4. gather:  optional copy of x rows into permuted order (16-byte moves).
+#include "moe_internal.h"
+
+namespace moe {
+namespace {
+
+constexpr int CHUNK = 1024;
+constexpr int ROUNDS = CHUNK / 64;
+
+__device__ __forceinline__ int local_index(int32_t id, int e0, int El)
+{
+    int d = id - e0;
+    return (d >= 0 && d < El) ? d : El;  // El marks a pair owned elsewhere
+}
+
+__global__ __launch_bounds__(64) void count_kernel(const int32_t *__restrict__ ids, int64_t npairs,
+                                                   int e0, int El, int32_t *__restrict__ chunk_cnt)
+{
+    extern __shared__ int32_t hist[];
+    const int lane = threadIdx.x;
+    const int64_t c = blockIdx.x;
+    for (int i = lane; i < El; i += 64) hist[i] = 0;
+    __syncthreads();
+    const int64_t base = c * CHUNK;
+    int32_t v[ROUNDS];
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r) {
+        int64_t p = base + r * 64 + lane;
+        v[r] = p < npairs ? ids[p] : -1;
+    }
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r) {
+        int le = local_index(v[r], e0, El);
+        if (le < El) atomicAdd(&hist[le], 1);
+    }
+    __syncthreads();
+    for (int i = lane; i < El; i += 64) chunk_cnt[c * El + i] = hist[i];
+}
+
+// One block of 1024 threads.  chunk_cnt [nchunks, El] is rewritten in place
+// with each (chunk, expert)'s first output row.
+__global__ __launch_bounds__(1024) void scan_kernel(int32_t *__restrict__ chunk_cnt, int64_t nchunks,
+                                                    int El, int32_t *__restrict__ counts,
+                                                    int32_t *__restrict__ offsets)
+{
+    __shared__ int32_t tot[1024];
+    __shared__ int32_t wsum[16];
+    const int e = threadIdx.x;
+    int32_t run = 0;
+    if (e < El) {
+        for (int64_t c = 0; c < nchunks; ++c) {
+            int32_t v = chunk_cnt[c * El + e];
+            chunk_cnt[c * El + e] = run;
+            run += v;
+        }
+        counts[e] = run;
+    }
+    // exclusive scan of the per-expert totals over e (block-wide)
+    const int lane = e & 63, wv = e >> 6;
+    int32_t incl = run;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        int32_t o = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += o;
+    }
+    if (lane == 63) wsum[wv] = incl;
+    __syncthreads();
+    int32_t before = 0;
+    for (int i = 0; i < wv; ++i) before += wsum[i];
+    int32_t excl = before + incl - run;
+    tot[e] = excl;
+    if (e < El) offsets[e] = excl;
+    if (e == 1023) offsets[El] = before + incl;  // total over all experts
+    __syncthreads();
+    if (e < El) {
+        for (int64_t c = 0; c < nchunks; ++c) chunk_cnt[c * El + e] += tot[e];
+    }
+}
+
+__global__ __launch_bounds__(64) void scatter_kernel(const int32_t *__restrict__ ids, int64_t npairs,
+                                                     int e0, int El, int nbits,
+                                                     const int32_t *__restrict__ chunk_base,
+                                                     int32_t *__restrict__ row_to_pair,
+                                                     int32_t *__restrict__ pair_to_row)
+{
+    extern __shared__ int32_t next_row[];
+    const int lane = threadIdx.x;
+    const int64_t c = blockIdx.x;
+    for (int i = lane; i < El; i += 64) next_row[i] = chunk_base[c * El + i];
+    const int64_t base = c * CHUNK;
+    int32_t v[ROUNDS];
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r) {
+        int64_t p = base + r * 64 + lane;
+        v[r] = p < npairs ? ids[p] : -1;
+    }
+    __syncthreads();
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    for (int r = 0; r < ROUNDS; ++r) {
+        const int64_t p = base + r * 64 + lane;
+        const bool valid = p < npairs;
+        const int le = valid ? local_index(v[r], e0, El) : El + 1;
+        uint64_t peers = ~0ull;
+        for (int b = 0; b < nbits; ++b) {
+            const bool bit = (le >> b) & 1;
+            const uint64_t bal = __ballot(bit);
+            peers &= bit ? bal : ~bal;
+        }
+        const int rank = __popcll(peers & below);
+        if (le < El) {
+            const int32_t row = next_row[le] + rank;
+            row_to_pair[row] = (int32_t)p;
+            pair_to_row[p] = row;
+        } else if (valid) {
+            pair_to_row[p] = -1;
+        }
+        __syncthreads();
+        if (le < El && rank == 0) next_row[le] += __popcll(peers);
+        __syncthreads();
+    }
+}
+
+__global__ __launch_bounds__(256) void gather_kernel(const uint16_t *__restrict__ x, int H, int k,
+                                                     const int32_t *__restrict__ row_to_pair,
+                                                     const int32_t *__restrict__ offsets, int El,
+                                                     int64_t cap, uint16_t *__restrict__ x_perm)
+{
+    int64_t n = offsets[El];
+    if (n > cap) n = cap;
+    const int vecs = H / 8;
+    for (int64_t r = blockIdx.x; r < n; r += gridDim.x) {
+        const int64_t t = row_to_pair[r] / k;
+        const uint4 *src = reinterpret_cast<const uint4 *>(x + t * H);
+        uint4 *dst = reinterpret_cast<uint4 *>(x_perm + r * H);
+        for (int i = threadIdx.x; i < vecs; i += 256) dst[i] = src[i];
+    }
+}
+
+}  // namespace
+
+int64_t permute_chunks(int64_t T, int k) { return ceil_div(T * k, CHUNK); }
+
+hipError_t launch_permute(const int32_t *ids, int64_t T, int k, int e0, int El, int32_t *counts,
+                          int32_t *offsets, int32_t *row_to_pair, int32_t *pair_to_row,
+                          const uint16_t *x, int H, uint16_t *x_perm, int64_t cap, int32_t *ws,
+                          hipStream_t s)
+{
+    const int64_t npairs = T * k;
+    const int64_t nchunks = permute_chunks(T, k);
+    int nbits = 0;
+    while ((1 << nbits) < El + 2) ++nbits;  // distinguishes 0..El+1
+    hipError_t err;
+    {
+        KernelTimer timer(MOE_K_PERMUTE, s);
+        if (nchunks > 0) {
+            count_kernel<<<dim3((unsigned)nchunks), dim3(64), El * sizeof(int32_t), s>>>(
+                ids, npairs, e0, El, ws);
+            if ((err = hipGetLastError()) != hipSuccess) return err;
+        }
+        scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(ws, nchunks, El, counts, offsets);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+        if (nchunks > 0) {
+            scatter_kernel<<<dim3((unsigned)nchunks), dim3(64), El * sizeof(int32_t), s>>>(
+                ids, npairs, e0, El, nbits, ws, row_to_pair, pair_to_row);
+            if ((err = hipGetLastError()) != hipSuccess) return err;
+        }
+    }
+    if (x_perm != nullptr && cap > 0) {
+        KernelTimer timer(MOE_K_GATHER, s);
+        int64_t blocks = cap < 4096 ? cap : 4096;
+        gather_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(x, H, k, row_to_pair, offsets, El,
+                                                                   cap, x_perm);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+    }
+    return hipSuccess;
+}
+
+}  // namespace moe

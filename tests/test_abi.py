@@ -1,0 +1,120 @@
+"""The C ABI without a GPU: the library loads, exports every symbol that
+include/libmoe.h declares, sizes workspaces, and rejects bad arguments on the
+host before any HIP call (so these run on a machine with no GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_26607_amd as moe
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "libmoe.h")
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
+FAKE = ctypes.c_void_p(0x100000)  # never dereferenced: every call below fails validation
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = moe.lib()
+    names = declared_functions()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(L, n), f"missing export {n}"
+
+
+def test_status_strings_and_version():
+    L = moe.lib()
+    assert L.moe_version() >= 1
+    for s, name in [(0, b"MOE_OK"), (1, b"MOE_ERR_INVALID_ARG"), (2, b"MOE_ERR_UNSUPPORTED"),
+                    (3, b"MOE_ERR_WORKSPACE"), (4, b"MOE_ERR_HIP")]:
+        assert L.moe_status_str(s) == name
+
+
+def test_workspace_sizes():
+    assert moe.permute_workspace_size(4096, 2, 8) >= (4096 * 2 // 1024 + 1) * 8 * 4
+    assert moe.permute_workspace_size(-1, 2, 8) == 0
+    assert moe.ffn_workspace_size(8192, 8, 4096, 1792) >= 8192 * 1792 * 2
+    assert moe.ffn_workspace_size(8192, 0, 4096, 1792) == 0
+
+
+@pytest.mark.parametrize("T,E,k,st", [(4, 8, 0, INVALID), (4, 8, 9, INVALID), (4, 0, 1, INVALID),
+                                      (-1, 8, 2, INVALID), (4, 2048, 2, UNSUPPORTED),
+                                      (4, 64, 17, UNSUPPORTED), (1 << 29, 64, 8, UNSUPPORTED)])
+def test_route_rejects(T, E, k, st):
+    L = moe.lib()
+    assert L.moe_route(FAKE, T, E, k, FAKE, FAKE, None) == st
+    assert L.moe_last_error()
+
+
+def test_route_null_pointers():
+    assert moe.lib().moe_route(None, 4, 8, 2, FAKE, FAKE, None) == INVALID
+
+
+def test_permute_rejects():
+    L = moe.lib()
+    big = 1 << 20
+    args = dict(ids=FAKE, T=16, k=2, E=8, e0=0, El=8, counts=FAKE, offsets=FAKE, r2p=FAKE, p2r=FAKE,
+                x=FAKE, H=64, xp=FAKE, ws=FAKE, wsb=big)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return L.moe_permute(a["ids"], a["T"], a["k"], a["E"], a["e0"], a["El"], a["counts"],
+                             a["offsets"], a["r2p"], a["p2r"], a["x"], a["H"], a["xp"], a["ws"],
+                             a["wsb"], None)
+    assert call(e0=4, El=8) == INVALID          # local range past E
+    assert call(El=0) == INVALID
+    assert call(e0=-1) == INVALID
+    assert call(counts=None) == INVALID
+    assert call(ids=None) == INVALID
+    assert call(H=60) == UNSUPPORTED           # not a multiple of 8
+    assert call(x=None) == INVALID             # x_perm without x
+    assert call(ws=None) == WORKSPACE
+    assert call(wsb=16) == WORKSPACE
+    assert call(k=17, E=32) == UNSUPPORTED
+
+
+def test_ffn_rejects():
+    L = moe.lib()
+    big = 1 << 30
+
+    def call(xp=FAKE, off=FAKE, El=8, cap=64, H=64, Is=32, w13=FAKE, w2=FAKE, y=FAKE, ws=FAKE, wsb=big):
+        return L.moe_grouped_ffn(xp, off, El, cap, H, Is, w13, w2, y, ws, wsb, None)
+    assert call(El=0) == INVALID
+    assert call(El=1025) == UNSUPPORTED
+    assert call(H=12) == UNSUPPORTED
+    assert call(Is=0) == INVALID
+    assert call(cap=-1) == INVALID
+    assert call(off=None) == INVALID
+    assert call(w2=None) == INVALID
+    assert call(wsb=100) == WORKSPACE
+    assert call(ws=ctypes.c_void_p(0x100010)) == WORKSPACE   # not 256-byte aligned
+    assert call(xp=ctypes.c_void_p(0x100002)) == INVALID     # not 16-byte aligned
+
+
+def test_combine_rejects():
+    L = moe.lib()
+
+    def call(y=FAKE, yr=8, p2r=FAKE, w=FAKE, T=4, k=2, H=64, sy=None, sb=0, sc=0, acc=0, out=FAKE):
+        return L.moe_combine(y, yr, p2r, w, T, k, H, sy, sb, sc, acc, out, None)
+    assert call(k=0) == INVALID
+    assert call(k=17) == UNSUPPORTED
+    assert call(H=63) == UNSUPPORTED
+    assert call(out=None) == INVALID
+    assert call(y=None) == INVALID
+    assert call(sy=FAKE, sb=3, sc=2) == INVALID   # shared rows past T
+    assert call(T=-1) == INVALID
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    from paper_2606_26607_amd import binding
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        binding.lib()

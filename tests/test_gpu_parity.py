@@ -1,0 +1,279 @@
+"""GPU path vs the CPU oracle, through the C ABI (needs an MI355X).
+
+Routing ids, counts, offsets and permutation indices must match bit for
+bit; gate weights within 1e-6; layer and stage outputs within
+max|err| <= 2e-2 * max|ref|.  Full-size workloads compare every integer
+output and a sample of output rows that the oracle evaluates one by one.
+"""
+import numpy as np
+import pytest
+import torch
+
+import moe_inputs as mi
+import paper_2606_26607_amd as moe
+from tests.util import W_ATOL, assert_close_rel, bf16_f64, dev_bf16, host_bf16
+
+pytestmark = pytest.mark.gpu
+
+SEEDS = (0, 1, 2)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    moe.lib()
+
+
+def gpu_route(logits: np.ndarray, k: int):
+    ids, w = moe.route(torch.from_numpy(logits).cuda(), k)
+    torch.cuda.synchronize()
+    return ids.cpu().numpy(), w.cpu().numpy()
+
+
+def gpu_permute(ids: np.ndarray, E: int, e0: int, El: int, x: np.ndarray = None):
+    o = moe.permute(torch.from_numpy(ids).cuda(), E, e0, El,
+                    x=dev_bf16(x) if x is not None else None)
+    torch.cuda.synchronize()
+    T, k = ids.shape
+    n = int(o["offsets"][-1].item())
+    res = dict(counts=o["counts"].cpu().numpy(), offsets=o["offsets"].cpu().numpy(),
+               row_to_pair=o["row_to_pair"].cpu().numpy()[:n],
+               pair_to_row=o["pair_to_row"].cpu().numpy()[:T * k])
+    if x is not None:
+        res["x_perm"] = host_bf16(o["x_perm"])[:n]
+    return res
+
+
+# ------------------------------------------------------------------ route
+@pytest.mark.parametrize("name", list(mi.CONFIGS))
+@pytest.mark.parametrize("seed", SEEDS)
+def test_route_configs(oracle, name, seed):
+    cfg = mi.CONFIGS[name].with_(seed=mi.CONFIGS[name].seed + seed)
+    inp = mi.make_inputs(cfg, with_weights=False)
+    ids, w = gpu_route(inp.logits, cfg.k)
+    rid, rw = oracle.route(inp.logits, cfg.k)
+    np.testing.assert_array_equal(ids, rid)
+    assert np.abs(w - rw).max() <= W_ATOL
+    assert np.abs(w.sum(1) - 1).max() <= 1e-6
+
+
+@pytest.mark.parametrize("T,E,k", [(1, 1, 1), (3, 8, 8), (257, 16, 4), (100, 33, 5), (64, 64, 16),
+                                   (1000, 128, 8), (513, 256, 8), (77, 1000, 16), (64, 1024, 16),
+                                   (40000, 8, 2)])
+def test_route_ties_and_signed_zeros(oracle, T, E, k):
+    g = np.random.default_rng(T * 7 + E)
+    lg = g.integers(-2, 3, (T, E)).astype(np.float32)
+    z = lg == 0
+    lg[z] = np.where(g.random(z.sum()) < 0.5, -0.0, 0.0)
+    ids, w = gpu_route(lg, k)
+    rid, rw = oracle.route(lg, k)
+    np.testing.assert_array_equal(ids, rid)
+    assert np.abs(w - rw).max() <= W_ATOL
+
+
+def test_route_extreme_logits(oracle):
+    g = np.random.default_rng(9)
+    lg = (g.standard_normal((300, 64)) * 40).astype(np.float32)
+    lg[5] = 0.0
+    lg[6] = -1e30
+    lg[7, 3] = 1e30
+    ids, w = gpu_route(lg, 8)
+    rid, rw = oracle.route(lg, 8)
+    np.testing.assert_array_equal(ids, rid)
+    assert np.abs(w - rw).max() <= W_ATOL
+
+
+def test_route_empty_batch():
+    ids, w = moe.route(torch.empty((0, 8), dtype=torch.float32, device="cuda"), 2)
+    torch.cuda.synchronize()
+    assert ids.shape == (0, 2)
+
+
+# ---------------------------------------------------------------- permute
+@pytest.mark.parametrize("name", list(mi.CONFIGS))
+def test_permute_configs(oracle, name):
+    cfg = mi.CONFIGS[name]
+    inp = mi.make_inputs(cfg, with_weights=False)
+    rid, _ = oracle.route(inp.logits, cfg.k)
+    got = gpu_permute(rid, cfg.E, cfg.e0, cfg.E_l, inp.x)
+    c, o, r2p, p2r = oracle.permute(rid, cfg.e0, cfg.E_l)
+    np.testing.assert_array_equal(got["counts"], c)
+    np.testing.assert_array_equal(got["offsets"], o)
+    np.testing.assert_array_equal(got["row_to_pair"], r2p)
+    np.testing.assert_array_equal(got["pair_to_row"], p2r)
+    np.testing.assert_array_equal(got["x_perm"], inp.x[r2p // cfg.k])
+
+
+@pytest.mark.parametrize("T,E,k,P", [(1, 8, 2, 1), (1, 8, 2, 8), (1023, 8, 2, 2), (1025, 64, 8, 8),
+                                     (5000, 128, 8, 8), (3000, 1024, 16, 4), (2048, 16, 1, 1),
+                                     (70000, 8, 2, 8)])
+def test_permute_every_rank(oracle, T, E, k, P):
+    ids = mi.random_topk_ids(T, E, k, seed=T + E + k)
+    total = 0
+    for r in range(P):
+        e0, El = r * (E // P), E // P
+        got = gpu_permute(ids, E, e0, El)
+        c, o, r2p, p2r = oracle.permute(ids, e0, El)
+        np.testing.assert_array_equal(got["counts"], c)
+        np.testing.assert_array_equal(got["offsets"], o)
+        np.testing.assert_array_equal(got["row_to_pair"], r2p)
+        np.testing.assert_array_equal(got["pair_to_row"], p2r)
+        total += int(o[-1])
+    assert total == T * k
+
+
+def test_permute_hot_expert_and_empty_experts(oracle):
+    T, E, k = 4099, 16, 4
+    ids = mi.random_topk_ids(T, E, k, seed=5, hot=7)
+    x = mi.random_bf16((T, 64), seed=5)
+    got = gpu_permute(ids, E, 4, 8, x)
+    c, o, r2p, p2r = oracle.permute(ids, 4, 8)
+    assert c[3] == T
+    np.testing.assert_array_equal(got["offsets"], o)
+    np.testing.assert_array_equal(got["row_to_pair"], r2p)
+    np.testing.assert_array_equal(got["pair_to_row"], p2r)
+    np.testing.assert_array_equal(got["x_perm"], x[r2p // k])
+    # a rank none of whose experts are chosen
+    ids0 = np.zeros((300, 1), np.int32)
+    got = gpu_permute(ids0, 16, 8, 8)
+    assert np.all(got["counts"] == 0) and np.all(got["offsets"] == 0)
+    assert np.all(got["pair_to_row"] == -1)
+
+
+def test_permute_empty_batch():
+    o = moe.permute(torch.empty((0, 2), dtype=torch.int32, device="cuda"), 8, 0, 8)
+    torch.cuda.synchronize()
+    assert np.all(o["offsets"].cpu().numpy() == 0) and np.all(o["counts"].cpu().numpy() == 0)
+
+
+# -------------------------------------------------------------- grouped FFN
+def ffn_case(oracle, El, H, Is, T, k, seed, hot=None):
+    E = El
+    ids = mi.random_topk_ids(T, E, k, seed=seed, hot=hot)
+    _, offs, r2p, _ = oracle.permute(ids, 0, El)
+    n = int(offs[-1])
+    x_perm = mi.random_bf16((n, H), seed=seed, tag=41)
+    w13 = mi.random_bf16((El, 2 * Is, H), seed=seed, tag=42, std=0.05)
+    w2 = mi.random_bf16((El, H, Is), seed=seed, tag=43, std=0.05)
+    y = moe.grouped_ffn(dev_bf16(x_perm), torch.from_numpy(offs).cuda(), dev_bf16(w13), dev_bf16(w2))
+    torch.cuda.synchronize()
+    got = bf16_f64(host_bf16(y)[:n])
+    ref = oracle.grouped_ffn(x_perm, offs, w13, w2)
+    return got, ref
+
+
+@pytest.mark.parametrize("El,H,Is,T,k", [(1, 64, 32, 1, 1), (4, 256, 192, 150, 2), (8, 136, 72, 99, 3),
+                                         (3, 512, 256, 300, 1), (16, 128, 64, 400, 4),
+                                         (2, 1024, 512, 130, 2)])
+def test_grouped_ffn_stage(oracle, El, H, Is, T, k):
+    got, ref = ffn_case(oracle, El, H, Is, T, k, seed=El * 100 + H)
+    assert_close_rel(got, ref, what=f"ffn El={El} H={H} Is={Is}")
+
+
+def test_grouped_ffn_skewed_and_empty_experts(oracle):
+    got, ref = ffn_case(oracle, 8, 256, 128, 700, 2, seed=3, hot=5)
+    assert_close_rel(got, ref, what="skewed")
+
+
+def test_grouped_ffn_all_rows_empty():
+    El, H, Is = 4, 64, 32
+    offs = torch.zeros(El + 1, dtype=torch.int32, device="cuda")
+    y = torch.full((16, H), 3.0, dtype=torch.bfloat16, device="cuda")
+    w13 = torch.zeros((El, 2 * Is, H), dtype=torch.bfloat16, device="cuda")
+    w2 = torch.zeros((El, H, Is), dtype=torch.bfloat16, device="cuda")
+    moe.grouped_ffn(torch.zeros((16, H), dtype=torch.bfloat16, device="cuda"), offs, w13, w2, y=y)
+    torch.cuda.synchronize()
+    assert torch.all(y == 3.0)   # rows past offsets[El] untouched
+
+
+# ------------------------------------------------------------------ combine
+@pytest.mark.parametrize("T,k,H,El,E,acc,shared", [(37, 2, 64, 8, 8, 0, False), (200, 8, 7168, 32, 256, 0, True),
+                                                   (100, 4, 256, 2, 8, 1, False), (1, 1, 8, 1, 1, 0, False),
+                                                   (513, 16, 520, 64, 128, 1, True)])
+def test_combine_stage(oracle, T, k, H, El, E, acc, shared):
+    ids = mi.random_topk_ids(T, E, k, seed=T + k)
+    _, offs, r2p, p2r = oracle.permute(ids, 0, El)
+    n = int(offs[-1])
+    y = mi.random_bf16((max(n, 1), H), seed=T)
+    w = mi.random_gate_weights(T, k, seed=T)
+    prior = mi.random_bf16((T, H), seed=T + 1)
+    sb, sc = (T // 4, T // 3) if shared else (0, 0)
+    sy = mi.random_bf16((max(sc, 1), H), seed=T + 2) if shared else None
+    out = dev_bf16(prior)
+    moe.combine(dev_bf16(y), torch.from_numpy(p2r).cuda(), torch.from_numpy(w).cuda(), out=out,
+                shared_y=dev_bf16(sy[:sc]) if shared else None, shared_begin=sb, accumulate=bool(acc))
+    torch.cuda.synchronize()
+    ref = oracle.combine(y, p2r, w, T, k, shared_y=sy, sb=sb, sc=sc, accumulate=acc, prior=prior)
+    assert_close_rel(bf16_f64(host_bf16(out)), ref, rtol=1e-2, what="combine")
+
+
+# -------------------------------------------------------------- full layer
+def layer_on_gpu(inp: mi.MoeInputs):
+    cfg = inp.cfg
+    sw13 = dev_bf16(inp.sw13) if cfg.shared else None
+    sw2 = dev_bf16(inp.sw2) if cfg.shared else None
+    layer = moe.MoeLayer(cfg.T, cfg.E, cfg.k, cfg.e0, dev_bf16(inp.w13), dev_bf16(inp.w2), sw13, sw2,
+                         cfg.shared_begin, cfg.shared_count)
+    out = layer.forward(dev_bf16(inp.x), torch.from_numpy(inp.logits).cuda())
+    torch.cuda.synchronize()
+    return layer, host_bf16(out)
+
+
+def sample_tokens(cfg, ids, n=24, seed=0):
+    """Tokens to check at full size: random ones, plus (EP) tokens with no
+    local pair, the first and last token, and shared-expert rows."""
+    g = np.random.default_rng(seed)
+    picks = set(g.choice(cfg.T, size=min(n, cfg.T), replace=False).tolist()) | {0, cfg.T - 1}
+    local = ((ids >= cfg.e0) & (ids < cfg.e0 + cfg.E_l)).any(1)
+    none = np.nonzero(~local)[0]
+    if none.size:
+        picks |= set(none[:3].tolist())
+    if cfg.shared:
+        picks |= {cfg.shared_begin, cfg.shared_begin + cfg.shared_count - 1, cfg.shared_count}
+    return np.array(sorted(picks), np.int64)
+
+
+@pytest.mark.parametrize("name", list(mi.CONFIGS))
+def test_layer_configs(oracle, name):
+    cfg = mi.CONFIGS[name]
+    inp = mi.make_inputs(cfg)
+    layer, out = layer_on_gpu(inp)
+    rid, rw = oracle.route(inp.logits, cfg.k)
+    np.testing.assert_array_equal(layer.topk_ids.cpu().numpy(), rid)
+    assert np.abs(layer.topk_w.cpu().numpy() - rw).max() <= W_ATOL
+    c, o, r2p, p2r = oracle.permute(rid, cfg.e0, cfg.E_l)
+    np.testing.assert_array_equal(layer.bufs["offsets"].cpu().numpy(), o)
+    np.testing.assert_array_equal(layer.bufs["row_to_pair"].cpu().numpy()[:o[-1]], r2p)
+    np.testing.assert_array_equal(layer.bufs["pair_to_row"].cpu().numpy()[:cfg.T * cfg.k], p2r)
+    toks = np.arange(cfg.T) if cfg.T * cfg.k * cfg.H * cfg.I_s <= 64 * 2 * 256 * 512 else \
+        sample_tokens(cfg, rid)
+    ref = oracle.layer_tokens(inp.x, rid, rw, cfg.e0, cfg.E_l, inp.w13, inp.w2, toks, inp.sw13,
+                              inp.sw2, cfg.shared_begin, cfg.shared_count)
+    assert_close_rel(bf16_f64(out[toks]), ref, what=name)
+    # tokens with no local pair and no shared term are exactly zero
+    local = ((rid >= cfg.e0) & (rid < cfg.e0 + cfg.E_l)).any(1)
+    if cfg.shared:
+        local[cfg.shared_begin:cfg.shared_begin + cfg.shared_count] = True
+    assert np.all(out[~local] == 0)
+
+
+@pytest.mark.parametrize("layout,P", [("tp", 4), ("ep", 4)])
+def test_layer_slices_sum_to_unsliced(oracle, layout, P):
+    base = mi.MoeConfig("small", T=130, H=256, E=8, k=2, I=512, seed=77)
+    ref = oracle.layer(mi.make_inputs(base))
+    acc = np.zeros_like(ref)
+    for r in range(P):
+        _, out = layer_on_gpu(mi.make_inputs(base.with_(P=P, layout=layout, rank=r)))
+        acc += bf16_f64(out)
+    assert_close_rel(acc, ref, what=f"{layout} partial sum")
+
+
+def test_layer_is_deterministic():
+    inp = mi.make_inputs(mi.CONFIGS["c4"].with_(T=2048))
+    layer, out1 = layer_on_gpu(inp)
+    y1 = host_bf16(layer.y).copy()
+    out2 = host_bf16(layer.forward(dev_bf16(inp.x), torch.from_numpy(inp.logits).cuda()))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(out1, out2)
+    np.testing.assert_array_equal(y1, host_bf16(layer.y))
