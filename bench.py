@@ -1,0 +1,219 @@
+"""Benchmark: one GPU's share of the MoE layer forward (libmoe on MI355X).
+
+A step is the whole hot path over one batch: route -> permute (with the row
+gather) -> grouped SwiGLU FFN (+ the shared expert where the layer has one)
+-> combine.  Inputs (tokens, router logits, expert weights) are resident in
+HBM before the timed region starts.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c2]
+
+Prints ONE JSON line on stdout; details go to stderr.  The default workload
+is the Mixtral-shaped TP=8 slice (4096 tokens, hidden 4096, 8 experts,
+top-2, intermediate 14336 sliced to 1792).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MoE-layer tokens/s per GPU + % bf16 MFMA peak (prefill) / % HBM BW (decode)"
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_work(cfg, counts: np.ndarray):
+    """Flops and bytes the method must move for this step (no tile padding,
+    only experts with rows have their weights read)."""
+    H, Is = cfg.H, cfg.I_s
+    n = int(counts.sum())
+    active = int((counts > 0).sum())
+    sc = cfg.shared_count
+    gate_up_flops = 4.0 * H * Is * n
+    down_flops = 2.0 * H * Is * n
+    gate_up_bytes = active * 2 * Is * H * 2 + n * H * 2 + n * Is * 2
+    down_bytes = active * H * Is * 2 + n * Is * 2 + n * H * 2
+    sh_flops = 6.0 * H * cfg.I * sc
+    sh_bytes = (3 * cfg.I * H * 2 + sc * H * 4 + sc * cfg.I * 4) if sc else 0
+    touched = n  # x rows read once per routed pair by the gather, out written once per token
+    step_bytes = (active * 3 * Is * H * 2 + (touched + cfg.T) * H * 2 + sh_bytes)
+    return dict(n=n, active=active, gate_up_flops=gate_up_flops, down_flops=down_flops,
+                gate_up_bytes=gate_up_bytes, down_bytes=down_bytes,
+                flops=gate_up_flops + down_flops + sh_flops, bytes=step_bytes)
+
+
+def cpu_baseline(inp, target_s: float):
+    """The CPU oracle, timed on a bounded sample of the workload's tokens
+    (routing, permutation, expert FFNs and combine for those tokens)."""
+    from oracle import Oracle, build
+    build()
+    orc = Oracle()
+    cfg = inp.cfg
+    g = np.random.default_rng(123)
+    # calibrate on a few tokens, then size the sample to ~target_s
+    probe = np.sort(g.choice(cfg.T, size=min(8, cfg.T), replace=False)).astype(np.int64)
+
+    t0 = time.perf_counter()
+    ids, w = orc.route(inp.logits, cfg.k)
+    orc.permute(ids, cfg.e0, cfg.E_l)
+    t_rp = time.perf_counter() - t0   # routing + permutation of all T tokens
+
+    def run(tokens):
+        t0 = time.perf_counter()
+        orc.layer_tokens(inp.x, ids, w, cfg.e0, cfg.E_l, inp.w13, inp.w2, tokens, inp.sw13,
+                         inp.sw2, cfg.shared_begin, cfg.shared_count)
+        return time.perf_counter() - t0 + t_rp * len(tokens) / cfg.T
+    dt = run(probe)
+    per_tok = max(dt / len(probe), 1e-6)
+    S = int(min(cfg.T, max(8, target_s / per_tok)))
+    sample = np.sort(g.choice(cfg.T, size=S, replace=False)).astype(np.int64)
+    dt = run(sample)
+    return dict(value=S / (cfg.P * dt), unit="tokens/s", cores=orc.threads(), kind="oracle",
+                sample=f"{S} of {cfg.T} tokens: expert FFNs + combine for those tokens, plus "
+                       f"routing+permutation of all tokens scaled by {S}/{cfg.T}; fp64; {dt:.1f} s", seconds=dt, slice_tokens_per_s=S / dt)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="c2")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--graph", action="store_true", help="replay the step from a HIP graph")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU's share of the layer; --gpus {args.gpus} is not "
+              "supported (the multi-GPU collectives are outside this build)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import moe_inputs as mi
+    import paper_2606_26607_amd as moe
+
+    assert torch.cuda.is_available(), "bench needs a GPU"
+    cfg = mi.CONFIGS[args.config]
+    cfg = cfg.with_(seed=cfg.seed + args.seed)
+    t0 = time.time()
+    inp = mi.make_inputs(cfg)
+    log(f"[bench] inputs for {cfg.name} in {time.time() - t0:.1f}s")
+    dev = torch.device("cuda:0")
+
+    def up(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+    x = up(inp.x)
+    logits = torch.from_numpy(inp.logits).to(dev)
+    layer = moe.MoeLayer(cfg.T, cfg.E, cfg.k, cfg.e0, up(inp.w13), up(inp.w2),
+                         up(inp.sw13) if cfg.shared else None, up(inp.sw2) if cfg.shared else None,
+                         cfg.shared_begin, cfg.shared_count)
+    for _ in range(args.warmup):
+        layer.forward(x, logits)
+    torch.cuda.synchronize()
+    counts = layer.bufs["counts"].cpu().numpy()
+    work = algorithmic_work(cfg, counts)
+
+    step = lambda: layer.forward(x, logits)  # noqa: E731
+    graph = None
+    if args.graph:
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            step()
+        torch.cuda.current_stream().wait_stream(s)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        step = graph.replay
+        for _ in range(args.warmup):
+            step()
+
+    # timed region: K steps, per-kernel HIP events recorded by the library
+    moe.timing_reset()
+    moe.timing_enable(not args.graph)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    moe.timing_enable(False)
+    ms_per_step = elapsed * 1e3 / args.steps
+
+    kern = {}
+    for kind in moe.binding.KERNEL_KINDS:
+        ms, n = moe.timing_read(kind)
+        if n:
+            kern[kind] = dict(avg_us=1e3 * ms / n, launches=n)
+    log("[bench] kernels: " + ", ".join(f"{k}={v['avg_us']:.1f}us x{v['launches']}" for k, v in kern.items()))
+
+    decode = cfg.name.startswith("dsv3")
+    # dominant kernel: the gate-up GEMM (2/3 of the flops and of the weight bytes)
+    gu = kern.get("gate_up")
+    if gu is not None:
+        per_launch = gu["launches"] // args.steps or 1
+        dur_s = gu["avg_us"] * 1e-6 * per_launch
+        if decode:
+            achieved = work["gate_up_bytes"] / dur_s / 1e9
+            roof = dict(bound="hbm", achieved=achieved, peak=PEAK_HBM_GBS, unit="GB/s",
+                        frac=achieved / PEAK_HBM_GBS, traffic=None, kernel="gate_up",
+                        algorithmic_per_launch=work["gate_up_bytes"])
+        else:
+            achieved = work["gate_up_flops"] / dur_s / 1e12
+            roof = dict(bound="mfma", achieved=achieved, peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                        frac=achieved / PEAK_BF16_TFLOPS, traffic=None, kernel="gate_up",
+                        algorithmic_per_launch=work["gate_up_flops"])
+    else:
+        roof = None
+
+    step_s = ms_per_step * 1e-3
+    result = {
+        "metric": METRIC,
+        "value": cfg.T / (cfg.P * step_s),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "T": cfg.T, "H": cfg.H, "E": cfg.E, "k": cfg.k,
+                   "I": cfg.I, "I_s": cfg.I_s, "P": cfg.P, "layout": cfg.layout, "rank": cfg.rank,
+                   "local_experts": cfg.E_l, "local_pairs": work["n"], "active_experts": work["active"],
+                   "shared_expert": cfg.shared, "global_batch": cfg.T, "parallelism": "single-gpu-slice",
+                   "graph": bool(args.graph), "seed": cfg.seed},
+        "slice_tokens_per_s": cfg.T / step_s,
+        "chain_tflops": work["flops"] / step_s / 1e12,
+        "chain_frac_mfma": work["flops"] / step_s / 1e12 / PEAK_BF16_TFLOPS,
+        "chain_gbs": work["bytes"] / step_s / 1e9,
+        "chain_frac_hbm": work["bytes"] / step_s / 1e9 / PEAK_HBM_GBS,
+        "kernels_us": {k: round(v["avg_us"], 2) for k, v in kern.items()},
+        "roofline": roof,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu:
+        cb = cpu_baseline(inp, args.cpu_seconds)
+        log(f"[bench] cpu oracle: {cb['sample']} on {cb['cores']} threads ({platform.processor() or 'cpu'})")
+        result["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -15,8 +15,8 @@
 namespace moe {
 namespace {
 
-constexpr int BM = 64, BN = 64, BK = 64;
-constexpr int KCH = BK / 8;  // 16-byte chunks per tile row
+constexpr int BM = 64, BN = 64, BK = 64;  // the general kernel (any K multiple of 8)
+constexpr int KCH = BK / 8;               // 16-byte chunks per tile row
 
 __device__ __forceinline__ int64_t clamp_row(int32_t v, int64_t cap)
 {
@@ -136,6 +136,367 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t *__restrict__ 
     }
 }
 
+
+// ---------------------------------------------------------------------------
+// Large-tile kernel (K a multiple of 32): BMxBN tiles (BN counts weight rows;
+// a gated tile holds BN/2 gate rows and the BN/2 matching up rows), 4 waves
+// in a 2x2 grid, each wave (BM/2)x(BN/2) of 32x32x16 MFMA blocks.
+//
+// Operands move L2 -> LDS with buffer loads that write LDS directly (no VGPR
+// staging) into a ring of NSTAGE slices of BK=32 (all 160 KB of LDS), so
+// NSTAGE-1 slices are in flight while one is consumed: the feed is latency
+// bound otherwise.  Buffer range checking returns zeros for rows past the
+// expert's last row or past N.  Within a slice the fragments of k-step 1 are
+// read while the MFMAs of k-step 0 run; the workgroup barrier that hands over
+// to the next slice sits between the two k-steps, so the next slice's first
+// fragments are also read under MFMAs.  LDS rows are 64 bytes; 16-byte chunk
+// c of row r sits at c ^ swz(r), so each 16-row (and 8-row) group read by one
+// ds_read_b128 covers distinct banks.  The epilogue stages the bf16 tile in
+// LDS and writes it with coalesced 16-byte stores.
+// ---------------------------------------------------------------------------
+constexpr int BIG_BK = 32;   // K per slice
+constexpr int NSTAGE = 5;    // ring slices
+constexpr int CPR = BIG_BK / 8;   // 16-byte chunks per LDS row
+constexpr int RPI = 64 / CPR;     // rows per DMA instruction
+
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+
+// Workgroup barrier without the memory fence of __syncthreads(): that fence
+// would also wait for the slices still in flight.  The ordering the ring
+// needs is explicit: each wave waits (vmcnt) for its own loads of a slice to
+// land in LDS, and (lgkmcnt) for its own reads of a slot, before the barrier
+// that publishes the slice or frees the slot.
+__device__ __forceinline__ void lds_barrier()
+{
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// Wait until at most `n` (a multiple of `ins`, below 4*ins) DMA instructions
+// of this wave are outstanding.
+template <int INS>
+__device__ __forceinline__ void wait_dma(int n_slices)
+{
+    static_assert(3 * INS < 64, "vmcnt range");
+    if (n_slices >= 3) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(3 * INS) : "memory");
+    else if (n_slices == 2) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(2 * INS) : "memory");
+    else if (n_slices == 1) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(INS) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+}
+
+// Raw buffer descriptor: base, no stride, num_records bytes (reads past it
+// return zero), default data format for untyped loads.
+__device__ __forceinline__ i32x4_t buffer_desc(const void *base, int64_t bytes)
+{
+    const uint64_t b = reinterpret_cast<uint64_t>(base);
+    i32x4_t d;
+    d.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)b);
+    d.y = __builtin_amdgcn_readfirstlane((int)(uint32_t)((b >> 32) & 0xffffu));
+    d.z = __builtin_amdgcn_readfirstlane((int)bytes);
+    d.w = 0x00020000;
+    return d;
+}
+
+// 16 bytes per lane from global memory straight into LDS: lane i's data lands
+// at LDS byte address lds + 16*i.  Written as inline asm so that the
+// compiler does not track it as a pending LDS write (it would otherwise wait
+// for every such load before any LDS read); the ring waits explicitly.
+__device__ __forceinline__ void dma16(i32x4_t desc, uint32_t lds, uint32_t voff, uint32_t soff)
+{
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :: "s"(lds), "v"(voff), "s"(desc), "s"(soff) : "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void *p)
+{
+    return (uint32_t)(uintptr_t)(lds_ptr_t)(const_cast<void *>(p));
+}
+
+struct SliceSrc {
+    i32x4_t ra, rb;
+    uint32_t voff0, voff1;
+    int wave, brow0, K;
+};
+
+// DMA instruction q (0 <= q < A_INS + B_INS) of this wave for one BK-slice
+// into a ring slot: instructions below A_INS fill A rows, the rest B rows.
+// Instruction g of the tile fills LDS rows RPI*g .. RPI*g+RPI-1 (CPR chunks
+// each); lane i carries row RPI*g + i/CPR, LDS position i%CPR, i.e. global
+// chunk (i%CPR) ^ swz(row).
+template <int BMt, int BNt>
+__device__ __forceinline__ void issue_one(const SliceSrc &a, uint32_t lbase, int k0, int q)
+{
+    constexpr int A_INS = BMt / RPI / 4, B_INS = BNt / RPI / 4;
+    if (q < A_INS) {
+        const int g = a.wave * A_INS + q;
+        dma16(a.ra, lbase + g * 1024, (q & 1) ? a.voff1 : a.voff0, (uint32_t)(g * RPI * a.K + k0) * 2u);
+    } else {
+        const int i = q - A_INS;
+        const int g = a.wave * B_INS + i;
+        dma16(a.rb, lbase + (BMt * CPR + g * 64) * 16, (i & 1) ? a.voff1 : a.voff0,
+              (uint32_t)((a.brow0 + i * RPI) * a.K + k0) * 2u);
+    }
+}
+
+template <int BMt, int BNt>
+__device__ __forceinline__ void issue_slice(const SliceSrc &a, uint32_t lbase, int k0)
+{
+    constexpr int INS = BMt / RPI / 4 + BNt / RPI / 4;
+#pragma unroll
+    for (int q = 0; q < INS; ++q) issue_one<BMt, BNt>(a, lbase, k0, q);
+}
+
+template <int MB, int NB>
+struct Frags {
+    bf16x8_t a[2][MB], b[2][NB];
+};
+
+template <int MB, int NB>
+__device__ __forceinline__ void load_frags(Frags<MB, NB> &f, int sl, const uint4 *stg, int kk,
+                                           const int (&arow)[MB], const int (&brow)[NB])
+{
+    const int ch = kk * 2 + ((threadIdx.x & 63) >> 5);
+#pragma unroll
+    for (int i = 0; i < MB; ++i) {
+        uint4 v = stg[arow[i] * CPR + (ch ^ swz(arow[i]))];
+        f.a[sl][i] = *reinterpret_cast<bf16x8_t *>(&v);
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        uint4 v = stg[brow[j] * CPR + (ch ^ swz(brow[j]))];
+        f.b[sl][j] = *reinterpret_cast<bf16x8_t *>(&v);
+    }
+}
+
+template <int MB, int NB>
+__device__ __forceinline__ void mfma_step(f32x16_t (&acc)[MB][NB], const Frags<MB, NB> &f, int sl)
+{
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[sl][i], f.b[sl][j], acc[i][j], 0, 0, 0);
+}
+
+// The MFMAs of one k-step with NQ DMA issues spread between them: a burst of
+// buffer loads would stall this wave's in-order instruction stream behind the
+// memory pipeline and leave the matrix cores idle.  Load q0+q goes out after
+// every MB*NB/NQ MFMAs.
+template <int NQ, int BMt, int BNt>
+__device__ __forceinline__ void mfma_step_dma(f32x16_t (&acc)[BMt / 64][BNt / 64],
+                                              const Frags<BMt / 64, BNt / 64> &f, int sl,
+                                              const SliceSrc &src, uint32_t lbase, int k0, int q0)
+{
+    constexpr int MB = BMt / 64, NB = BNt / 64, TOT = MB * NB;
+    static_assert(NQ == 0 || TOT % NQ == 0, "even spread");
+#pragma unroll
+    for (int t = 0; t < TOT; ++t) {
+        const int i = t / NB, j = t % NB;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[sl][i], f.b[sl][j], acc[i][j], 0, 0, 0);
+        if constexpr (NQ > 0) {
+            if (t % (TOT / NQ) == 0) {
+                __builtin_amdgcn_sched_barrier(0);
+                issue_one<BMt, BNt>(src, lbase, k0, q0 + t / (TOT / NQ));
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ uint16_t bf16_bits(float f)
+{
+    __bf16 h = static_cast<__bf16>(f);  // round to nearest even
+    return *reinterpret_cast<uint16_t *>(&h);
+}
+
+template <int BMt, int BNt, bool GATED>
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
+void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ offsets,
+              const int32_t *__restrict__ tile_prefix, int El, int64_t cap, int N, int K,
+              const uint16_t *__restrict__ W, int64_t w_stride, int up_off,
+              uint16_t *__restrict__ C)
+{
+    constexpr int STAGE = (BMt + BNt) * CPR;        // 16-byte chunks per slice
+    constexpr int A_INS = BMt / RPI / 4, B_INS = BNt / RPI / 4, INS = A_INS + B_INS;
+    constexpr int MB = BMt / 64;                    // 32-row blocks per wave
+    constexpr int NB = BNt / 64;                    // 32-col blocks per wave (gate+up when gated)
+    constexpr int OUTN = GATED ? BNt / 2 : BNt;     // output columns per tile
+    static_assert(A_INS % 2 == 0 && B_INS % 2 == 0, "swizzle parity assumes even counts");
+    static_assert(BMt * OUTN * 2 <= NSTAGE * STAGE * 16, "epilogue staging must fit the ring");
+    __shared__ uint4 ring[NSTAGE * STAGE];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
+    const int wm = wave >> 1, wn = wave & 1;
+    const int n_tiles = (N + OUTN - 1) / OUTN;
+    const int64_t total = (int64_t)tile_prefix[El] * n_tiles;
+    // XCD-aware order: the 8 dies take workgroups round robin, so the
+    // workgroups of one die get a contiguous run of tiles (shared panels in L2).
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int per_xcd = gridDim.x >> 3;
+    // This lane's chunk within a DMA instruction: row lane/CPR of the
+    // instruction's rows, LDS position lane%CPR, global chunk
+    // (lane%CPR) ^ swz(row); swz depends on the instruction only through its
+    // parity, so two byte offsets cover every instruction.
+    const int lrow = lane >> 2;
+    const int pbase = (lane & 3) ^ ((lane >> 3) & 3);
+    const uint32_t voff0 = (uint32_t)(lrow * K + ((pbase ^ (lane >> 5)) * 8)) * 2u;
+    const uint32_t voff1 = (uint32_t)(lrow * K + ((pbase ^ ((lane >> 5) | 2)) * 8)) * 2u;
+    const uint32_t ring_base = lds_addr(ring);
+
+    // this lane's LDS rows for its MFMA fragments
+    int arow[MB], brow[NB];
+#pragma unroll
+    for (int i = 0; i < MB; ++i) arow[i] = wm * (BMt / 2) + i * 32 + (lane & 31);
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        if (GATED) {
+            // first NB/2 blocks: gate rows; last NB/2: the matching up rows
+            const int jj = j % (NB / 2);
+            brow[j] = BMt + (j < NB / 2 ? 0 : BNt / 2) + wn * (BNt / 4) + jj * 32 + (lane & 31);
+        } else {
+            brow[j] = BMt + wn * (BNt / 2) + j * 32 + (lane & 31);
+        }
+    }
+
+    for (int64_t it = 0;; ++it) {
+        const int64_t tile = it * gridDim.x + (int64_t)xcd * per_xcd + slot;
+        if (tile >= total) break;
+        // tile -> (expert, n-tile, m-tile); m-tiles are innermost
+        int lo = 0, hi = El - 1;
+        while (lo < hi) {
+            int mid = (lo + hi + 1) >> 1;
+            if ((int64_t)tile_prefix[mid] * n_tiles <= tile) lo = mid; else hi = mid - 1;
+        }
+        const int e = lo;
+        const int64_t local = tile - (int64_t)tile_prefix[e] * n_tiles;
+        const int mte = tile_prefix[e + 1] - tile_prefix[e];
+        const int nt = (int)(local / mte), mt = (int)(local % mte);
+        const int64_t r0 = clamp_row(offsets[e], cap) + (int64_t)mt * BMt;
+        int64_t r1 = clamp_row(offsets[e + 1], cap);
+        if (r1 > r0 + BMt) r1 = r0 + BMt;
+        const int n0 = nt * OUTN;
+        const int nvalid = N - n0 < OUTN ? N - n0 : OUTN;
+        const uint16_t *We = W + (int64_t)e * w_stride;
+
+        // this wave's B rows lie in one part (gate or up) when gated
+        const int bpart = GATED ? ((wave * B_INS * RPI) / (BNt / 2)) : 0;
+        const SliceSrc src{buffer_desc(A + r0 * K, (r1 - r0) * K * 2),
+                           buffer_desc(We + (int64_t)((GATED && bpart) ? up_off + n0 : n0) * K,
+                                       (int64_t)nvalid * K * 2),
+                           voff0, voff1, wave, wave * B_INS * RPI - bpart * (BNt / 2), K};
+
+        f32x16_t acc[MB][NB];
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+            for (int j = 0; j < NB; ++j) acc[i][j] = f32x16_t{};
+        Frags<MB, NB> f;
+
+        // Ring schedule: slice j lives in slot j % NSTAGE.  While slice s is
+        // consumed, its k-step 0 MFMAs carry the second half of slice
+        // s+NSTAGE-2's loads and its k-step 1 MFMAs the first half of slice
+        // s+NSTAGE-1's (into the slot slice s-1 just freed).
+        constexpr int HALF = INS / 2;
+        const int nk = K / BIG_BK;
+        int s = 0, cur = 0;
+        auto slot_addr = [&](int slice) { return ring_base + (uint32_t)((slice % NSTAGE) * STAGE * 16); };
+        auto begin_slice = [&]() {
+            load_frags(f, 1, ring + cur * STAGE, 1, arow, brow);
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        // hand over to slice s+1: wait until it has landed, publish it, read its first fragments
+        auto hand_over = [&]() {
+            const int last_full = s + NSTAGE - 2 < nk - 1 ? s + NSTAGE - 2 : nk - 1;
+            wait_dma<INS>(last_full - (s + 1));
+            lds_barrier();
+            load_frags(f, 0, ring + (cur + 1 == NSTAGE ? 0 : cur + 1) * STAGE, 0, arow, brow);
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        if (nk >= NSTAGE) {
+            // prologue: slices 0..NSTAGE-3 whole, the first half of NSTAGE-2
+            for (int q = 0; q < NSTAGE - 2; ++q) issue_slice<BMt, BNt>(src, slot_addr(q), q * BIG_BK);
+            for (int q = 0; q < HALF; ++q) issue_one<BMt, BNt>(src, slot_addr(NSTAGE - 2), (NSTAGE - 2) * BIG_BK, q);
+            asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"((NSTAGE - 3) * INS + HALF) : "memory");
+            lds_barrier();
+            load_frags(f, 0, ring, 0, arow, brow);
+            // steady state: both halves go out
+            for (; s + NSTAGE - 1 < nk; ++s) {
+                begin_slice();
+                mfma_step_dma<INS - HALF, BMt, BNt>(acc, f, 0, src, slot_addr(s + NSTAGE - 2),
+                                                     (s + NSTAGE - 2) * BIG_BK, HALF);
+                __builtin_amdgcn_sched_barrier(0);
+                hand_over();
+                mfma_step_dma<HALF, BMt, BNt>(acc, f, 1, src, slot_addr(s + NSTAGE - 1),
+                                              (s + NSTAGE - 1) * BIG_BK, 0);
+                __builtin_amdgcn_sched_barrier(0);
+                cur = cur + 1 == NSTAGE ? 0 : cur + 1;
+            }
+            // the newest slice still owes its second half
+            begin_slice();
+            mfma_step_dma<INS - HALF, BMt, BNt>(acc, f, 0, src, slot_addr(s + NSTAGE - 2),
+                                                 (s + NSTAGE - 2) * BIG_BK, HALF);
+            __builtin_amdgcn_sched_barrier(0);
+            hand_over();
+            mfma_step(acc, f, 1);
+            __builtin_amdgcn_sched_barrier(0);
+            cur = cur + 1 == NSTAGE ? 0 : cur + 1;
+            ++s;
+        } else {
+            for (int q = 0; q < nk; ++q) issue_slice<BMt, BNt>(src, slot_addr(q), q * BIG_BK);
+            wait_dma<INS>(nk - 1);
+            lds_barrier();
+            load_frags(f, 0, ring, 0, arow, brow);
+        }
+        // drain: no more loads
+        for (; s < nk; ++s) {
+            begin_slice();
+            mfma_step(acc, f, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            if (s + 1 < nk) hand_over();
+            mfma_step(acc, f, 1);
+            __builtin_amdgcn_sched_barrier(0);
+            cur = cur + 1 == NSTAGE ? 0 : cur + 1;
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        lds_barrier();  // every wave is done with the ring before it is reused
+
+        // epilogue: block (i, j) lane holds column (lane & 31), rows
+        // 8*(v/4) + 4*(lane/32) + v%4; stage the bf16 tile [BM][OUTN] in LDS
+        uint16_t *stage_out = reinterpret_cast<uint16_t *>(ring);
+#pragma unroll
+        for (int i = 0; i < MB; ++i) {
+#pragma unroll
+            for (int j = 0; j < (GATED ? NB / 2 : NB); ++j) {
+                const int col = wn * (GATED ? BNt / 4 : BNt / 2) + j * 32 + (lane & 31);
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int row = wm * (BMt / 2) + i * 32 + 8 * (v / 4) + 4 * (lane >> 5) + (v % 4);
+                    float o = acc[i][j][v];
+                    if (GATED) o = o / (1.0f + __expf(-o)) * acc[i][j + NB / 2][v];
+                    stage_out[row * OUTN + col] = bf16_bits(o);
+                }
+            }
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        lds_barrier();
+        const uint4 *so = ring;
+        constexpr int CH_ROW = OUTN / 8;
+        const int rows = (int)(r1 - r0);
+        for (int c = tid; c < BMt * CH_ROW; c += 256) {
+            const int row = c / CH_ROW, cc = c % CH_ROW;
+            if (row < rows && cc * 8 < nvalid)
+                *reinterpret_cast<uint4 *>(C + (r0 + row) * N + n0 + cc * 8) = so[c];
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        lds_barrier();  // staging reads done before the next tile's loads
+    }
+}
+
 }  // namespace
 
 size_t ffn_workspace_bytes(int64_t cap, int El, int H, int Is)
@@ -153,12 +514,43 @@ hipError_t launch_grouped_ffn(const uint16_t *x_perm, const int32_t *offsets, in
     uint16_t *h = reinterpret_cast<uint16_t *>(static_cast<char *>(ws) +
                                                align256((size_t)(El + 1) * sizeof(int32_t)));
     hipError_t err;
+    const bool big = (H % BIG_BK == 0) && (Is % BIG_BK == 0);
+    constexpr int BIGM = 256, BIGN = 256;
+    const int bm = big ? BIGM : BM;
     {
         KernelTimer timer(MOE_K_SCHEDULE, s);
-        schedule_kernel<<<dim3(1), dim3(1024), 0, s>>>(offsets, El, cap, BM, tile_prefix);
+        schedule_kernel<<<dim3(1), dim3(1024), 0, s>>>(offsets, El, cap, bm, tile_prefix);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
-    const int64_t max_mtiles = ceil_div(cap, BM) + El;
+    const int64_t max_mtiles = ceil_div(cap, bm) + El;
+    if (big) {
+        static int cus = 0;
+        if (cus == 0) {
+            int dev = 0;
+            if (hipGetDevice(&dev) != hipSuccess ||
+                hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+                cus = 256;
+            cus = (cus + 7) / 8 * 8;
+        }
+
+        {
+            KernelTimer timer(MOE_K_GATE_UP, s);
+            int64_t tiles = max_mtiles * ceil_div(Is, BIGN / 2);
+            int64_t grid = tiles < cus ? (tiles + 7) / 8 * 8 : cus;
+            gemm_big<BIGM, BIGN, true><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
+                x_perm, offsets, tile_prefix, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h);
+            if ((err = hipGetLastError()) != hipSuccess) return err;
+        }
+        {
+            KernelTimer timer(MOE_K_DOWN, s);
+            int64_t tiles = max_mtiles * ceil_div(H, BIGN);
+            int64_t grid = tiles < cus ? (tiles + 7) / 8 * 8 : cus;
+            gemm_big<BIGM, BIGN, false><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
+                h, offsets, tile_prefix, El, cap, H, Is, w2, (int64_t)H * Is, 0, y);
+            if ((err = hipGetLastError()) != hipSuccess) return err;
+        }
+        return hipSuccess;
+    }
     {
         KernelTimer timer(MOE_K_GATE_UP, s);
         int64_t tiles = max_mtiles * ceil_div(Is, BN);
