@@ -24,13 +24,17 @@ __device__ __forceinline__ int64_t clamp_row(int32_t v, int64_t cap)
     return r > cap ? cap : r;
 }
 
-// tile_prefix[e] = m-tiles (of BM rows) of experts before e; [El] = total.
+// tile_prefix[e] = m-tiles (of bm rows) of experts before e; [El] = total.
+// Also clears the stream-K tile counters of the two GEMMs (no memset node is
+// needed, so the chain stays graph-capturable).
 __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restrict__ offsets, int El,
                                                         int64_t cap, int bm,
-                                                        int32_t *__restrict__ tile_prefix)
+                                                        int32_t *__restrict__ tile_prefix,
+                                                        int32_t *__restrict__ counters, int64_t n_counters)
 {
     __shared__ int32_t wsum[16];
     const int e = threadIdx.x;
+    for (int64_t i = e; i < n_counters; i += 1024) counters[i] = 0;
     int32_t mt = 0;
     if (e < El) {
         int64_t a = clamp_row(offsets[e], cap), b = clamp_row(offsets[e + 1], cap);
@@ -313,12 +317,48 @@ __device__ __forceinline__ uint16_t bf16_bits(float f)
     return *reinterpret_cast<uint16_t *>(&h);
 }
 
+// Partial accumulator slot: one fp32 value per accumulator register of each
+// of the 256 threads, stored register-major so each access is a coalesced
+// 16-byte vector per lane.
+constexpr int SLOT_FLOATS = 256 * 256;
+
+// Work split of one launch over G persistent workgroups.  With at least G
+// tiles every tile is handed out whole, round robin (dp = T): workgroups on
+// one die then walk K in near lockstep over shared panels, which is what
+// keeps the die's L2 effective.  With fewer tiles than workgroups (a few
+// large-K tiles, e.g. one expert's down projection) the K-slices of all
+// tiles are cut into contiguous runs ("stream-K"), so every workgroup gets
+// the same number of slices; partial sums are combined by the last
+// contributor of each tile.
+struct WorkSplit {
+    int64_t T, dp, iters;  // tiles, whole tiles, K-slices in the stream-K part
+    int nk, G, Gsk;        // slices per tile, workgroups, workgroups in the stream-K part
+    __device__ WorkSplit(int64_t total, int nk_, int g) : T(total), nk(nk_), G(g)
+    {
+        dp = T >= G ? T : 0;
+        iters = (T - dp) * nk;
+        // every stream-K workgroup gets at least one slice, so the workgroups
+        // that meet a tile are exactly a consecutive range
+        Gsk = iters < G ? (int)iters : G;
+    }
+    // first stream-K slice of workgroup v (v <= Gsk)
+    __device__ int64_t begin(int v) const { return (int64_t)v * iters / Gsk; }
+    // workgroup whose stream-K run holds slice x
+    __device__ int owner(int64_t x) const
+    {
+        int v = (int)(x * Gsk / iters);
+        while (v + 1 < Gsk && begin(v + 1) <= x) ++v;
+        while (v > 0 && begin(v) > x) --v;
+        return v;
+    }
+};
+
 template <int BMt, int BNt, bool GATED>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
 void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ offsets,
               const int32_t *__restrict__ tile_prefix, int El, int64_t cap, int N, int K,
               const uint16_t *__restrict__ W, int64_t w_stride, int up_off,
-              uint16_t *__restrict__ C)
+              uint16_t *__restrict__ C, int32_t *__restrict__ tile_cnt, float *__restrict__ partials)
 {
     constexpr int STAGE = (BMt + BNt) * CPR;        // 16-byte chunks per slice
     constexpr int A_INS = BMt / RPI / 4, B_INS = BNt / RPI / 4, INS = A_INS + B_INS;
@@ -327,17 +367,19 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ offset
     constexpr int OUTN = GATED ? BNt / 2 : BNt;     // output columns per tile
     static_assert(A_INS % 2 == 0 && B_INS % 2 == 0, "swizzle parity assumes even counts");
     static_assert(BMt * OUTN * 2 <= NSTAGE * STAGE * 16, "epilogue staging must fit the ring");
+    static_assert(MB * NB * 16 * 256 == SLOT_FLOATS, "partial slot layout");
     __shared__ uint4 ring[NSTAGE * STAGE];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
     const int wm = wave >> 1, wn = wave & 1;
     const int n_tiles = (N + OUTN - 1) / OUTN;
-    const int64_t total = (int64_t)tile_prefix[El] * n_tiles;
-    // XCD-aware order: the 8 dies take workgroups round robin, so the
-    // workgroups of one die get a contiguous run of tiles (shared panels in L2).
-    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
-    const int per_xcd = gridDim.x >> 3;
+    const int nk = K / BIG_BK;
+    const WorkSplit ws((int64_t)tile_prefix[El] * n_tiles, nk, gridDim.x);
+    // XCD-aware numbering: the 8 dies take workgroups round robin, so the
+    // workgroups of one die get consecutive virtual ids and with them a
+    // contiguous run of tiles (shared panels in that die's L2).
+    const int v = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
     // This lane's chunk within a DMA instruction: row lane/CPR of the
     // instruction's rows, LDS position lane%CPR, global chunk
     // (lane%CPR) ^ swz(row); swz depends on the instruction only through its
@@ -363,9 +405,24 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ offset
         }
     }
 
-    for (int64_t it = 0;; ++it) {
-        const int64_t tile = it * gridDim.x + (int64_t)xcd * per_xcd + slot;
-        if (tile >= total) break;
+    // Write the staged bf16 tile [BM][OUTN] from LDS with 16-byte stores.
+    auto store_staged = [&](int64_t r0, int64_t r1, int n0, int nvalid) {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        lds_barrier();
+        const uint4 *so = ring;
+        constexpr int CH_ROW = OUTN / 8;
+        const int rows = (int)(r1 - r0);
+        for (int c = tid; c < BMt * CH_ROW; c += 256) {
+            const int row = c / CH_ROW, cc = c % CH_ROW;
+            if (row < rows && cc * 8 < nvalid)
+                *reinterpret_cast<uint4 *>(C + (r0 + row) * N + n0 + cc * 8) = so[c];
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        lds_barrier();  // staging reads done before the next piece's loads
+    };
+
+    // One piece of work: K-slices [klo, khi) of tile `tile`.
+    auto do_work = [&](int64_t tile, int klo, int khi) {
         // tile -> (expert, n-tile, m-tile); m-tiles are innermost
         int lo = 0, hi = El - 1;
         while (lo < hi) {
@@ -397,49 +454,50 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ offset
             for (int j = 0; j < NB; ++j) acc[i][j] = f32x16_t{};
         Frags<MB, NB> f;
 
-        // Ring schedule: slice j lives in slot j % NSTAGE.  While slice s is
-        // consumed, its k-step 0 MFMAs carry the second half of slice
-        // s+NSTAGE-2's loads and its k-step 1 MFMAs the first half of slice
-        // s+NSTAGE-1's (into the slot slice s-1 just freed).
+        // Ring schedule over slices klo..khi-1 (slice j in slot (j-klo) % NSTAGE).
+        // While slice s is consumed, its k-step 0 MFMAs carry the second half
+        // of slice s+NSTAGE-2's loads and its k-step 1 MFMAs the first half of
+        // slice s+NSTAGE-1's (into the slot that slice s-1 just freed).
         constexpr int HALF = INS / 2;
-        const int nk = K / BIG_BK;
+        const int ns = khi - klo;  // slices in this piece (>= 1)
         int s = 0, cur = 0;
-        auto slot_addr = [&](int slice) { return ring_base + (uint32_t)((slice % NSTAGE) * STAGE * 16); };
+        auto slot_addr = [&](int j) { return ring_base + (uint32_t)((j % NSTAGE) * STAGE * 16); };
+        auto kof = [&](int j) { return (klo + j) * BIG_BK; };
         auto begin_slice = [&]() {
             load_frags(f, 1, ring + cur * STAGE, 1, arow, brow);
             __builtin_amdgcn_sched_barrier(0);
         };
         // hand over to slice s+1: wait until it has landed, publish it, read its first fragments
         auto hand_over = [&]() {
-            const int last_full = s + NSTAGE - 2 < nk - 1 ? s + NSTAGE - 2 : nk - 1;
+            const int last_full = s + NSTAGE - 2 < ns - 1 ? s + NSTAGE - 2 : ns - 1;
             wait_dma<INS>(last_full - (s + 1));
             lds_barrier();
             load_frags(f, 0, ring + (cur + 1 == NSTAGE ? 0 : cur + 1) * STAGE, 0, arow, brow);
             __builtin_amdgcn_sched_barrier(0);
         };
-        if (nk >= NSTAGE) {
+        if (ns >= NSTAGE) {
             // prologue: slices 0..NSTAGE-3 whole, the first half of NSTAGE-2
-            for (int q = 0; q < NSTAGE - 2; ++q) issue_slice<BMt, BNt>(src, slot_addr(q), q * BIG_BK);
-            for (int q = 0; q < HALF; ++q) issue_one<BMt, BNt>(src, slot_addr(NSTAGE - 2), (NSTAGE - 2) * BIG_BK, q);
+            for (int q = 0; q < NSTAGE - 2; ++q) issue_slice<BMt, BNt>(src, slot_addr(q), kof(q));
+            for (int q = 0; q < HALF; ++q) issue_one<BMt, BNt>(src, slot_addr(NSTAGE - 2), kof(NSTAGE - 2), q);
             asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"((NSTAGE - 3) * INS + HALF) : "memory");
             lds_barrier();
             load_frags(f, 0, ring, 0, arow, brow);
             // steady state: both halves go out
-            for (; s + NSTAGE - 1 < nk; ++s) {
+            for (; s + NSTAGE - 1 < ns; ++s) {
                 begin_slice();
                 mfma_step_dma<INS - HALF, BMt, BNt>(acc, f, 0, src, slot_addr(s + NSTAGE - 2),
-                                                     (s + NSTAGE - 2) * BIG_BK, HALF);
+                                                     kof(s + NSTAGE - 2), HALF);
                 __builtin_amdgcn_sched_barrier(0);
                 hand_over();
                 mfma_step_dma<HALF, BMt, BNt>(acc, f, 1, src, slot_addr(s + NSTAGE - 1),
-                                              (s + NSTAGE - 1) * BIG_BK, 0);
+                                              kof(s + NSTAGE - 1), 0);
                 __builtin_amdgcn_sched_barrier(0);
                 cur = cur + 1 == NSTAGE ? 0 : cur + 1;
             }
             // the newest slice still owes its second half
             begin_slice();
             mfma_step_dma<INS - HALF, BMt, BNt>(acc, f, 0, src, slot_addr(s + NSTAGE - 2),
-                                                 (s + NSTAGE - 2) * BIG_BK, HALF);
+                                                 kof(s + NSTAGE - 2), HALF);
             __builtin_amdgcn_sched_barrier(0);
             hand_over();
             mfma_step(acc, f, 1);
@@ -447,23 +505,107 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ offset
             cur = cur + 1 == NSTAGE ? 0 : cur + 1;
             ++s;
         } else {
-            for (int q = 0; q < nk; ++q) issue_slice<BMt, BNt>(src, slot_addr(q), q * BIG_BK);
-            wait_dma<INS>(nk - 1);
+            for (int q = 0; q < ns; ++q) issue_slice<BMt, BNt>(src, slot_addr(q), kof(q));
+            wait_dma<INS>(ns - 1);
             lds_barrier();
             load_frags(f, 0, ring, 0, arow, brow);
         }
         // drain: no more loads
-        for (; s < nk; ++s) {
+        for (; s < ns; ++s) {
             begin_slice();
             mfma_step(acc, f, 0);
             __builtin_amdgcn_sched_barrier(0);
-            if (s + 1 < nk) hand_over();
+            if (s + 1 < ns) hand_over();
             mfma_step(acc, f, 1);
             __builtin_amdgcn_sched_barrier(0);
             cur = cur + 1 == NSTAGE ? 0 : cur + 1;
         }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         lds_barrier();  // every wave is done with the ring before it is reused
+
+        if (klo != 0 || khi != nk) {
+            // Part of a stream-K tile.  Contributors are the workgroups whose
+            // runs meet the tile's slices; each stores its partial, and the
+            // last to arrive sums all of them in contributor order (the same
+            // order whoever arrives last) and writes the tile.
+            const int64_t tb = (tile - ws.dp) * nk;  // first stream-K slice of the tile
+            const int vfirst = ws.owner(tb), vlast = ws.owner(tb + nk - 1);
+            auto slot_of = [&](int u) {  // slot 0: u's run starts in this tile; 1: it ends here
+                return (int64_t)u * 2 + (ws.begin(u) >= tb ? 0 : 1);
+            };
+            // Partials move with agent-coherent (sc1) stores and loads, so no
+            // L2-wide write-back/invalidate fence is needed: a fence would
+            // flush the operand panels other workgroups on the die are reusing.
+            typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+            const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(
+                partials, (short)0, (int)((int64_t)2 * ws.G * SLOT_FLOATS * 4), 0x00020000);
+            constexpr int SC1 = 0x10;
+            {
+                const uint32_t base_b = (uint32_t)(slot_of(v) * SLOT_FLOATS * 4);
+#pragma unroll
+                for (int i = 0; i < MB; ++i)
+#pragma unroll
+                    for (int j = 0; j < NB; ++j)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            float4 pv = make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                                    acc[i][j][4 * q + 3]);
+                            __builtin_amdgcn_raw_buffer_store_b128(
+                                *reinterpret_cast<u32x4_t *>(&pv), pr,
+                                base_b + (uint32_t)((((i * NB + j) * 4 + q) * 256 + tid) * 16), 0, SC1);
+                        }
+            }
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // partial is visible device-wide
+            lds_barrier();
+            int *flag = reinterpret_cast<int *>(ring);
+            if (tid == 0) {
+                const int old = __hip_atomic_fetch_add(&tile_cnt[tile], 1, __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
+                *flag = old == vlast - vfirst;
+            }
+            asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+            lds_barrier();
+            const bool last = *flag != 0;
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            lds_barrier();
+            if (!last) return;
+            // Last contributor: sum the partials in contributor order straight
+            // from memory into the bf16 staging tile (the accumulator
+            // registers are not needed again).
+            uint16_t *stage_out = reinterpret_cast<uint16_t *>(ring);
+            for (int i = 0; i < MB; ++i) {
+                for (int j = 0; j < (GATED ? NB / 2 : NB); ++j) {
+                    const int col = wn * (GATED ? BNt / 4 : BNt / 2) + j * 32 + (lane & 31);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        float4 g = make_float4(0.f, 0.f, 0.f, 0.f), u = g;
+                        for (int c = vfirst; c <= vlast; ++c) {
+                            const uint32_t base_b = (uint32_t)(slot_of(c) * SLOT_FLOATS * 4);
+                            u32x4_t w = __builtin_amdgcn_raw_buffer_load_b128(
+                                pr, base_b + (uint32_t)((((i * NB + j) * 4 + q) * 256 + tid) * 16), 0, SC1);
+                            const float4 pv = *reinterpret_cast<float4 *>(&w);
+                            g.x += pv.x; g.y += pv.y; g.z += pv.z; g.w += pv.w;
+                            if (GATED) {
+                                u32x4_t w2 = __builtin_amdgcn_raw_buffer_load_b128(
+                                    pr, base_b + (uint32_t)((((i * NB + j + NB / 2) * 4 + q) * 256 + tid) * 16), 0, SC1);
+                                const float4 pu = *reinterpret_cast<float4 *>(&w2);
+                                u.x += pu.x; u.y += pu.y; u.z += pu.z; u.w += pu.w;
+                            }
+                        }
+                        const float gv[4] = {g.x, g.y, g.z, g.w}, uv[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int row = wm * (BMt / 2) + i * 32 + 8 * q + 4 * (lane >> 5) + r;
+                            float o = gv[r];
+                            if (GATED) o = o / (1.0f + __expf(-o)) * uv[r];
+                            stage_out[row * OUTN + col] = bf16_bits(o);
+                        }
+                    }
+                }
+            }
+            store_staged(r0, r1, n0, nvalid);
+            return;
+        }
 
         // epilogue: block (i, j) lane holds column (lane & 31), rows
         // 8*(v/4) + 4*(lane/32) + v%4; stage the bf16 tile [BM][OUTN] in LDS
@@ -474,35 +616,92 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ offset
             for (int j = 0; j < (GATED ? NB / 2 : NB); ++j) {
                 const int col = wn * (GATED ? BNt / 4 : BNt / 2) + j * 32 + (lane & 31);
 #pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int row = wm * (BMt / 2) + i * 32 + 8 * (v / 4) + 4 * (lane >> 5) + (v % 4);
-                    float o = acc[i][j][v];
-                    if (GATED) o = o / (1.0f + __expf(-o)) * acc[i][j + NB / 2][v];
+                for (int q = 0; q < 16; ++q) {
+                    const int row = wm * (BMt / 2) + i * 32 + 8 * (q / 4) + 4 * (lane >> 5) + (q % 4);
+                    float o = acc[i][j][q];
+                    if (GATED) o = o / (1.0f + __expf(-o)) * acc[i][j + NB / 2][q];
                     stage_out[row * OUTN + col] = bf16_bits(o);
                 }
             }
         }
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        lds_barrier();
-        const uint4 *so = ring;
-        constexpr int CH_ROW = OUTN / 8;
-        const int rows = (int)(r1 - r0);
-        for (int c = tid; c < BMt * CH_ROW; c += 256) {
-            const int row = c / CH_ROW, cc = c % CH_ROW;
-            if (row < rows && cc * 8 < nvalid)
-                *reinterpret_cast<uint4 *>(C + (r0 + row) * N + n0 + cc * 8) = so[c];
+        store_staged(r0, r1, n0, nvalid);
+    };
+
+    // This workgroup's work items, in order: whole tiles v, v+G, ... below
+    // dp, then its stream-K run.  One call site keeps the kernel's register
+    // allocation to a single copy of the pipeline.
+    const int64_t n_dp = v < ws.dp ? (ws.dp - 1 - v) / ws.G + 1 : 0;
+    const bool has_sk = ws.iters > 0 && v < ws.Gsk;
+    int64_t sk_i = has_sk ? ws.begin(v) : 0;
+    const int64_t sk_end = has_sk ? ws.begin(v + 1) : 0;
+    for (int64_t w = 0;; ++w) {
+        int64_t tile;
+        int klo, khi;
+        if (w < n_dp) {
+            tile = v + w * ws.G;
+            klo = 0;
+            khi = nk;
+        } else if (sk_i < sk_end) {
+            tile = ws.dp + sk_i / nk;
+            klo = (int)(sk_i % nk);
+            khi = (int)(klo + (sk_end - sk_i) < nk ? klo + (sk_end - sk_i) : nk);
+            sk_i += khi - klo;
+        } else {
+            break;
         }
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        lds_barrier();  // staging reads done before the next tile's loads
+        do_work(tile, klo, khi);
     }
 }
 
 }  // namespace
 
+namespace {
+
+constexpr int BIGM = 256, BIGN = 256;
+
+int device_cus()
+{
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        cus = 256;
+    return (cus + 7) / 8 * 8;  // whole rounds over the 8 dies
+}
+
+// Workspace layout of the grouped FFN (every part 256-byte aligned):
+//   tile_prefix [El+1] | counters gate-up [Tgu] | counters down [Tdn] |
+//   partial slots [2*G][SLOT_FLOATS] fp32 | h [cap, I_s] bf16
+struct FfnLayout {
+    int bm;
+    int64_t max_mtiles, t_gu, t_dn;
+    int grid_gu, grid_dn;
+    size_t off_cnt, off_part, off_h, total;
+    FfnLayout(int64_t cap, int El, int H, int Is)
+    {
+        const bool big = (H % BIG_BK == 0) && (Is % BIG_BK == 0);
+        bm = big ? BIGM : BM;
+        max_mtiles = ceil_div(cap, bm) + El;
+        t_gu = max_mtiles * ceil_div(Is, big ? BIGN / 2 : BN);
+        t_dn = max_mtiles * ceil_div(H, big ? BIGN : BN);
+        const int cus = device_cus();
+        auto grid = [&](int64_t tiles) {
+            return (int)(tiles < cus ? (tiles + 7) / 8 * 8 : cus);
+        };
+        grid_gu = grid(t_gu);
+        grid_dn = grid(t_dn);
+        const int slots = big ? 2 * (grid_gu > grid_dn ? grid_gu : grid_dn) : 0;
+        off_cnt = align256((size_t)(El + 1) * sizeof(int32_t));
+        off_part = off_cnt + align256((size_t)(t_gu + t_dn) * sizeof(int32_t));
+        off_h = off_part + align256((size_t)slots * SLOT_FLOATS * sizeof(float));
+        total = off_h + align256((size_t)cap * Is * 2);
+    }
+};
+
+}  // namespace
+
 size_t ffn_workspace_bytes(int64_t cap, int El, int H, int Is)
 {
-    (void)H;
-    return align256((size_t)(El + 1) * sizeof(int32_t)) + align256((size_t)cap * Is * 2);
+    return FfnLayout(cap, El, H, Is).total;
 }
 
 hipError_t launch_grouped_ffn(const uint16_t *x_perm, const int32_t *offsets, int El, int64_t cap,
@@ -510,59 +709,47 @@ hipError_t launch_grouped_ffn(const uint16_t *x_perm, const int32_t *offsets, in
                               void *ws, hipStream_t s)
 {
     if (cap == 0) return hipSuccess;
-    int32_t *tile_prefix = static_cast<int32_t *>(ws);
-    uint16_t *h = reinterpret_cast<uint16_t *>(static_cast<char *>(ws) +
-                                               align256((size_t)(El + 1) * sizeof(int32_t)));
+    const FfnLayout L(cap, El, H, Is);
+    char *base = static_cast<char *>(ws);
+    int32_t *tile_prefix = reinterpret_cast<int32_t *>(base);
+    int32_t *cnt = reinterpret_cast<int32_t *>(base + L.off_cnt);
+    float *partials = reinterpret_cast<float *>(base + L.off_part);
+    uint16_t *h = reinterpret_cast<uint16_t *>(base + L.off_h);
+    const bool big = L.bm == BIGM;
     hipError_t err;
-    const bool big = (H % BIG_BK == 0) && (Is % BIG_BK == 0);
-    constexpr int BIGM = 256, BIGN = 256;
-    const int bm = big ? BIGM : BM;
     {
         KernelTimer timer(MOE_K_SCHEDULE, s);
-        schedule_kernel<<<dim3(1), dim3(1024), 0, s>>>(offsets, El, cap, bm, tile_prefix);
+        schedule_kernel<<<dim3(1), dim3(1024), 0, s>>>(offsets, El, cap, L.bm, tile_prefix, cnt,
+                                                       big ? L.t_gu + L.t_dn : 0);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
-    const int64_t max_mtiles = ceil_div(cap, bm) + El;
     if (big) {
-        static int cus = 0;
-        if (cus == 0) {
-            int dev = 0;
-            if (hipGetDevice(&dev) != hipSuccess ||
-                hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-                cus = 256;
-            cus = (cus + 7) / 8 * 8;
-        }
-
         {
             KernelTimer timer(MOE_K_GATE_UP, s);
-            int64_t tiles = max_mtiles * ceil_div(Is, BIGN / 2);
-            int64_t grid = tiles < cus ? (tiles + 7) / 8 * 8 : cus;
-            gemm_big<BIGM, BIGN, true><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
-                x_perm, offsets, tile_prefix, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h);
+            gemm_big<BIGM, BIGN, true><<<dim3((unsigned)L.grid_gu), dim3(256), 0, s>>>(
+                x_perm, offsets, tile_prefix, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h, cnt,
+                partials);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         {
             KernelTimer timer(MOE_K_DOWN, s);
-            int64_t tiles = max_mtiles * ceil_div(H, BIGN);
-            int64_t grid = tiles < cus ? (tiles + 7) / 8 * 8 : cus;
-            gemm_big<BIGM, BIGN, false><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
-                h, offsets, tile_prefix, El, cap, H, Is, w2, (int64_t)H * Is, 0, y);
+            gemm_big<BIGM, BIGN, false><<<dim3((unsigned)L.grid_dn), dim3(256), 0, s>>>(
+                h, offsets, tile_prefix, El, cap, H, Is, w2, (int64_t)H * Is, 0, y, cnt + L.t_gu,
+                partials);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         return hipSuccess;
     }
     {
         KernelTimer timer(MOE_K_GATE_UP, s);
-        int64_t tiles = max_mtiles * ceil_div(Is, BN);
-        int64_t grid = tiles < 2048 ? tiles : 2048;
+        int64_t grid = L.t_gu < 2048 ? L.t_gu : 2048;
         gemm_kernel<true><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
             x_perm, offsets, tile_prefix, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     {
         KernelTimer timer(MOE_K_DOWN, s);
-        int64_t tiles = max_mtiles * ceil_div(H, BN);
-        int64_t grid = tiles < 2048 ? tiles : 2048;
+        int64_t grid = L.t_dn < 2048 ? L.t_dn : 2048;
         gemm_kernel<false><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
             h, offsets, tile_prefix, El, cap, H, Is, w2, (int64_t)H * Is, 0, y);
         if ((err = hipGetLastError()) != hipSuccess) return err;
