@@ -54,6 +54,34 @@ def algorithmic_work(cfg, counts: np.ndarray):
                 flops=gate_up_flops + down_flops + sh_flops, bytes=step_bytes)
 
 
+def kernel_source_sha() -> str:
+    """Hash of the grouped-FFN kernel source: counter summaries taken on
+    another version of the kernel no longer describe this one."""
+    import hashlib
+    path = os.path.join(ROOT, "paper_2606_26607_amd", "csrc", "ffn.hip")
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per gate-up launch from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE scaled by the copy-kernel calibration),
+    or None when there is none for this kernel source."""
+    path = os.path.join(ROOT, "profiles", f"gate_up_{workload}_counters.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256") != kernel_source_sha():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_dispatch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(inp, target_s: float):
     """The CPU oracle, timed on a bounded sample of the workload's tokens
     (routing, permutation, expert FFNs and combine for those tokens)."""
@@ -95,6 +123,8 @@ def main():
     ap.add_argument("--graph", action="store_true", help="replay the step from a HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="also run one device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -124,6 +154,14 @@ def main():
     for _ in range(args.warmup):
         layer.forward(x, logits)
     torch.cuda.synchronize()
+    if args.copy_calib_mib:
+        # a plain copy of known size: its FETCH_SIZE / WRITE_SIZE calibrate the counters
+        src = torch.empty(args.copy_calib_mib << 19, dtype=torch.int16, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     counts = layer.bufs["counts"].cpu().numpy()
     work = algorithmic_work(cfg, counts)
 
@@ -170,13 +208,14 @@ def main():
         if decode:
             achieved = work["gate_up_bytes"] / dur_s / 1e9
             roof = dict(bound="hbm", achieved=achieved, peak=PEAK_HBM_GBS, unit="GB/s",
-                        frac=achieved / PEAK_HBM_GBS, traffic=None, kernel="gate_up",
+                        frac=achieved / PEAK_HBM_GBS, traffic=measured_traffic(cfg.name), kernel="gate_up",
                         algorithmic_per_launch=work["gate_up_bytes"])
         else:
             achieved = work["gate_up_flops"] / dur_s / 1e12
             roof = dict(bound="mfma", achieved=achieved, peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
-                        frac=achieved / PEAK_BF16_TFLOPS, traffic=None, kernel="gate_up",
-                        algorithmic_per_launch=work["gate_up_flops"])
+                        frac=achieved / PEAK_BF16_TFLOPS, traffic=measured_traffic(cfg.name), kernel="gate_up",
+                        algorithmic_per_launch=work["gate_up_flops"],
+                        algorithmic_bytes_per_launch=work["gate_up_bytes"])
     else:
         roof = None
 
