@@ -10,6 +10,8 @@
 // and experts with no rows cost nothing.  The gate-up workgroup owns the
 // matching gate and up columns, so SwiGLU is applied in registers before h
 // is written.
+#include <type_traits>
+
 #include "moe_internal.h"
 
 namespace moe {
@@ -142,35 +144,40 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t *__restrict__ 
 
 
 // ---------------------------------------------------------------------------
-// Large-tile kernel (K a multiple of 32): BMxBN tiles (BN counts weight rows;
-// a gated tile holds BN/2 gate rows and the BN/2 matching up rows), 4 waves
-// in a 2x2 grid, each wave (BM/2)x(BN/2) of 32x32x16 MFMA blocks.
+// Large-tile kernel (K a multiple of 64, at least 128): BMxBN tiles (BN counts
+// weight rows; a gated tile holds BN/2 gate rows and the BN/2 matching up
+// rows), 4 waves in a 2x2 grid, each wave (BM/2)x(BN/2) of 32x32x16 MFMA
+// blocks, accumulators in AGPRs.
 //
 // Operands move L2 -> LDS with buffer loads that write LDS directly (no VGPR
-// staging) into a ring of NSTAGE slices of BK=32 (all 160 KB of LDS), so
-// NSTAGE-1 slices are in flight while one is consumed: the feed is latency
-// bound otherwise.  Buffer range checking returns zeros for rows past the
-// expert's last row or past N.  Within a slice the fragments of k-step 1 are
-// read while the MFMAs of k-step 0 run; the workgroup barrier that hands over
-// to the next slice sits between the two k-steps, so the next slice's first
-// fragments are also read under MFMAs.  LDS rows are 64 bytes; 16-byte chunk
-// c of row r sits at c ^ swz(r), so each 16-row (and 8-row) group read by one
-// ds_read_b128 covers distinct banks.  The epilogue stages the bf16 tile in
-// LDS and writes it with coalesced 16-byte stores.
+// staging) in BK=64 slices (128-byte row segments: whole L2 lines).  A
+// (activations, mostly L2 hits) and B (weights, more misses) have separate
+// rings: 2 A slots and 3 B slots fill the 160 KB of LDS, so while slice s is
+// consumed the loads of A(s+1) and B(s+2) are in flight.  The loads are issued
+// one per four MFMAs (A under k-steps 0-1, B under k-steps 2-3): a burst would
+// stall the wave's in-order instruction stream behind the memory pipeline.
+// Fragments of k-step kk+1 are read while the MFMAs of kk run, and the
+// barrier that hands over to slice s+1 sits before the last k-step, so the
+// next slice's first fragments are read under MFMAs too.  Buffer range
+// checking returns zeros for rows past the expert's last row or past N.
+// LDS rows are 128 bytes; 16-byte chunk c of row r sits at c ^ swz(r), so
+// each 16-row (and 8-row) group read by one ds_read_b128 covers distinct
+// banks.  The epilogue stages the bf16 tile in LDS and writes it with
+// coalesced 16-byte stores.
 // ---------------------------------------------------------------------------
-constexpr int BIG_BK = 32;   // K per slice
-constexpr int NSTAGE = 5;    // ring slices
+constexpr int BIG_BK = 64;        // K per slice
 constexpr int CPR = BIG_BK / 8;   // 16-byte chunks per LDS row
 constexpr int RPI = 64 / CPR;     // rows per DMA instruction
+constexpr int A_SLOTS = 2, B_SLOTS = 3;
 
-__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 typedef __attribute__((address_space(3))) void *lds_ptr_t;
 typedef int i32x4_t __attribute__((ext_vector_type(4)));
 
 // Workgroup barrier without the memory fence of __syncthreads(): that fence
-// would also wait for the slices still in flight.  The ordering the ring
-// needs is explicit: each wave waits (vmcnt) for its own loads of a slice to
+// would also wait for the slices still in flight.  The ordering the rings
+// need is explicit: each wave waits (vmcnt) for its own loads of a slice to
 // land in LDS, and (lgkmcnt) for its own reads of a slot, before the barrier
 // that publishes the slice or frees the slot.
 __device__ __forceinline__ void lds_barrier()
@@ -178,18 +185,6 @@ __device__ __forceinline__ void lds_barrier()
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-}
-
-// Wait until at most `n` (a multiple of `ins`, below 4*ins) DMA instructions
-// of this wave are outstanding.
-template <int INS>
-__device__ __forceinline__ void wait_dma(int n_slices)
-{
-    static_assert(3 * INS < 64, "vmcnt range");
-    if (n_slices >= 3) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(3 * INS) : "memory");
-    else if (n_slices == 2) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(2 * INS) : "memory");
-    else if (n_slices == 1) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(INS) : "memory");
-    else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
 }
 
 // Raw buffer descriptor: base, no stride, num_records bytes (reads past it
@@ -208,7 +203,7 @@ __device__ __forceinline__ i32x4_t buffer_desc(const void *base, int64_t bytes)
 // 16 bytes per lane from global memory straight into LDS: lane i's data lands
 // at LDS byte address lds + 16*i.  Written as inline asm so that the
 // compiler does not track it as a pending LDS write (it would otherwise wait
-// for every such load before any LDS read); the ring waits explicitly.
+// for every such load before any LDS read); the rings wait explicitly.
 __device__ __forceinline__ void dma16(i32x4_t desc, uint32_t lds, uint32_t voff, uint32_t soff)
 {
     asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
@@ -226,32 +221,24 @@ struct SliceSrc {
     int wave, brow0, K;
 };
 
-// DMA instruction q (0 <= q < A_INS + B_INS) of this wave for one BK-slice
-// into a ring slot: instructions below A_INS fill A rows, the rest B rows.
-// Instruction g of the tile fills LDS rows RPI*g .. RPI*g+RPI-1 (CPR chunks
-// each); lane i carries row RPI*g + i/CPR, LDS position i%CPR, i.e. global
-// chunk (i%CPR) ^ swz(row).
-template <int BMt, int BNt>
-__device__ __forceinline__ void issue_one(const SliceSrc &a, uint32_t lbase, int k0, int q)
+// DMA instruction q of this wave for one BK-slice of A (or of B) into a ring
+// slot.  Instruction g of the operand tile fills LDS rows RPI*g .. RPI*g+RPI-1;
+// lane i carries row RPI*g + i/CPR, LDS position i%CPR, i.e. global chunk
+// (i%CPR) ^ swz(row), which depends on g only through its parity.
+template <int BMt>
+__device__ __forceinline__ void issue_a(const SliceSrc &a, uint32_t slot, int k0, int q)
 {
-    constexpr int A_INS = BMt / RPI / 4, B_INS = BNt / RPI / 4;
-    if (q < A_INS) {
-        const int g = a.wave * A_INS + q;
-        dma16(a.ra, lbase + g * 1024, (q & 1) ? a.voff1 : a.voff0, (uint32_t)(g * RPI * a.K + k0) * 2u);
-    } else {
-        const int i = q - A_INS;
-        const int g = a.wave * B_INS + i;
-        dma16(a.rb, lbase + (BMt * CPR + g * 64) * 16, (i & 1) ? a.voff1 : a.voff0,
-              (uint32_t)((a.brow0 + i * RPI) * a.K + k0) * 2u);
-    }
+    constexpr int A_INS = BMt / RPI / 4;
+    const int g = a.wave * A_INS + q;
+    dma16(a.ra, slot + g * 1024, (q & 1) ? a.voff1 : a.voff0, (uint32_t)(g * RPI * a.K + k0) * 2u);
 }
 
-template <int BMt, int BNt>
-__device__ __forceinline__ void issue_slice(const SliceSrc &a, uint32_t lbase, int k0)
+template <int BNt>
+__device__ __forceinline__ void issue_b(const SliceSrc &a, uint32_t slot, int k0, int q)
 {
-    constexpr int INS = BMt / RPI / 4 + BNt / RPI / 4;
-#pragma unroll
-    for (int q = 0; q < INS; ++q) issue_one<BMt, BNt>(a, lbase, k0, q);
+    constexpr int B_INS = BNt / RPI / 4;
+    const int g = a.wave * B_INS + q;
+    dma16(a.rb, slot + g * 1024, (q & 1) ? a.voff1 : a.voff0, (uint32_t)((a.brow0 + q * RPI) * a.K + k0) * 2u);
 }
 
 template <int MB, int NB>
@@ -260,40 +247,27 @@ struct Frags {
 };
 
 template <int MB, int NB>
-__device__ __forceinline__ void load_frags(Frags<MB, NB> &f, int sl, const uint4 *stg, int kk,
+__device__ __forceinline__ void load_frags(Frags<MB, NB> &f, int sl, const uint4 *sa, const uint4 *sb, int kk,
                                            const int (&arow)[MB], const int (&brow)[NB])
 {
     const int ch = kk * 2 + ((threadIdx.x & 63) >> 5);
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
-        uint4 v = stg[arow[i] * CPR + (ch ^ swz(arow[i]))];
+        uint4 v = sa[arow[i] * CPR + (ch ^ swz(arow[i]))];
         f.a[sl][i] = *reinterpret_cast<bf16x8_t *>(&v);
     }
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-        uint4 v = stg[brow[j] * CPR + (ch ^ swz(brow[j]))];
+        uint4 v = sb[brow[j] * CPR + (ch ^ swz(brow[j]))];
         f.b[sl][j] = *reinterpret_cast<bf16x8_t *>(&v);
     }
 }
 
-template <int MB, int NB>
-__device__ __forceinline__ void mfma_step(f32x16_t (&acc)[MB][NB], const Frags<MB, NB> &f, int sl)
-{
-#pragma unroll
-    for (int i = 0; i < MB; ++i)
-#pragma unroll
-        for (int j = 0; j < NB; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[sl][i], f.b[sl][j], acc[i][j], 0, 0, 0);
-}
-
-// The MFMAs of one k-step with NQ DMA issues spread between them: a burst of
-// buffer loads would stall this wave's in-order instruction stream behind the
-// memory pipeline and leave the matrix cores idle.  Load q0+q goes out after
-// every MB*NB/NQ MFMAs.
-template <int NQ, int BMt, int BNt>
-__device__ __forceinline__ void mfma_step_dma(f32x16_t (&acc)[BMt / 64][BNt / 64],
-                                              const Frags<BMt / 64, BNt / 64> &f, int sl,
-                                              const SliceSrc &src, uint32_t lbase, int k0, int q0)
+// The MFMAs of one k-step; with IS_B < 2, NQ loads (q0 + 0 .. q0 + NQ-1) of A
+// (IS_B = 0) or B (IS_B = 1) go out one after every MB*NB/NQ MFMAs.
+template <int IS_B, int NQ, int BMt, int BNt>
+__device__ __forceinline__ void mfma_step(f32x16_t (&acc)[BMt / 64][BNt / 64], const Frags<BMt / 64, BNt / 64> &f,
+                                          int sl, const SliceSrc &src, uint32_t slot, int k0, int q0)
 {
     constexpr int MB = BMt / 64, NB = BNt / 64, TOT = MB * NB;
     static_assert(NQ == 0 || TOT % NQ == 0, "even spread");
@@ -304,7 +278,8 @@ __device__ __forceinline__ void mfma_step_dma(f32x16_t (&acc)[BMt / 64][BNt / 64
         if constexpr (NQ > 0) {
             if (t % (TOT / NQ) == 0) {
                 __builtin_amdgcn_sched_barrier(0);
-                issue_one<BMt, BNt>(src, lbase, k0, q0 + t / (TOT / NQ));
+                if (IS_B) issue_b<BNt>(src, slot, k0, q0 + t / (TOT / NQ));
+                else issue_a<BMt>(src, slot, k0, q0 + t / (TOT / NQ));
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
@@ -360,15 +335,16 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ offset
               const uint16_t *__restrict__ W, int64_t w_stride, int up_off,
               uint16_t *__restrict__ C, int32_t *__restrict__ tile_cnt, float *__restrict__ partials)
 {
-    constexpr int STAGE = (BMt + BNt) * CPR;        // 16-byte chunks per slice
-    constexpr int A_INS = BMt / RPI / 4, B_INS = BNt / RPI / 4, INS = A_INS + B_INS;
+    constexpr int A_STAGE = BMt * CPR, B_STAGE = BNt * CPR;  // 16-byte chunks per slot
+    constexpr int A_INS = BMt / RPI / 4, B_INS = BNt / RPI / 4;
     constexpr int MB = BMt / 64;                    // 32-row blocks per wave
     constexpr int NB = BNt / 64;                    // 32-col blocks per wave (gate+up when gated)
     constexpr int OUTN = GATED ? BNt / 2 : BNt;     // output columns per tile
-    static_assert(A_INS % 2 == 0 && B_INS % 2 == 0, "swizzle parity assumes even counts");
-    static_assert(BMt * OUTN * 2 <= NSTAGE * STAGE * 16, "epilogue staging must fit the ring");
+    constexpr int RING = A_SLOTS * A_STAGE + B_SLOTS * B_STAGE;
+    static_assert(A_INS == 8 && B_INS == 8, "4 loads under each of the 4 k-steps");
+    static_assert(BMt * OUTN * 2 <= RING * 16, "epilogue staging must fit the rings");
     static_assert(MB * NB * 16 * 256 == SLOT_FLOATS, "partial slot layout");
-    __shared__ uint4 ring[NSTAGE * STAGE];
+    __shared__ uint4 ring[RING];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
@@ -384,11 +360,12 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ offset
     // instruction's rows, LDS position lane%CPR, global chunk
     // (lane%CPR) ^ swz(row); swz depends on the instruction only through its
     // parity, so two byte offsets cover every instruction.
-    const int lrow = lane >> 2;
-    const int pbase = (lane & 3) ^ ((lane >> 3) & 3);
-    const uint32_t voff0 = (uint32_t)(lrow * K + ((pbase ^ (lane >> 5)) * 8)) * 2u;
-    const uint32_t voff1 = (uint32_t)(lrow * K + ((pbase ^ ((lane >> 5) | 2)) * 8)) * 2u;
+    const int lrow = lane >> 3;
+    const uint32_t voff0 = (uint32_t)(lrow * K + (((lane & 7) ^ lrow) * 8)) * 2u;
+    const uint32_t voff1 = (uint32_t)(lrow * K + (((lane & 7) ^ lrow ^ 1) * 8)) * 2u;
     const uint32_t ring_base = lds_addr(ring);
+    const uint4 *const a_ring = ring;
+    const uint4 *const b_ring = ring + A_SLOTS * A_STAGE;
 
     // this lane's LDS rows for its MFMA fragments
     int arow[MB], brow[NB];
@@ -399,9 +376,9 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ offset
         if (GATED) {
             // first NB/2 blocks: gate rows; last NB/2: the matching up rows
             const int jj = j % (NB / 2);
-            brow[j] = BMt + (j < NB / 2 ? 0 : BNt / 2) + wn * (BNt / 4) + jj * 32 + (lane & 31);
+            brow[j] = (j < NB / 2 ? 0 : BNt / 2) + wn * (BNt / 4) + jj * 32 + (lane & 31);
         } else {
-            brow[j] = BMt + wn * (BNt / 2) + j * 32 + (lane & 31);
+            brow[j] = wn * (BNt / 2) + j * 32 + (lane & 31);
         }
     }
 
@@ -454,72 +431,65 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ offset
             for (int j = 0; j < NB; ++j) acc[i][j] = f32x16_t{};
         Frags<MB, NB> f;
 
-        // Ring schedule over slices klo..khi-1 (slice j in slot (j-klo) % NSTAGE).
-        // While slice s is consumed, its k-step 0 MFMAs carry the second half
-        // of slice s+NSTAGE-2's loads and its k-step 1 MFMAs the first half of
-        // slice s+NSTAGE-1's (into the slot that slice s-1 just freed).
-        constexpr int HALF = INS / 2;
+        // Slices klo..khi-1 (local index j): A(j) in A slot j % 2, B(j) in B
+        // slot j % 3.  Under slice s go out A(s+1) (k-steps 0-1) and B(s+2)
+        // (k-steps 2-3), into the slots that slice s-1 freed.
         const int ns = khi - klo;  // slices in this piece (>= 1)
-        int s = 0, cur = 0;
-        auto slot_addr = [&](int j) { return ring_base + (uint32_t)((j % NSTAGE) * STAGE * 16); };
         auto kof = [&](int j) { return (klo + j) * BIG_BK; };
-        auto begin_slice = [&]() {
-            load_frags(f, 1, ring + cur * STAGE, 1, arow, brow);
-            __builtin_amdgcn_sched_barrier(0);
-        };
-        // hand over to slice s+1: wait until it has landed, publish it, read its first fragments
-        auto hand_over = [&]() {
-            const int last_full = s + NSTAGE - 2 < ns - 1 ? s + NSTAGE - 2 : ns - 1;
-            wait_dma<INS>(last_full - (s + 1));
-            lds_barrier();
-            load_frags(f, 0, ring + (cur + 1 == NSTAGE ? 0 : cur + 1) * STAGE, 0, arow, brow);
-            __builtin_amdgcn_sched_barrier(0);
-        };
-        if (ns >= NSTAGE) {
-            // prologue: slices 0..NSTAGE-3 whole, the first half of NSTAGE-2
-            for (int q = 0; q < NSTAGE - 2; ++q) issue_slice<BMt, BNt>(src, slot_addr(q), kof(q));
-            for (int q = 0; q < HALF; ++q) issue_one<BMt, BNt>(src, slot_addr(NSTAGE - 2), kof(NSTAGE - 2), q);
-            asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"((NSTAGE - 3) * INS + HALF) : "memory");
-            lds_barrier();
-            load_frags(f, 0, ring, 0, arow, brow);
-            // steady state: both halves go out
-            for (; s + NSTAGE - 1 < ns; ++s) {
-                begin_slice();
-                mfma_step_dma<INS - HALF, BMt, BNt>(acc, f, 0, src, slot_addr(s + NSTAGE - 2),
-                                                     kof(s + NSTAGE - 2), HALF);
-                __builtin_amdgcn_sched_barrier(0);
-                hand_over();
-                mfma_step_dma<HALF, BMt, BNt>(acc, f, 1, src, slot_addr(s + NSTAGE - 1),
-                                              kof(s + NSTAGE - 1), 0);
-                __builtin_amdgcn_sched_barrier(0);
-                cur = cur + 1 == NSTAGE ? 0 : cur + 1;
-            }
-            // the newest slice still owes its second half
-            begin_slice();
-            mfma_step_dma<INS - HALF, BMt, BNt>(acc, f, 0, src, slot_addr(s + NSTAGE - 2),
-                                                 kof(s + NSTAGE - 2), HALF);
-            __builtin_amdgcn_sched_barrier(0);
-            hand_over();
-            mfma_step(acc, f, 1);
-            __builtin_amdgcn_sched_barrier(0);
-            cur = cur + 1 == NSTAGE ? 0 : cur + 1;
-            ++s;
+        auto a_slot = [&](int j) { return ring_base + (uint32_t)((j % A_SLOTS) * A_STAGE * 16); };
+        auto b_slot = [&](int j) { return ring_base + (uint32_t)((A_SLOTS * A_STAGE + (j % B_SLOTS) * B_STAGE) * 16); };
+        auto a_ptr = [&](int j) { return a_ring + (j % A_SLOTS) * A_STAGE; };
+        auto b_ptr = [&](int j) { return b_ring + (j % B_SLOTS) * B_STAGE; };
+        // prologue: B(0), A(0), B(1); wait for the first two
+#pragma unroll
+        for (int q = 0; q < B_INS; ++q) issue_b<BNt>(src, b_slot(0), kof(0), q);
+#pragma unroll
+        for (int q = 0; q < A_INS; ++q) issue_a<BMt>(src, a_slot(0), kof(0), q);
+        if (ns > 1) {
+#pragma unroll
+            for (int q = 0; q < B_INS; ++q) issue_b<BNt>(src, b_slot(1), kof(1), q);
+            asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(B_INS) : "memory");
         } else {
-            for (int q = 0; q < ns; ++q) issue_slice<BMt, BNt>(src, slot_addr(q), kof(q));
-            wait_dma<INS>(ns - 1);
-            lds_barrier();
-            load_frags(f, 0, ring, 0, arow, brow);
+            asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
         }
-        // drain: no more loads
-        for (; s < ns; ++s) {
-            begin_slice();
-            mfma_step(acc, f, 0);
+        lds_barrier();
+        load_frags(f, 0, a_ptr(0), b_ptr(0), 0, arow, brow);
+
+        // One slice.  HAVE_A: A(s+1) exists; HAVE_B: B(s+2) exists; A and B
+        // loads absent at the tail keep the MFMA runs free of branches.
+        auto slice = [&](int s, auto have_a, auto have_b) {
+            constexpr bool HA = decltype(have_a)::value, HB = decltype(have_b)::value;
+            const uint4 *sa = a_ptr(s), *sb = b_ptr(s);
+            load_frags(f, 1, sa, sb, 1, arow, brow);
             __builtin_amdgcn_sched_barrier(0);
-            if (s + 1 < ns) hand_over();
-            mfma_step(acc, f, 1);
+            mfma_step<0, HA ? A_INS / 2 : 0, BMt, BNt>(acc, f, 0, src, a_slot(s + 1), kof(s + 1), 0);
             __builtin_amdgcn_sched_barrier(0);
-            cur = cur + 1 == NSTAGE ? 0 : cur + 1;
-        }
+            load_frags(f, 0, sa, sb, 2, arow, brow);
+            __builtin_amdgcn_sched_barrier(0);
+            mfma_step<0, HA ? A_INS / 2 : 0, BMt, BNt>(acc, f, 1, src, a_slot(s + 1), kof(s + 1), A_INS / 2);
+            __builtin_amdgcn_sched_barrier(0);
+            load_frags(f, 1, sa, sb, 3, arow, brow);
+            __builtin_amdgcn_sched_barrier(0);
+            mfma_step<1, HB ? B_INS / 2 : 0, BMt, BNt>(acc, f, 0, src, b_slot(s + 2), kof(s + 2), 0);
+            __builtin_amdgcn_sched_barrier(0);
+            if (HA) {
+                // hand over to slice s+1: A(s+1) and B(s+1) have landed when at
+                // most the B(s+2) loads just issued are outstanding
+                if (HB) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(B_INS / 2) : "memory");
+                else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+                lds_barrier();
+                load_frags(f, 0, a_ptr(s + 1), b_ptr(s + 1), 0, arow, brow);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            mfma_step<1, HB ? B_INS / 2 : 0, BMt, BNt>(acc, f, 1, src, b_slot(s + 2), kof(s + 2), B_INS / 2);
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        using T_ = std::true_type;
+        using F_ = std::false_type;
+        int s = 0;
+        for (; s + 2 < ns; ++s) slice(s, T_{}, T_{});
+        if (s + 1 < ns) slice(s++, T_{}, F_{});
+        slice(s, F_{}, F_{});
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         lds_barrier();  // every wave is done with the ring before it is reused
 
@@ -678,7 +648,7 @@ struct FfnLayout {
     size_t off_cnt, off_part, off_h, total;
     FfnLayout(int64_t cap, int El, int H, int Is)
     {
-        const bool big = (H % BIG_BK == 0) && (Is % BIG_BK == 0);
+        const bool big = (H % BIG_BK == 0) && (Is % BIG_BK == 0) && H >= 2 * BIG_BK && Is >= 2 * BIG_BK;
         bm = big ? BIGM : BM;
         max_mtiles = ceil_div(cap, bm) + El;
         t_gu = max_mtiles * ceil_div(Is, big ? BIGN / 2 : BN);
