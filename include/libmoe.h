@@ -108,23 +108,30 @@ moe_status moe_permute(const int32_t *topk_ids, int64_t T, int k, int E, int exp
 
 /*
  * Grouped SwiGLU expert FFN (Sec. 3.1 weight shapes).  For every local
- * expert e and every row r in [offsets[e], offsets[e+1]):
- *   g = x_perm[r] . W13[e, 0:I_s]^T,   u = x_perm[r] . W13[e, I_s:2*I_s]^T
+ * expert e and every row r in [offsets[e], offsets[e+1]), with input row
+ *   in_r = x[row_to_pair[r] / k]   when row_to_pair is not NULL (x is the
+ *          token matrix [x_rows, H]: the permutation's row gather is done by
+ *          the GEMM's operand loads, so no permuted copy is materialised), or
+ *   in_r = x[r]                    when row_to_pair is NULL (x is an already
+ *          permuted buffer such as moe_permute's x_perm, x_rows >= cap_rows):
+ *   g = in_r . W13[e, 0:I_s]^T,   u = in_r . W13[e, I_s:2*I_s]^T
  *   h = silu(g) * u  (fp32, then rounded to bf16)
  *   y[r] = h . W2[e]^T  (fp32 accumulation, rounded to bf16)
- *   x_perm [cap_rows, H] bf16;  offsets [El + 1] int32 (as moe_permute
- *   writes them; rows beyond cap_rows are never touched even if offsets
- *   claim them);  w13 [El, 2*I_s, H] bf16;  w2 [El, H, I_s] bf16;
- *   y [cap_rows, H] bf16 out (rows >= offsets[El] untouched).
+ *   offsets [El + 1] int32 (as moe_permute writes them; rows beyond cap_rows
+ *   are never touched even if offsets claim them);  row_to_pair [cap_rows]
+ *   int32 (entries must lie in [0, x_rows*k));  w13 [El, 2*I_s, H] bf16;
+ *   w2 [El, H, I_s] bf16;  y [cap_rows, H] bf16 out (rows >= offsets[El]
+ *   untouched).
  * Experts with no rows read none of their weights.
  * workspace: at least moe_ffn_workspace_size(cap_rows, El, H, I_s) bytes,
- * 256-byte aligned (holds the bf16 intermediate h and the tile schedule).
+ * 256-byte aligned (holds the bf16 intermediate h, the tile schedule and the
+ * split-K partials).
  */
 size_t moe_ffn_workspace_size(int64_t cap_rows, int n_local_experts, int H, int I_s);
-moe_status moe_grouped_ffn(const uint16_t *x_perm, const int32_t *offsets, int n_local_experts,
-                           int64_t cap_rows, int H, int I_s, const uint16_t *w13,
-                           const uint16_t *w2, uint16_t *y, void *workspace,
-                           size_t workspace_bytes, void *stream);
+moe_status moe_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *row_to_pair, int k,
+                           const int32_t *offsets, int n_local_experts, int64_t cap_rows, int H,
+                           int I_s, const uint16_t *w13, const uint16_t *w2, uint16_t *y,
+                           void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * Combine (unpermute and gate-weighted reduce).  For every token t:

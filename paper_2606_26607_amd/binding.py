@@ -53,7 +53,7 @@ def lib():
         "moe_permute_workspace_size": ([i64, i32, i32], sz),
         "moe_permute": ([vp, i64, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, vp, vp, sz, vp], i32),
         "moe_ffn_workspace_size": ([i64, i32, i32, i32], sz),
-        "moe_grouped_ffn": ([vp, vp, i32, i64, i32, i32, vp, vp, vp, vp, sz, vp], i32),
+        "moe_grouped_ffn": ([vp, i64, vp, i32, vp, i32, i64, i32, i32, vp, vp, vp, vp, sz, vp], i32),
         "moe_combine": ([vp, i64, vp, vp, i64, i32, i32, vp, i64, i64, i32, vp, vp], i32),
         "moe_timing_enable": ([i32], i32),
         "moe_timing_reset": ([], i32),
@@ -144,29 +144,43 @@ def permute(topk_ids: torch.Tensor, E: int, expert_begin: int, n_local: int,
     return o
 
 
-def grouped_ffn(x_perm: torch.Tensor, offsets: torch.Tensor, w13: torch.Tensor, w2: torch.Tensor,
+def grouped_ffn(x: torch.Tensor, offsets: torch.Tensor, w13: torch.Tensor, w2: torch.Tensor,
+                row_to_pair: Optional[torch.Tensor] = None, k: int = 1, cap_rows: Optional[int] = None,
                 y: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
                 stream=None) -> torch.Tensor:
-    _need(x_perm, torch.bfloat16, "x_perm", 2)
+    """SwiGLU expert FFN over the expert row blocks given by `offsets`.
+
+    Without `row_to_pair`, `x` is an already permuted [cap_rows, H] buffer.
+    With it, `x` is the token matrix and row r's input is
+    x[row_to_pair[r] // k] (the row gather is fused into the GEMM).
+    """
+    _need(x, torch.bfloat16, "x", 2)
     _need(offsets, torch.int32, "offsets", 1)
     _need(w13, torch.bfloat16, "w13", 3)
     _need(w2, torch.bfloat16, "w2", 3)
-    cap, H = x_perm.shape
+    x_rows, H = x.shape
+    if row_to_pair is not None:
+        _need(row_to_pair, torch.int32, "row_to_pair", 1)
+        cap = row_to_pair.numel() if cap_rows is None else cap_rows
+        if row_to_pair.numel() < cap:
+            raise ValueError("row_to_pair must hold cap_rows entries")
+    else:
+        cap = x_rows if cap_rows is None else cap_rows
     El = offsets.numel() - 1
     I_s = w2.shape[2]
     if tuple(w13.shape) != (El, 2 * I_s, H) or tuple(w2.shape) != (El, H, I_s):
         raise ValueError(f"weight shapes {tuple(w13.shape)}, {tuple(w2.shape)} do not match "
                          f"El={El}, H={H}, I_s={I_s}")
     if y is None:
-        y = torch.empty((cap, H), dtype=torch.bfloat16, device=x_perm.device)
+        y = torch.empty((max(cap, 1), H), dtype=torch.bfloat16, device=x.device)
     _need(y, torch.bfloat16, "y", 2)
     if y.shape[0] < cap or y.shape[1] != H:
         raise ValueError("y must be [cap_rows, H]")
     if workspace is None:
-        workspace = torch.empty(ffn_workspace_size(cap, El, H, I_s), dtype=torch.uint8,
-                                device=x_perm.device)
-    _check(lib().moe_grouped_ffn(_ptr(x_perm), _ptr(offsets), El, cap, H, I_s, _ptr(w13), _ptr(w2),
-                                 _ptr(y), _ptr(workspace), workspace.numel(), _stream(stream)))
+        workspace = torch.empty(ffn_workspace_size(cap, El, H, I_s), dtype=torch.uint8, device=x.device)
+    _check(lib().moe_grouped_ffn(_ptr(x), x_rows, _ptr(row_to_pair), k, _ptr(offsets), El, cap, H, I_s,
+                                 _ptr(w13), _ptr(w2), _ptr(y), _ptr(workspace), workspace.numel(),
+                                 _stream(stream)))
     return y
 
 
@@ -239,7 +253,6 @@ class MoeLayer:
             "offsets": torch.empty(self.El + 1, dtype=torch.int32, device=dev),
             "row_to_pair": torch.empty(cap1, dtype=torch.int32, device=dev),
             "pair_to_row": torch.empty(max(T * k, 1), dtype=torch.int32, device=dev),
-            "x_perm": torch.empty((cap1, self.H), dtype=torch.bfloat16, device=dev),
         }
         self.ws_perm = torch.empty(max(permute_workspace_size(T, k, self.El), 256), dtype=torch.uint8,
                                    device=dev)
@@ -258,10 +271,11 @@ class MoeLayer:
 
     def forward(self, x: torch.Tensor, logits: torch.Tensor, stream=None) -> torch.Tensor:
         route(logits, self.k, self.topk_ids, self.topk_w, stream=stream)
-        permute(self.topk_ids, self.E, self.e0, self.El, x=x, out=self.bufs, workspace=self.ws_perm,
+        # the permutation's row gather is fused into the gate-up GEMM
+        permute(self.topk_ids, self.E, self.e0, self.El, out=self.bufs, workspace=self.ws_perm,
                 stream=stream)
-        grouped_ffn(self.bufs["x_perm"], self.bufs["offsets"], self.w13, self.w2, y=self.y,
-                    workspace=self.ws_ffn, stream=stream)
+        grouped_ffn(x, self.bufs["offsets"], self.w13, self.w2, row_to_pair=self.bufs["row_to_pair"],
+                    k=self.k, cap_rows=self.cap, y=self.y, workspace=self.ws_ffn, stream=stream)
         shared_y = None
         if self.sc:
             grouped_ffn(x[self.sb:self.sb + self.sc], self.s_offsets, self.sw13, self.sw2, y=self.s_y,

@@ -64,7 +64,7 @@ extern "C" const char *moe_status_str(int status)
 
 extern "C" const char *moe_last_error(void) { return g_msg; }
 
-extern "C" int moe_version(void) { return 1; }
+extern "C" int moe_version(void) { return 2; }
 
 extern "C" moe_status moe_route(const float *logits, int64_t T, int E, int k, int32_t *topk_ids,
                                 float *topk_w, void *stream)
@@ -120,10 +120,11 @@ extern "C" size_t moe_ffn_workspace_size(int64_t cap_rows, int n_local_experts, 
     return ffn_workspace_bytes(cap_rows, n_local_experts, H, I_s);
 }
 
-extern "C" moe_status moe_grouped_ffn(const uint16_t *x_perm, const int32_t *offsets,
-                                      int n_local_experts, int64_t cap_rows, int H, int I_s,
-                                      const uint16_t *w13, const uint16_t *w2, uint16_t *y,
-                                      void *workspace, size_t workspace_bytes, void *stream)
+extern "C" moe_status moe_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *row_to_pair,
+                                      int k, const int32_t *offsets, int n_local_experts,
+                                      int64_t cap_rows, int H, int I_s, const uint16_t *w13,
+                                      const uint16_t *w2, uint16_t *y, void *workspace,
+                                      size_t workspace_bytes, void *stream)
 {
     moe_status st;
     if (n_local_experts < 1) return fail(MOE_ERR_INVALID_ARG, "n_local_experts=%d", n_local_experts);
@@ -131,19 +132,26 @@ extern "C" moe_status moe_grouped_ffn(const uint16_t *x_perm, const int32_t *off
         return fail(MOE_ERR_UNSUPPORTED, "n_local_experts=%d exceeds %d", n_local_experts, MOE_MAX_EXPERTS);
     if (cap_rows < 0) return fail(MOE_ERR_INVALID_ARG, "cap_rows=%lld", (long long)cap_rows);
     if (cap_rows >= ((int64_t)1 << 31)) return fail(MOE_ERR_UNSUPPORTED, "cap_rows too large");
+    if (x_rows < 0) return fail(MOE_ERR_INVALID_ARG, "x_rows=%lld", (long long)x_rows);
     if ((st = check_width("H", H)) != MOE_OK) return st;
     if ((st = check_width("I_s", I_s)) != MOE_OK) return st;
     if (!offsets) return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn: null offsets");
-    if (cap_rows > 0 && (!x_perm || !w13 || !w2 || !y))
+    if (row_to_pair) {
+        if (k < 1) return fail(MOE_ERR_INVALID_ARG, "k=%d must be >= 1 with row_to_pair", k);
+    } else if (x_rows < cap_rows) {
+        return fail(MOE_ERR_INVALID_ARG, "x_rows=%lld < cap_rows=%lld for a permuted x",
+                    (long long)x_rows, (long long)cap_rows);
+    }
+    if (cap_rows > 0 && (!x || !w13 || !w2 || !y))
         return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn: null pointer");
-    if (!aligned16(x_perm) || !aligned16(w13) || !aligned16(w2) || !aligned16(y))
+    if (!aligned16(x) || !aligned16(w13) || !aligned16(w2) || !aligned16(y))
         return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn: tensors must be 16-byte aligned");
     const size_t need = moe_ffn_workspace_size(cap_rows, n_local_experts, H, I_s);
     if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u))
         return fail(MOE_ERR_WORKSPACE, "moe_grouped_ffn: workspace %zu < %zu bytes or misaligned",
                     workspace_bytes, need);
-    return hip_status(launch_grouped_ffn(x_perm, offsets, n_local_experts, cap_rows, H, I_s, w13, w2,
-                                         y, workspace, (hipStream_t)stream),
+    return hip_status(launch_grouped_ffn(x, x_rows, row_to_pair, k, offsets, n_local_experts, cap_rows,
+                                         H, I_s, w13, w2, y, workspace, (hipStream_t)stream),
                       "moe_grouped_ffn launch");
 }
 

@@ -61,6 +61,7 @@ __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restric
 // BMxBN tile (two accumulators when gated).
 template <bool GATED>
 __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t *__restrict__ A,
+                                                   const int32_t *__restrict__ row_index, int kdiv,
                                                    const int32_t *__restrict__ offsets,
                                                    const int32_t *__restrict__ tile_prefix, int El,
                                                    int64_t cap, int N, int K,
@@ -97,7 +98,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t *__restrict__ 
                 const int64_t gr = r0 + row;
                 const int kk = k0 + kc * 8;
                 uint4 v = {0u, 0u, 0u, 0u};
-                if (gr < r1 && kk < K) v = *reinterpret_cast<const uint4 *>(A + gr * K + kk);
+                if (gr < r1 && kk < K) {
+                    const int64_t src_row = row_index ? (int64_t)(row_index[gr] / kdiv) : gr;
+                    v = *reinterpret_cast<const uint4 *>(A + src_row * K + kk);
+                }
                 As[row * KCH + (kc ^ (row & 7))] = v;
             }
             for (int c = tid; c < BROWS * KCH; c += 256) {
@@ -215,30 +219,33 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p)
     return (uint32_t)(uintptr_t)(lds_ptr_t)(const_cast<void *>(p));
 }
 
+// Per-tile DMA sources.  Every row offset is in the per-lane VGPR offset,
+// never in the SGPR offset: the buffer range check covers the VGPR offset,
+// so a row past the expert's end (A) or past N (B) is given the offset
+// num_records and reads as zeros instead of touching memory beyond the
+// operand.  The SGPR offset carries only the slice's K position within a row.
 struct SliceSrc {
     i32x4_t ra, rb;
-    uint32_t voff0, voff1;
-    int wave, brow0, K;
+    uint32_t voa[8], vob[8];  // per DMA instruction q: this lane's row/chunk byte offset
+    int wave;
 };
 
 // DMA instruction q of this wave for one BK-slice of A (or of B) into a ring
 // slot.  Instruction g of the operand tile fills LDS rows RPI*g .. RPI*g+RPI-1;
-// lane i carries row RPI*g + i/CPR, LDS position i%CPR, i.e. global chunk
-// (i%CPR) ^ swz(row), which depends on g only through its parity.
+// lane i carries row RPI*g + i/CPR at LDS position i%CPR, holding global
+// chunk (i%CPR) ^ swz(row).
 template <int BMt>
 __device__ __forceinline__ void issue_a(const SliceSrc &a, uint32_t slot, int k0, int q)
 {
     constexpr int A_INS = BMt / RPI / 4;
-    const int g = a.wave * A_INS + q;
-    dma16(a.ra, slot + g * 1024, (q & 1) ? a.voff1 : a.voff0, (uint32_t)(g * RPI * a.K + k0) * 2u);
+    dma16(a.ra, slot + (a.wave * A_INS + q) * 1024, a.voa[q], (uint32_t)k0 * 2u);
 }
 
 template <int BNt>
 __device__ __forceinline__ void issue_b(const SliceSrc &a, uint32_t slot, int k0, int q)
 {
     constexpr int B_INS = BNt / RPI / 4;
-    const int g = a.wave * B_INS + q;
-    dma16(a.rb, slot + g * 1024, (q & 1) ? a.voff1 : a.voff0, (uint32_t)((a.brow0 + q * RPI) * a.K + k0) * 2u);
+    dma16(a.rb, slot + (a.wave * B_INS + q) * 1024, a.vob[q], (uint32_t)k0 * 2u);
 }
 
 template <int MB, int NB>
@@ -330,7 +337,8 @@ struct WorkSplit {
 
 template <int BMt, int BNt, bool GATED>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
-void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ offsets,
+void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ row_index, int kdiv,
+              int64_t a_rows, const int32_t *__restrict__ offsets,
               const int32_t *__restrict__ tile_prefix, int El, int64_t cap, int N, int K,
               const uint16_t *__restrict__ W, int64_t w_stride, int up_off,
               uint16_t *__restrict__ C, int32_t *__restrict__ tile_cnt, float *__restrict__ partials)
@@ -361,8 +369,6 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ offset
     // (lane%CPR) ^ swz(row); swz depends on the instruction only through its
     // parity, so two byte offsets cover every instruction.
     const int lrow = lane >> 3;
-    const uint32_t voff0 = (uint32_t)(lrow * K + (((lane & 7) ^ lrow) * 8)) * 2u;
-    const uint32_t voff1 = (uint32_t)(lrow * K + (((lane & 7) ^ lrow ^ 1) * 8)) * 2u;
     const uint32_t ring_base = lds_addr(ring);
     const uint4 *const a_ring = ring;
     const uint4 *const b_ring = ring + A_SLOTS * A_STAGE;
@@ -419,10 +425,32 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ offset
 
         // this wave's B rows lie in one part (gate or up) when gated
         const int bpart = GATED ? ((wave * B_INS * RPI) / (BNt / 2)) : 0;
-        const SliceSrc src{buffer_desc(A + r0 * K, (r1 - r0) * K * 2),
-                           buffer_desc(We + (int64_t)((GATED && bpart) ? up_off + n0 : n0) * K,
-                                       (int64_t)nvalid * K * 2),
-                           voff0, voff1, wave, wave * B_INS * RPI - bpart * (BNt / 2), K};
+        const int brow0 = wave * B_INS * RPI - bpart * (BNt / 2);  // first B row of this wave in its part
+        SliceSrc src;
+        src.wave = wave;
+        // A rows come from the permuted buffer (rows r0.. contiguous) or, with
+        // row_index, straight from the token matrix (the fused row gather)
+        const int64_t a_bytes = row_index ? a_rows * K * 2 : (r1 - r0) * K * 2;
+        src.ra = buffer_desc(row_index ? A : A + r0 * K, a_bytes);
+        const int64_t b_bytes = (int64_t)nvalid * K * 2;
+        src.rb = buffer_desc(We + (int64_t)((GATED && bpart) ? up_off + n0 : n0) * K, b_bytes);
+#pragma unroll
+        for (int q = 0; q < A_INS; ++q) {
+            const int trow = (wave * A_INS + q) * RPI + lrow;     // row of the tile
+            const int kc = (lane & 7) ^ lrow ^ (q & 1);           // global chunk: position ^ swz(row)
+            const int64_t r = r0 + trow;
+            int64_t off;
+            if (r >= r1) off = a_bytes;                            // past the expert: zeros
+            else if (row_index) off = ((int64_t)(row_index[r] / kdiv) * K + kc * 8) * 2;
+            else off = ((int64_t)trow * K + kc * 8) * 2;
+            src.voa[q] = (uint32_t)off;
+        }
+#pragma unroll
+        for (int q = 0; q < B_INS; ++q) {
+            const int prow = brow0 + q * RPI + lrow;              // row within its part
+            const int kc = (lane & 7) ^ lrow ^ (q & 1);
+            src.vob[q] = prow < nvalid ? (uint32_t)(((int64_t)prow * K + kc * 8) * 2) : (uint32_t)b_bytes;
+        }
 
         f32x16_t acc[MB][NB];
 #pragma unroll
@@ -674,9 +702,10 @@ size_t ffn_workspace_bytes(int64_t cap, int El, int H, int Is)
     return FfnLayout(cap, El, H, Is).total;
 }
 
-hipError_t launch_grouped_ffn(const uint16_t *x_perm, const int32_t *offsets, int El, int64_t cap,
-                              int H, int Is, const uint16_t *w13, const uint16_t *w2, uint16_t *y,
-                              void *ws, hipStream_t s)
+hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *row_index, int kdiv,
+                              const int32_t *offsets, int El, int64_t cap, int H, int Is,
+                              const uint16_t *w13, const uint16_t *w2, uint16_t *y, void *ws,
+                              hipStream_t s)
 {
     if (cap == 0) return hipSuccess;
     const FfnLayout L(cap, El, H, Is);
@@ -685,11 +714,14 @@ hipError_t launch_grouped_ffn(const uint16_t *x_perm, const int32_t *offsets, in
     int32_t *cnt = reinterpret_cast<int32_t *>(base + L.off_cnt);
     float *partials = reinterpret_cast<float *>(base + L.off_part);
     uint16_t *h = reinterpret_cast<uint16_t *>(base + L.off_h);
-    const bool big = L.bm == BIGM;
+    // the large-tile kernel addresses operands with 32-bit buffer offsets
+    const int64_t lim = ((int64_t)1 << 32) - 4 * (int64_t)(H > Is ? H : Is);
+    const bool big = L.bm == BIGM && (row_index ? x_rows : cap) * (int64_t)H * 2 < lim &&
+                     (int64_t)BIGM * Is * 2 < lim;
     hipError_t err;
     {
         KernelTimer timer(MOE_K_SCHEDULE, s);
-        schedule_kernel<<<dim3(1), dim3(1024), 0, s>>>(offsets, El, cap, L.bm, tile_prefix, cnt,
+        schedule_kernel<<<dim3(1), dim3(1024), 0, s>>>(offsets, El, cap, big ? BIGM : BM, tile_prefix, cnt,
                                                        big ? L.t_gu + L.t_dn : 0);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
@@ -697,31 +729,36 @@ hipError_t launch_grouped_ffn(const uint16_t *x_perm, const int32_t *offsets, in
         {
             KernelTimer timer(MOE_K_GATE_UP, s);
             gemm_big<BIGM, BIGN, true><<<dim3((unsigned)L.grid_gu), dim3(256), 0, s>>>(
-                x_perm, offsets, tile_prefix, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h, cnt,
-                partials);
+                x, row_index, kdiv, x_rows, offsets, tile_prefix, El, cap, Is, H, w13, (int64_t)2 * Is * H,
+                Is, h, cnt, partials);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         {
             KernelTimer timer(MOE_K_DOWN, s);
             gemm_big<BIGM, BIGN, false><<<dim3((unsigned)L.grid_dn), dim3(256), 0, s>>>(
-                h, offsets, tile_prefix, El, cap, H, Is, w2, (int64_t)H * Is, 0, y, cnt + L.t_gu,
-                partials);
+                h, nullptr, 1, cap, offsets, tile_prefix, El, cap, H, Is, w2, (int64_t)H * Is, 0, y,
+                cnt + L.t_gu, partials);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         return hipSuccess;
     }
+    // general path: tiles of BM rows (the layout sized the tile counters with
+    // the large tiles, which is an upper bound here too)
+    const int64_t mt = ceil_div(cap, BM) + El;
     {
         KernelTimer timer(MOE_K_GATE_UP, s);
-        int64_t grid = L.t_gu < 2048 ? L.t_gu : 2048;
+        int64_t tiles = mt * ceil_div(Is, BN);
+        int64_t grid = tiles < 2048 ? tiles : 2048;
         gemm_kernel<true><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
-            x_perm, offsets, tile_prefix, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h);
+            x, row_index, kdiv, offsets, tile_prefix, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     {
         KernelTimer timer(MOE_K_DOWN, s);
-        int64_t grid = L.t_dn < 2048 ? L.t_dn : 2048;
+        int64_t tiles = mt * ceil_div(H, BN);
+        int64_t grid = tiles < 2048 ? tiles : 2048;
         gemm_kernel<false><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
-            h, offsets, tile_prefix, El, cap, H, Is, w2, (int64_t)H * Is, 0, y);
+            h, nullptr, 1, offsets, tile_prefix, El, cap, H, Is, w2, (int64_t)H * Is, 0, y);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     return hipSuccess;

@@ -84,8 +84,9 @@ def test_ffn_rejects():
     L = moe.lib()
     big = 1 << 30
 
-    def call(xp=FAKE, off=FAKE, El=8, cap=64, H=64, Is=32, w13=FAKE, w2=FAKE, y=FAKE, ws=FAKE, wsb=big):
-        return L.moe_grouped_ffn(xp, off, El, cap, H, Is, w13, w2, y, ws, wsb, None)
+    def call(xp=FAKE, xr=64, r2p=None, k=1, off=FAKE, El=8, cap=64, H=64, Is=32, w13=FAKE, w2=FAKE, y=FAKE,
+             ws=FAKE, wsb=big):
+        return L.moe_grouped_ffn(xp, xr, r2p, k, off, El, cap, H, Is, w13, w2, y, ws, wsb, None)
     assert call(El=0) == INVALID
     assert call(El=1025) == UNSUPPORTED
     assert call(H=12) == UNSUPPORTED
@@ -96,6 +97,9 @@ def test_ffn_rejects():
     assert call(wsb=100) == WORKSPACE
     assert call(ws=ctypes.c_void_p(0x100010)) == WORKSPACE   # not 256-byte aligned
     assert call(xp=ctypes.c_void_p(0x100002)) == INVALID     # not 16-byte aligned
+    assert call(xr=32) == INVALID                            # permuted x shorter than cap_rows
+    assert call(xr=-1) == INVALID
+    assert call(r2p=FAKE, k=0) == INVALID                    # gather without a slot count
 
 
 def test_combine_rejects():

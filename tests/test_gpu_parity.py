@@ -165,10 +165,32 @@ def ffn_case(oracle, El, H, Is, T, k, seed, hot=None):
 
 @pytest.mark.parametrize("El,H,Is,T,k", [(1, 64, 32, 1, 1), (4, 256, 192, 150, 2), (8, 136, 72, 99, 3),
                                          (3, 512, 256, 300, 1), (16, 128, 64, 400, 4),
-                                         (2, 1024, 512, 130, 2)])
+                                         (2, 1024, 512, 130, 2), (5, 384, 320, 611, 3)])
 def test_grouped_ffn_stage(oracle, El, H, Is, T, k):
     got, ref = ffn_case(oracle, El, H, Is, T, k, seed=El * 100 + H)
     assert_close_rel(got, ref, what=f"ffn El={El} H={H} Is={Is}")
+
+
+@pytest.mark.parametrize("El,E,H,Is,T,k,e0", [(4, 4, 256, 192, 150, 2, 0), (3, 8, 512, 256, 300, 2, 2),
+                                              (8, 8, 1024, 512, 257, 2, 0), (2, 16, 136, 72, 99, 3, 6)])
+def test_grouped_ffn_fused_gather(oracle, El, E, H, Is, T, k, e0):
+    """Rows read straight from the token matrix through row_to_pair equal the
+    FFN of the explicitly gathered rows."""
+    ids = mi.random_topk_ids(T, E, k, seed=T + H)
+    _, offs, r2p, _ = oracle.permute(ids, e0, El)
+    n = int(offs[-1])
+    x = mi.random_bf16((T, H), seed=T, tag=44)
+    w13 = mi.random_bf16((El, 2 * Is, H), seed=T, tag=45, std=0.05)
+    w2 = mi.random_bf16((El, H, Is), seed=T, tag=46, std=0.05)
+    cap = T * min(k, El)
+    r2p_dev = torch.full((cap,), -1, dtype=torch.int32)
+    r2p_dev[:n] = torch.from_numpy(r2p)
+    y = moe.grouped_ffn(dev_bf16(x), torch.from_numpy(offs).cuda(), dev_bf16(w13), dev_bf16(w2),
+                        row_to_pair=r2p_dev.cuda(), k=k, cap_rows=cap)
+    torch.cuda.synchronize()
+    got = bf16_f64(host_bf16(y)[:n])
+    ref = oracle.grouped_ffn(x[r2p // k], offs, w13, w2)
+    assert_close_rel(got, ref, what=f"fused El={El} H={H} Is={Is}")
 
 
 def test_grouped_ffn_skewed_and_empty_experts(oracle):
