@@ -41,11 +41,13 @@ def algorithmic_work(cfg, counts: np.ndarray):
     n = int(counts.sum())
     active = int((counts > 0).sum())
     sc = cfg.shared_count
-    gate_up_flops = 4.0 * H * Is * n
-    down_flops = 2.0 * H * Is * n
+    gate_up_flops = 4.0 * H * Is * n + 4.0 * H * cfg.I * sc
+    down_flops = 2.0 * H * Is * n + 2.0 * H * cfg.I * sc
     gate_up_bytes = active * 2 * Is * H * 2 + n * H * 2 + n * Is * 2
+    if sc:  # the shared expert's gate-up: its weights plus its token rows in, h rows out
+        gate_up_bytes += 2 * cfg.I * H * 2 + sc * H * 2 + sc * cfg.I * 2
     down_bytes = active * H * Is * 2 + n * Is * 2 + n * H * 2
-    sh_flops = 6.0 * H * cfg.I * sc
+    sh_flops = 0.0  # already in gate_up_flops / down_flops
     sh_bytes = (3 * cfg.I * H * 2 + sc * H * 4 + sc * cfg.I * 4) if sc else 0
     touched = n  # x rows read once per routed pair by the gather, out written once per token
     step_bytes = (active * 3 * Is * H * 2 + (touched + cfg.T) * H * 2 + sh_bytes)
@@ -200,20 +202,24 @@ def main():
     log("[bench] kernels: " + ", ".join(f"{k}={v['avg_us']:.1f}us x{v['launches']}" for k, v in kern.items()))
 
     decode = cfg.name.startswith("dsv3")
-    # dominant kernel: the gate-up GEMM (2/3 of the flops and of the weight bytes)
-    gu = kern.get("gate_up")
+    # dominant kernel: the gate-up GEMM (2/3 of the flops and of the weight
+    # bytes); its launches per step (the routed experts and, where present,
+    # the shared expert) are summed.  Prefill is priced on MFMA, decode
+    # (a few rows per expert, weights streamed once) on HBM.
+    dom = "gate_up"
+    gu = kern.get(dom)
     if gu is not None:
-        per_launch = gu["launches"] // args.steps or 1
-        dur_s = gu["avg_us"] * 1e-6 * per_launch
+        dur_s = gu["avg_us"] * 1e-6 * gu["launches"] / args.steps   # kernel time per step
         if decode:
             achieved = work["gate_up_bytes"] / dur_s / 1e9
             roof = dict(bound="hbm", achieved=achieved, peak=PEAK_HBM_GBS, unit="GB/s",
-                        frac=achieved / PEAK_HBM_GBS, traffic=measured_traffic(cfg.name), kernel="gate_up",
-                        algorithmic_per_launch=work["gate_up_bytes"])
+                        frac=achieved / PEAK_HBM_GBS, traffic=measured_traffic(cfg.name), kernel=dom,
+                        launches_per_step=gu["launches"] // args.steps,
+                        algorithmic_per_step=work["gate_up_bytes"])
         else:
             achieved = work["gate_up_flops"] / dur_s / 1e12
             roof = dict(bound="mfma", achieved=achieved, peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
-                        frac=achieved / PEAK_BF16_TFLOPS, traffic=measured_traffic(cfg.name), kernel="gate_up",
+                        frac=achieved / PEAK_BF16_TFLOPS, traffic=measured_traffic(cfg.name), kernel=dom,
                         algorithmic_per_launch=work["gate_up_flops"],
                         algorithmic_bytes_per_launch=work["gate_up_bytes"])
     else:

@@ -165,8 +165,8 @@ typedef enum moe_kernel_kind {
     MOE_K_PERMUTE = 1,   /* count + scan + scatter */
     MOE_K_GATHER = 2,    /* x_perm row gather */
     MOE_K_SCHEDULE = 3,  /* grouped-FFN tile schedule */
-    MOE_K_GATE_UP = 4,   /* gate-up GEMM with the SwiGLU epilogue */
-    MOE_K_DOWN = 5,      /* down GEMM (and its split-K reduction) */
+    MOE_K_GATE_UP = 4,   /* gate-up GEMM with the SwiGLU epilogue (both tile classes) */
+    MOE_K_DOWN = 5,      /* down GEMM (both tile classes, split-K reduction included) */
     MOE_K_COMBINE = 6,
     MOE_K_COUNT = 7
 } moe_kernel_kind;

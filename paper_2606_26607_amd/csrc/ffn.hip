@@ -26,24 +26,12 @@ __device__ __forceinline__ int64_t clamp_row(int32_t v, int64_t cap)
     return r > cap ? cap : r;
 }
 
-// tile_prefix[e] = m-tiles (of bm rows) of experts before e; [El] = total.
-// Also clears the stream-K tile counters of the two GEMMs (no memset node is
-// needed, so the chain stays graph-capturable).
-__global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restrict__ offsets, int El,
-                                                        int64_t cap, int bm,
-                                                        int32_t *__restrict__ tile_prefix,
-                                                        int32_t *__restrict__ counters, int64_t n_counters)
+// Block-wide exclusive scan of one value per thread (1024 threads); returns
+// the exclusive prefix and writes the total to *total (thread 1023).
+__device__ __forceinline__ int32_t block_exscan(int32_t v, int32_t *wsum, int32_t *total)
 {
-    __shared__ int32_t wsum[16];
-    const int e = threadIdx.x;
-    for (int64_t i = e; i < n_counters; i += 1024) counters[i] = 0;
-    int32_t mt = 0;
-    if (e < El) {
-        int64_t a = clamp_row(offsets[e], cap), b = clamp_row(offsets[e + 1], cap);
-        mt = b > a ? (int32_t)((b - a + bm - 1) / bm) : 0;
-    }
-    const int lane = e & 63, wv = e >> 6;
-    int32_t incl = mt;
+    const int e = threadIdx.x, lane = e & 63, wv = e >> 6;
+    int32_t incl = v;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
         int32_t o = __shfl_up(incl, off, 64);
@@ -53,8 +41,40 @@ __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restric
     __syncthreads();
     int32_t before = 0;
     for (int i = 0; i < wv; ++i) before += wsum[i];
-    if (e < El) tile_prefix[e] = before + incl - mt;
-    if (e == 1023) tile_prefix[El] = before + incl;
+    if (e == 1023) *total = before + incl;
+    __syncthreads();
+    return before + incl - v;
+}
+
+// Tile schedule of the grouped FFN.  Experts with at most small_max rows go
+// to the small-row kernel (m-tiles of bm_small rows; small_max = 0 disables
+// it), the others to the large-tile kernel (m-tiles of bm rows):
+//   pre[e] / pre_small[e] = m-tiles of that class of the experts before e,
+//   pre[El] / pre_small[El] = totals.
+// Also clears the split-K tile counters (no memset node is needed, so the
+// chain stays graph-capturable).
+__global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restrict__ offsets, int El,
+                                                        int64_t cap, int bm, int bm_small, int small_max,
+                                                        int32_t *__restrict__ pre,
+                                                        int32_t *__restrict__ pre_small,
+                                                        int32_t *__restrict__ counters, int64_t n_counters)
+{
+    __shared__ int32_t wsum[16];
+    const int e = threadIdx.x;
+    for (int64_t i = e; i < n_counters; i += 1024) counters[i] = 0;
+    int32_t mt = 0, mts = 0;
+    if (e < El) {
+        int64_t a = clamp_row(offsets[e], cap), b = clamp_row(offsets[e + 1], cap);
+        const int64_t n = b > a ? b - a : 0;
+        if (n > 0 && n <= small_max) mts = (int32_t)((n + bm_small - 1) / bm_small);
+        else if (n > 0) mt = (int32_t)((n + bm - 1) / bm);
+    }
+    const int32_t x = block_exscan(mt, wsum, &pre[El]);
+    if (e < El) pre[e] = x;
+    if (pre_small) {
+        const int32_t xs = block_exscan(mts, wsum, &pre_small[El]);
+        if (e < El) pre_small[e] = xs;
+    }
 }
 
 // 256 threads = 4 waves in a 2x2 grid, each wave owns a 32x32 block of the
@@ -270,23 +290,28 @@ __device__ __forceinline__ void load_frags(Frags<MB, NB> &f, int sl, const uint4
     }
 }
 
-// The MFMAs of one k-step; with IS_B < 2, NQ loads (q0 + 0 .. q0 + NQ-1) of A
-// (IS_B = 0) or B (IS_B = 1) go out one after every MB*NB/NQ MFMAs.
-template <int IS_B, int NQ, int BMt, int BNt>
-__device__ __forceinline__ void mfma_step(f32x16_t (&acc)[BMt / 64][BNt / 64], const Frags<BMt / 64, BNt / 64> &f,
-                                          int sl, const SliceSrc &src, uint32_t slot, int k0, int q0)
+// The MFMAs of one k-step (MB x NB blocks) with NQ loads of A (IS_B = 0) or
+// B (IS_B = 1), numbered q0 .. q0+NQ-1, spread evenly between them.
+template <int IS_B, int NQ, int MB, int NB, int BMt, int BNt>
+__device__ __forceinline__ void mfma_step(f32x16_t (&acc)[MB][NB], const Frags<MB, NB> &f, int sl,
+                                          const SliceSrc &src, uint32_t slot, int k0, int q0)
 {
-    constexpr int MB = BMt / 64, NB = BNt / 64, TOT = MB * NB;
-    static_assert(NQ == 0 || TOT % NQ == 0, "even spread");
+    constexpr int TOT = MB * NB;
 #pragma unroll
     for (int t = 0; t < TOT; ++t) {
         const int i = t / NB, j = t % NB;
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[sl][i], f.b[sl][j], acc[i][j], 0, 0, 0);
+        constexpr int dummy = 0;
+        (void)dummy;
         if constexpr (NQ > 0) {
-            if (t % (TOT / NQ) == 0) {
+            const int qa = t * NQ / TOT, qb = (t + 1) * NQ / TOT;
+            if (qb > qa) {
                 __builtin_amdgcn_sched_barrier(0);
-                if (IS_B) issue_b<BNt>(src, slot, k0, q0 + t / (TOT / NQ));
-                else issue_a<BMt>(src, slot, k0, q0 + t / (TOT / NQ));
+#pragma unroll
+                for (int q = qa; q < qb; ++q) {
+                    if (IS_B) issue_b<BNt>(src, slot, k0, q0 + q);
+                    else issue_a<BMt>(src, slot, k0, q0 + q);
+                }
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
@@ -299,25 +324,27 @@ __device__ __forceinline__ uint16_t bf16_bits(float f)
     return *reinterpret_cast<uint16_t *>(&h);
 }
 
-// Partial accumulator slot: one fp32 value per accumulator register of each
-// of the 256 threads, stored register-major so each access is a coalesced
-// 16-byte vector per lane.
-constexpr int SLOT_FLOATS = 256 * 256;
+// A partial accumulator slot holds one fp32 value per accumulator register
+// of each of the 256 threads, stored register-major so each access is a
+// coalesced 16-byte vector per lane.
 
-// Work split of one launch over G persistent workgroups.  With at least G
-// tiles every tile is handed out whole, round robin (dp = T): workgroups on
-// one die then walk K in near lockstep over shared panels, which is what
-// keeps the die's L2 effective.  With fewer tiles than workgroups (a few
-// large-K tiles, e.g. one expert's down projection) the K-slices of all
-// tiles are cut into contiguous runs ("stream-K"), so every workgroup gets
-// the same number of slices; partial sums are combined by the last
-// contributor of each tile.
+// Work split of one launch over G persistent workgroups.  By default every
+// tile is handed out whole, round robin (dp = T): workgroups on one die then
+// walk K in near lockstep over shared panels, which is what keeps the die's
+// L2 effective.  With fewer tiles than workgroups and a long K (a few
+// large-K tiles, e.g. one expert's down projection), or always for the
+// weight-streaming small-row kernel (bound by HBM, not by L2 reuse), the
+// K-slices of all tiles are cut into contiguous runs ("stream-K"), so every
+// workgroup gets the same number of slices; partial sums are combined by
+// the last contributor of each tile.
 struct WorkSplit {
     int64_t T, dp, iters;  // tiles, whole tiles, K-slices in the stream-K part
     int nk, G, Gsk;        // slices per tile, workgroups, workgroups in the stream-K part
-    __device__ WorkSplit(int64_t total, int nk_, int g) : T(total), nk(nk_), G(g)
+    __device__ WorkSplit(int64_t total, int nk_, int g, bool split_always) : T(total), nk(nk_), G(g)
     {
-        dp = T >= G ? T : 0;
+        // splitting pays only when a tile has many slices: each split tile
+        // moves its fp32 partial sums through memory once more
+        dp = (split_always || (T < G && nk >= 64)) ? 0 : T;
         iters = (T - dp) * nk;
         // every stream-K workgroup gets at least one slice, so the workgroups
         // that meet a tile are exactly a consecutive range
@@ -335,31 +362,63 @@ struct WorkSplit {
     }
 };
 
-template <int BMt, int BNt, bool GATED>
-__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
-void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ row_index, int kdiv,
-              int64_t a_rows, const int32_t *__restrict__ offsets,
-              const int32_t *__restrict__ tile_prefix, int El, int64_t cap, int N, int K,
-              const uint16_t *__restrict__ W, int64_t w_stride, int up_off,
-              uint16_t *__restrict__ C, int32_t *__restrict__ tile_cnt, float *__restrict__ partials)
+// Operands of one grouped GEMM launch (both tile classes).
+struct GemmArgs {
+    const uint16_t *A;          // activations: token matrix (with row_index) or permuted rows
+    const int32_t *row_index;   // row -> pair index (divided by kdiv gives the token), or null
+    int kdiv;
+    int64_t a_rows;             // rows of A when row_index is given
+    const int32_t *offsets;     // [El+1] expert row ranges
+    int El;
+    int64_t cap;
+    int N, K;                   // output columns (per part when gated), reduction length
+    const uint16_t *W;          // [El] weight blocks of w_stride elements, rows K-contiguous
+    int64_t w_stride;
+    int up_off;                 // first up row when gated
+    uint16_t *C;                // [cap, N] bf16 out
+};
+
+// Per tile class: its m-tile prefix over experts, split-K tile counters and
+// partial slots.
+struct TileClass {
+    const int32_t *tile_prefix;
+    int32_t *tile_cnt;
+    float *partials;
+};
+
+// One tile class (BMt x BNt tiles, WM x (4/WM) waves) of a grouped GEMM,
+// processed by every workgroup of the persistent grid; `ring` is the
+// workgroup's LDS (at least the class's ring size).  Pointers are restrict
+// parameters so that the inlined body keeps the no-alias facts of kernel
+// arguments (its loads are not reordered around the stores it makes).
+template <int BMt, int BNt, bool GATED, int WM, bool SPLIT_ALWAYS>
+__device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restrict__ A,
+                                           const int32_t *__restrict__ row_index, int kdiv, int64_t a_rows,
+                                           const int32_t *__restrict__ offsets,
+                                           const int32_t *__restrict__ tile_prefix, int El, int64_t cap,
+                                           int N, int K, const uint16_t *__restrict__ W, int64_t w_stride,
+                                           int up_off, uint16_t *__restrict__ C,
+                                           int32_t *__restrict__ tile_cnt, float *__restrict__ partials)
 {
     constexpr int A_STAGE = BMt * CPR, B_STAGE = BNt * CPR;  // 16-byte chunks per slot
     constexpr int A_INS = BMt / RPI / 4, B_INS = BNt / RPI / 4;
-    constexpr int MB = BMt / 64;                    // 32-row blocks per wave
-    constexpr int NB = BNt / 64;                    // 32-col blocks per wave (gate+up when gated)
+    constexpr int WN = 4 / WM;                      // waves in a WM x WN grid
+    constexpr int MB = BMt / WM / 32;               // 32-row blocks per wave
+    constexpr int NB = BNt / WN / 32;               // 32-col blocks per wave (gate+up when gated)
     constexpr int OUTN = GATED ? BNt / 2 : BNt;     // output columns per tile
+    static_assert(MB >= 1 && NB >= (GATED ? 2 : 1), "tile too small for the wave grid");
     constexpr int RING = A_SLOTS * A_STAGE + B_SLOTS * B_STAGE;
-    static_assert(A_INS == 8 && B_INS == 8, "4 loads under each of the 4 k-steps");
+    static_assert(A_INS >= 1 && B_INS >= 2 && B_INS % 2 == 0, "DMA instruction split");
     static_assert(BMt * OUTN * 2 <= RING * 16, "epilogue staging must fit the rings");
-    static_assert(MB * NB * 16 * 256 == SLOT_FLOATS, "partial slot layout");
-    __shared__ uint4 ring[RING];
+    constexpr int SLOT = MB * NB * 16 * 256;        // floats per partial slot
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WN, wn = wave % WN;
     const int n_tiles = (N + OUTN - 1) / OUTN;
     const int nk = K / BIG_BK;
-    const WorkSplit ws((int64_t)tile_prefix[El] * n_tiles, nk, gridDim.x);
+    const WorkSplit ws((int64_t)tile_prefix[El] * n_tiles, nk, gridDim.x, SPLIT_ALWAYS);
+    if (ws.T == 0) return;
     // XCD-aware numbering: the 8 dies take workgroups round robin, so the
     // workgroups of one die get consecutive virtual ids and with them a
     // contiguous run of tiles (shared panels in that die's L2).
@@ -376,15 +435,15 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ row_in
     // this lane's LDS rows for its MFMA fragments
     int arow[MB], brow[NB];
 #pragma unroll
-    for (int i = 0; i < MB; ++i) arow[i] = wm * (BMt / 2) + i * 32 + (lane & 31);
+    for (int i = 0; i < MB; ++i) arow[i] = wm * (BMt / WM) + i * 32 + (lane & 31);
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
         if (GATED) {
             // first NB/2 blocks: gate rows; last NB/2: the matching up rows
             const int jj = j % (NB / 2);
-            brow[j] = (j < NB / 2 ? 0 : BNt / 2) + wn * (BNt / 4) + jj * 32 + (lane & 31);
+            brow[j] = (j < NB / 2 ? 0 : BNt / 2) + wn * (BNt / 2 / WN) + jj * 32 + (lane & 31);
         } else {
-            brow[j] = wn * (BNt / 2) + j * 32 + (lane & 31);
+            brow[j] = wn * (BNt / WN) + j * 32 + (lane & 31);
         }
     }
 
@@ -437,7 +496,7 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ row_in
 #pragma unroll
         for (int q = 0; q < A_INS; ++q) {
             const int trow = (wave * A_INS + q) * RPI + lrow;     // row of the tile
-            const int kc = (lane & 7) ^ lrow ^ (q & 1);           // global chunk: position ^ swz(row)
+            const int kc = (lane & 7) ^ lrow ^ ((wave * A_INS + q) & 1);  // position ^ swz(row)
             const int64_t r = r0 + trow;
             int64_t off;
             if (r >= r1) off = a_bytes;                            // past the expert: zeros
@@ -448,7 +507,7 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ row_in
 #pragma unroll
         for (int q = 0; q < B_INS; ++q) {
             const int prow = brow0 + q * RPI + lrow;              // row within its part
-            const int kc = (lane & 7) ^ lrow ^ (q & 1);
+            const int kc = (lane & 7) ^ lrow ^ ((wave * B_INS + q) & 1);  // LDS row (wave*B_INS+q)*RPI+lrow
             src.vob[q] = prow < nvalid ? (uint32_t)(((int64_t)prow * K + kc * 8) * 2) : (uint32_t)b_bytes;
         }
 
@@ -490,15 +549,16 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ row_in
             const uint4 *sa = a_ptr(s), *sb = b_ptr(s);
             load_frags(f, 1, sa, sb, 1, arow, brow);
             __builtin_amdgcn_sched_barrier(0);
-            mfma_step<0, HA ? A_INS / 2 : 0, BMt, BNt>(acc, f, 0, src, a_slot(s + 1), kof(s + 1), 0);
+            mfma_step<0, HA ? A_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 0, src, a_slot(s + 1), kof(s + 1), 0);
             __builtin_amdgcn_sched_barrier(0);
             load_frags(f, 0, sa, sb, 2, arow, brow);
             __builtin_amdgcn_sched_barrier(0);
-            mfma_step<0, HA ? A_INS / 2 : 0, BMt, BNt>(acc, f, 1, src, a_slot(s + 1), kof(s + 1), A_INS / 2);
+            mfma_step<0, HA ? A_INS - A_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 1, src, a_slot(s + 1), kof(s + 1),
+                                                                   A_INS / 2);
             __builtin_amdgcn_sched_barrier(0);
             load_frags(f, 1, sa, sb, 3, arow, brow);
             __builtin_amdgcn_sched_barrier(0);
-            mfma_step<1, HB ? B_INS / 2 : 0, BMt, BNt>(acc, f, 0, src, b_slot(s + 2), kof(s + 2), 0);
+            mfma_step<1, HB ? B_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 0, src, b_slot(s + 2), kof(s + 2), 0);
             __builtin_amdgcn_sched_barrier(0);
             if (HA) {
                 // hand over to slice s+1: A(s+1) and B(s+1) have landed when at
@@ -509,7 +569,8 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ row_in
                 load_frags(f, 0, a_ptr(s + 1), b_ptr(s + 1), 0, arow, brow);
                 __builtin_amdgcn_sched_barrier(0);
             }
-            mfma_step<1, HB ? B_INS / 2 : 0, BMt, BNt>(acc, f, 1, src, b_slot(s + 2), kof(s + 2), B_INS / 2);
+            mfma_step<1, HB ? B_INS - B_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 1, src, b_slot(s + 2), kof(s + 2),
+                                                                   B_INS / 2);
             __builtin_amdgcn_sched_barrier(0);
         };
         using T_ = std::true_type;
@@ -536,10 +597,10 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ row_in
             // flush the operand panels other workgroups on the die are reusing.
             typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
             const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(
-                partials, (short)0, (int)((int64_t)2 * ws.G * SLOT_FLOATS * 4), 0x00020000);
+                partials, (short)0, (int)((int64_t)2 * ws.G * SLOT * 4), 0x00020000);
             constexpr int SC1 = 0x10;
             {
-                const uint32_t base_b = (uint32_t)(slot_of(v) * SLOT_FLOATS * 4);
+                const uint32_t base_b = (uint32_t)(slot_of(v) * SLOT * 4);
 #pragma unroll
                 for (int i = 0; i < MB; ++i)
 #pragma unroll
@@ -573,12 +634,12 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ row_in
             uint16_t *stage_out = reinterpret_cast<uint16_t *>(ring);
             for (int i = 0; i < MB; ++i) {
                 for (int j = 0; j < (GATED ? NB / 2 : NB); ++j) {
-                    const int col = wn * (GATED ? BNt / 4 : BNt / 2) + j * 32 + (lane & 31);
+                    const int col = wn * (OUTN / WN) + j * 32 + (lane & 31);
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
                         float4 g = make_float4(0.f, 0.f, 0.f, 0.f), u = g;
                         for (int c = vfirst; c <= vlast; ++c) {
-                            const uint32_t base_b = (uint32_t)(slot_of(c) * SLOT_FLOATS * 4);
+                            const uint32_t base_b = (uint32_t)(slot_of(c) * SLOT * 4);
                             u32x4_t w = __builtin_amdgcn_raw_buffer_load_b128(
                                 pr, base_b + (uint32_t)((((i * NB + j) * 4 + q) * 256 + tid) * 16), 0, SC1);
                             const float4 pv = *reinterpret_cast<float4 *>(&w);
@@ -593,7 +654,7 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ row_in
                         const float gv[4] = {g.x, g.y, g.z, g.w}, uv[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
-                            const int row = wm * (BMt / 2) + i * 32 + 8 * q + 4 * (lane >> 5) + r;
+                            const int row = wm * (BMt / WM) + i * 32 + 8 * q + 4 * (lane >> 5) + r;
                             float o = gv[r];
                             if (GATED) o = o / (1.0f + __expf(-o)) * uv[r];
                             stage_out[row * OUTN + col] = bf16_bits(o);
@@ -612,10 +673,10 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ row_in
         for (int i = 0; i < MB; ++i) {
 #pragma unroll
             for (int j = 0; j < (GATED ? NB / 2 : NB); ++j) {
-                const int col = wn * (GATED ? BNt / 4 : BNt / 2) + j * 32 + (lane & 31);
+                const int col = wn * (OUTN / WN) + j * 32 + (lane & 31);
 #pragma unroll
                 for (int q = 0; q < 16; ++q) {
-                    const int row = wm * (BMt / 2) + i * 32 + 8 * (q / 4) + 4 * (lane >> 5) + (q % 4);
+                    const int row = wm * (BMt / WM) + i * 32 + 8 * (q / 4) + 4 * (lane >> 5) + (q % 4);
                     float o = acc[i][j][q];
                     if (GATED) o = o / (1.0f + __expf(-o)) * acc[i][j + NB / 2][q];
                     stage_out[row * OUTN + col] = bf16_bits(o);
@@ -651,11 +712,35 @@ void gemm_big(const uint16_t *__restrict__ A, const int32_t *__restrict__ row_in
     }
 }
 
+constexpr int BIGM = 256, BIGN = 256;  // large tiles: 256 rows x 256 weight rows
+constexpr int SMALLM = 32;             // small-row tiles: 32 rows x 256 weight rows
+constexpr int SMALL_MAX = 96;          // experts with at most this many rows use small-row tiles
+constexpr int BIG_RING = (A_SLOTS * BIGM + B_SLOTS * BIGN) * CPR;
+// floats per partial slot of each class (one per accumulator register)
+constexpr int SLOT_SMALL = (SMALLM / 32) * (BIGN / 4 / 32) * 16 * 256;
+constexpr int SLOT_BIG = (BIGM / 2 / 32) * (BIGN / 2 / 32) * 16 * 256;
+
+// One grouped GEMM launch: the small-row experts first (32-row tiles,
+// K-split over the whole grid: these stream weights, and spreading them over
+// every CU is what reaches HBM bandwidth), then the large-row experts (256-row
+// tiles) in the same persistent grid.  The classes cover disjoint experts, so
+// a workgroup goes on to the second without waiting for the first.
+template <bool GATED>
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
+void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
+{
+    __shared__ uint4 ring[BIG_RING];
+    gemm_class<SMALLM, BIGN, GATED, 1, true>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets,
+                                             small.tile_prefix, g.El, g.cap, g.N, g.K, g.W, g.w_stride,
+                                             g.up_off, g.C, small.tile_cnt, small.partials);
+    gemm_class<BIGM, BIGN, GATED, 2, false>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets,
+                                            large.tile_prefix, g.El, g.cap, g.N, g.K, g.W, g.w_stride,
+                                            g.up_off, g.C, large.tile_cnt, large.partials);
+}
+
 }  // namespace
 
 namespace {
-
-constexpr int BIGM = 256, BIGN = 256;
 
 int device_cus()
 {
@@ -667,30 +752,35 @@ int device_cus()
 }
 
 // Workspace layout of the grouped FFN (every part 256-byte aligned):
-//   tile_prefix [El+1] | counters gate-up [Tgu] | counters down [Tdn] |
-//   partial slots [2*G][SLOT_FLOATS] fp32 | h [cap, I_s] bf16
+//   prefix large [El+1] | prefix small [El+1] |
+//   tile counters: large gate-up, large down, small gate-up, small down |
+//   split-K partial slots: small [2*G][SLOT_SMALL], large [2*G][SLOT_BIG] fp32 |
+//   h [cap, I_s] bf16
+// The two GEMMs run one after the other on the stream and share the partial
+// slots; each keeps its own tile counters.
 struct FfnLayout {
-    int bm;
-    int64_t max_mtiles, t_gu, t_dn;
-    int grid_gu, grid_dn;
-    size_t off_cnt, off_part, off_h, total;
+    bool big;
+    int64_t t_gu, t_dn, ts_gu, ts_dn;  // tile-count bounds per class and GEMM
+    int grid;                          // persistent workgroups of a large-tile launch
+    size_t off_pre_s, off_cnt, off_part_s, off_part, off_h, total;
     FfnLayout(int64_t cap, int El, int H, int Is)
     {
-        const bool big = (H % BIG_BK == 0) && (Is % BIG_BK == 0) && H >= 2 * BIG_BK && Is >= 2 * BIG_BK;
-        bm = big ? BIGM : BM;
-        max_mtiles = ceil_div(cap, bm) + El;
-        t_gu = max_mtiles * ceil_div(Is, big ? BIGN / 2 : BN);
-        t_dn = max_mtiles * ceil_div(H, big ? BIGN : BN);
-        const int cus = device_cus();
-        auto grid = [&](int64_t tiles) {
-            return (int)(tiles < cus ? (tiles + 7) / 8 * 8 : cus);
-        };
-        grid_gu = grid(t_gu);
-        grid_dn = grid(t_dn);
-        const int slots = big ? 2 * (grid_gu > grid_dn ? grid_gu : grid_dn) : 0;
-        off_cnt = align256((size_t)(El + 1) * sizeof(int32_t));
-        off_part = off_cnt + align256((size_t)(t_gu + t_dn) * sizeof(int32_t));
-        off_h = off_part + align256((size_t)slots * SLOT_FLOATS * sizeof(float));
+        big = (H % BIG_BK == 0) && (Is % BIG_BK == 0) && H >= 2 * BIG_BK && Is >= 2 * BIG_BK;
+        const int bm = big ? BIGM : BM;
+        const int64_t mt = ceil_div(cap, bm) + El;
+        t_gu = mt * ceil_div(Is, big ? BIGN / 2 : BN);
+        t_dn = mt * ceil_div(H, big ? BIGN : BN);
+        // a small-row expert has at most SMALL_MAX rows: ceil(SMALL_MAX/SMALLM) m-tiles
+        const int64_t mts = big ? (int64_t)El * ceil_div(SMALL_MAX, SMALLM) : 0;
+        ts_gu = mts * ceil_div(Is, BIGN / 2);
+        ts_dn = mts * ceil_div(H, BIGN);
+        grid = device_cus();
+        const size_t slots = big ? 2 * (size_t)grid : 0;
+        off_pre_s = align256((size_t)(El + 1) * sizeof(int32_t));
+        off_cnt = off_pre_s + align256((size_t)(El + 1) * sizeof(int32_t));
+        off_part_s = off_cnt + align256((size_t)(t_gu + t_dn + ts_gu + ts_dn) * sizeof(int32_t));
+        off_part = off_part_s + align256(slots * SLOT_SMALL * sizeof(float));
+        off_h = off_part + align256(slots * SLOT_BIG * sizeof(float));
         total = off_h + align256((size_t)cap * Is * 2);
     }
 };
@@ -710,34 +800,38 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
     if (cap == 0) return hipSuccess;
     const FfnLayout L(cap, El, H, Is);
     char *base = static_cast<char *>(ws);
-    int32_t *tile_prefix = reinterpret_cast<int32_t *>(base);
+    int32_t *pre = reinterpret_cast<int32_t *>(base);
+    int32_t *pre_s = reinterpret_cast<int32_t *>(base + L.off_pre_s);
     int32_t *cnt = reinterpret_cast<int32_t *>(base + L.off_cnt);
-    float *partials = reinterpret_cast<float *>(base + L.off_part);
+    float *part_s = reinterpret_cast<float *>(base + L.off_part_s);
+    float *part = reinterpret_cast<float *>(base + L.off_part);
     uint16_t *h = reinterpret_cast<uint16_t *>(base + L.off_h);
-    // the large-tile kernel addresses operands with 32-bit buffer offsets
+    // the large-tile kernels address operands with 32-bit buffer offsets
     const int64_t lim = ((int64_t)1 << 32) - 4 * (int64_t)(H > Is ? H : Is);
-    const bool big = L.bm == BIGM && (row_index ? x_rows : cap) * (int64_t)H * 2 < lim &&
-                     (int64_t)BIGM * Is * 2 < lim;
+    const bool big = L.big && (row_index ? x_rows : cap) * (int64_t)H * 2 < lim &&
+                     cap * (int64_t)Is * 2 < lim;
     hipError_t err;
     {
         KernelTimer timer(MOE_K_SCHEDULE, s);
-        schedule_kernel<<<dim3(1), dim3(1024), 0, s>>>(offsets, El, cap, big ? BIGM : BM, tile_prefix, cnt,
-                                                       big ? L.t_gu + L.t_dn : 0);
+        schedule_kernel<<<dim3(1), dim3(1024), 0, s>>>(
+            offsets, El, cap, big ? BIGM : BM, SMALLM, big ? SMALL_MAX : 0, pre, big ? pre_s : nullptr, cnt,
+            big ? L.t_gu + L.t_dn + L.ts_gu + L.ts_dn : 0);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     if (big) {
+        int32_t *c_gu = cnt, *c_dn = cnt + L.t_gu, *cs_gu = c_dn + L.t_dn, *cs_dn = cs_gu + L.ts_gu;
         {
             KernelTimer timer(MOE_K_GATE_UP, s);
-            gemm_big<BIGM, BIGN, true><<<dim3((unsigned)L.grid_gu), dim3(256), 0, s>>>(
-                x, row_index, kdiv, x_rows, offsets, tile_prefix, El, cap, Is, H, w13, (int64_t)2 * Is * H,
-                Is, h, cnt, partials);
+            const GemmArgs g{x, row_index, kdiv, x_rows, offsets, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h};
+            gemm_grouped<true><<<dim3((unsigned)L.grid), dim3(256), 0, s>>>(
+                g, TileClass{pre_s, cs_gu, part_s}, TileClass{pre, c_gu, part});
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         {
             KernelTimer timer(MOE_K_DOWN, s);
-            gemm_big<BIGM, BIGN, false><<<dim3((unsigned)L.grid_dn), dim3(256), 0, s>>>(
-                h, nullptr, 1, cap, offsets, tile_prefix, El, cap, H, Is, w2, (int64_t)H * Is, 0, y,
-                cnt + L.t_gu, partials);
+            const GemmArgs g{h, nullptr, 1, cap, offsets, El, cap, H, Is, w2, (int64_t)H * Is, 0, y};
+            gemm_grouped<false><<<dim3((unsigned)L.grid), dim3(256), 0, s>>>(
+                g, TileClass{pre_s, cs_dn, part_s}, TileClass{pre, c_dn, part});
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         return hipSuccess;
@@ -750,7 +844,7 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
         int64_t tiles = mt * ceil_div(Is, BN);
         int64_t grid = tiles < 2048 ? tiles : 2048;
         gemm_kernel<true><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
-            x, row_index, kdiv, offsets, tile_prefix, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h);
+            x, row_index, kdiv, offsets, pre, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     {
@@ -758,7 +852,7 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
         int64_t tiles = mt * ceil_div(H, BN);
         int64_t grid = tiles < 2048 ? tiles : 2048;
         gemm_kernel<false><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
-            h, nullptr, 1, offsets, tile_prefix, El, cap, H, Is, w2, (int64_t)H * Is, 0, y);
+            h, nullptr, 1, offsets, pre, El, cap, H, Is, w2, (int64_t)H * Is, 0, y);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     return hipSuccess;
