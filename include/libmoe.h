@@ -168,7 +168,8 @@ typedef enum moe_kernel_kind {
     MOE_K_GATE_UP = 4,   /* gate-up GEMM with the SwiGLU epilogue (both tile classes) */
     MOE_K_DOWN = 5,      /* down GEMM (both tile classes, split-K reduction included) */
     MOE_K_COMBINE = 6,
-    MOE_K_COUNT = 7
+    MOE_K_SPLITK_REDUCE = 7, /* combination of split-K partials of the large tiles (long K only) */
+    MOE_K_COUNT = 8
 } moe_kernel_kind;
 
 moe_status moe_timing_enable(int enable);

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libmoe.so")
 MAX_TOPK = 16
 MAX_EXPERTS = 1024
 KERNEL_KINDS = {"route": 0, "permute": 1, "gather": 2, "schedule": 3, "gate_up": 4, "down": 5,
-                "combine": 6}
+                "combine": 6, "splitk_reduce": 7}
 
 
 class MoeError(RuntimeError):

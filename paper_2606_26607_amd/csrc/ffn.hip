@@ -46,29 +46,117 @@ __device__ __forceinline__ int32_t block_exscan(int32_t v, int32_t *wsum, int32_
     return before + incl - v;
 }
 
-// Tile schedule of the grouped FFN.  Experts with at most small_max rows go
-// to the small-row kernel (m-tiles of bm_small rows; small_max = 0 disables
-// it), the others to the large-tile kernel (m-tiles of bm rows):
+// Shape of both GEMMs as the schedule's cost model sees it: output tiles per
+// m-tile (n_tiles) and K-slices per tile (nk).
+struct SchedShape {
+    int nt_gu, nk_gu, nt_dn, nk_dn, grid;
+};
+
+// Estimated time of one GEMM's large-tile class of `tiles` tiles, in units
+// of one large-tile K-slice on one workgroup: whole rounds of the grid, or
+// the stream-K share (with its partial-sum traffic) when there are fewer
+// tiles than workgroups and K is long.
+__device__ __forceinline__ float large_cost(int64_t tiles, int nk, int grid)
+{
+    if (tiles == 0) return 0.f;
+    const float t = (float)tiles, g = (float)grid;
+    if (tiles < grid && nk >= 64) return 1.25f * t * (float)nk / g;
+    return ceilf(t / g) * (float)nk;
+}
+
+// Tile schedule of the grouped FFN.  An expert's rows [a, b) are cut at
+// split[e]: rows [a, split) go to the large-tile class (m-tiles of bm rows),
+// rows [split, b) to the small-row class (m-tiles of bm_small rows).  An
+// expert with at most small_max rows is all small.  A larger one may give
+// its leftover rows after whole large tiles to the small class: a nearly
+// empty large tile costs as much as a full one, while small-row tiles are
+// split evenly over the grid.  Which leftovers move (none, or those of at
+// most 32, 64 or 96 rows) is chosen for the lowest estimated time of both
+// GEMMs under a cost model (large_cost; a small-row K-slice costs 0.8 of a
+// large one).  small_max = 0 disables the small class.
 //   pre[e] / pre_small[e] = m-tiles of that class of the experts before e,
 //   pre[El] / pre_small[El] = totals.
 // Also clears the split-K tile counters (no memset node is needed, so the
 // chain stays graph-capturable).
 __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restrict__ offsets, int El,
                                                         int64_t cap, int bm, int bm_small, int small_max,
-                                                        int32_t *__restrict__ pre,
+                                                        SchedShape sh, int32_t *__restrict__ pre,
                                                         int32_t *__restrict__ pre_small,
+                                                        int32_t *__restrict__ split,
                                                         int32_t *__restrict__ counters, int64_t n_counters)
 {
+    constexpr int NC = 4;  // leftover thresholds 0, 32, 64, 96 (up to small_max)
     __shared__ int32_t wsum[16];
-    const int e = threadIdx.x;
+    __shared__ int32_t part[16][2 * NC];
+    __shared__ int32_t chosen;
+    const int e = threadIdx.x, lane = e & 63, wv = e >> 6;
     for (int64_t i = e; i < n_counters; i += 1024) counters[i] = 0;
-    int32_t mt = 0, mts = 0;
+    // rows fit int32: cap < 2^31 is checked on the host
+    int32_t a = 0, n = 0;
     if (e < El) {
-        int64_t a = clamp_row(offsets[e], cap), b = clamp_row(offsets[e + 1], cap);
-        const int64_t n = b > a ? b - a : 0;
-        if (n > 0 && n <= small_max) mts = (int32_t)((n + bm_small - 1) / bm_small);
-        else if (n > 0) mt = (int32_t)((n + bm - 1) / bm);
+        a = (int32_t)clamp_row(offsets[e], cap);
+        const int32_t b = (int32_t)clamp_row(offsets[e + 1], cap);
+        n = b > a ? b - a : 0;
     }
+    // m-tiles of both classes (x: large, y: small) for a leftover threshold th
+    auto tiles_for = [&](int th) {
+        int2 r = make_int2(0, 0);
+        if (n > 0 && n <= small_max) {
+            r.y = (n + bm_small - 1) / bm_small;
+        } else if (n > 0) {
+            const int32_t whole = n / bm, rest = n - whole * bm;
+            if (rest > 0 && rest <= th) {
+                r.x = whole;
+                r.y = (rest + bm_small - 1) / bm_small;
+            } else {
+                r.x = (n + bm - 1) / bm;
+            }
+        }
+        return r;
+    };
+    auto wave_sum = [&](int32_t v) {
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+        return v;
+    };
+    int th = 0;
+    if (small_max > 0) {
+        // class totals of every candidate threshold in one block reduction
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const int2 r = tiles_for(32 * c);
+            const int32_t sx = wave_sum(r.x), sy = wave_sum(r.y);
+            if (lane == 0) {
+                part[wv][2 * c] = sx;
+                part[wv][2 * c + 1] = sy;
+            }
+        }
+        __syncthreads();
+        if (e == 0) {
+            float best = 0.f;
+            for (int c = 0; c < NC && 32 * c <= small_max; ++c) {
+                int64_t tl = 0, ts = 0;
+                for (int w = 0; w < 16; ++w) {
+                    tl += part[w][2 * c];
+                    ts += part[w][2 * c + 1];
+                }
+                const float cost = large_cost(tl * sh.nt_gu, sh.nk_gu, sh.grid) +
+                                   large_cost(tl * sh.nt_dn, sh.nk_dn, sh.grid) +
+                                   0.8f * (float)(ts * (sh.nt_gu * sh.nk_gu + sh.nt_dn * sh.nk_dn)) /
+                                       (float)sh.grid;
+                if (c == 0 || cost < best) {
+                    best = cost;
+                    th = 32 * c;
+                }
+            }
+            chosen = th;
+        }
+        __syncthreads();
+        th = chosen;
+    }
+    const int2 r = tiles_for(th);
+    const int32_t mt = r.x, mts = r.y;
+    if (split && e < El) split[e] = a + (mts ? mt * bm : n);
     const int32_t x = block_exscan(mt, wsum, &pre[El]);
     if (e < El) pre[e] = x;
     if (pre_small) {
@@ -234,6 +322,14 @@ __device__ __forceinline__ void dma16(i32x4_t desc, uint32_t lds, uint32_t voff,
                  :: "s"(lds), "v"(voff), "s"(desc), "s"(soff) : "memory");
 }
 
+// The same with an agent-coherent (sc1) load, for data another workgroup
+// (possibly on another die, behind another L2) stored with sc1.
+__device__ __forceinline__ void dma16_sc1(i32x4_t desc, uint32_t lds, uint32_t voff, uint32_t soff)
+{
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen sc1 lds"
+                 :: "s"(lds), "v"(voff), "s"(desc), "s"(soff) : "memory");
+}
+
 __device__ __forceinline__ uint32_t lds_addr(const void *p)
 {
     return (uint32_t)(uintptr_t)(lds_ptr_t)(const_cast<void *>(p));
@@ -324,27 +420,68 @@ __device__ __forceinline__ uint16_t bf16_bits(float f)
     return *reinterpret_cast<uint16_t *>(&h);
 }
 
+// Coordinates of tile `tile` of a tile class: expert e, rows [r0, r1) and
+// output columns [n0, n0 + nvalid).  Tiles are numbered expert by expert,
+// then by n-tile, with m-tiles innermost; the class's rows of expert e are
+// [offsets[e], split[e]) for the large class and [split[e], offsets[e+1])
+// for the tail class.
+struct TileCoord {
+    int e;
+    int64_t r0, r1;
+    int n0, nvalid;
+};
+
+template <int BMt, int OUTN, bool TAIL>
+__device__ __forceinline__ TileCoord tile_coord(int64_t tile, const int32_t *__restrict__ tile_prefix, int El,
+                                                int n_tiles, const int32_t *__restrict__ offsets,
+                                                const int32_t *__restrict__ split, int64_t cap, int N)
+{
+    int lo = 0, hi = El - 1;
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if ((int64_t)tile_prefix[mid] * n_tiles <= tile) lo = mid; else hi = mid - 1;
+    }
+    TileCoord c;
+    c.e = lo;
+    const int64_t local = tile - (int64_t)tile_prefix[lo] * n_tiles;
+    const int mte = tile_prefix[lo + 1] - tile_prefix[lo];
+    const int nt = (int)(local / mte), mt = (int)(local % mte);
+    const int64_t rb = TAIL ? clamp_row(split[lo], cap) : clamp_row(offsets[lo], cap);
+    const int64_t re = TAIL ? clamp_row(offsets[lo + 1], cap) : clamp_row(split[lo], cap);
+    c.r0 = rb + (int64_t)mt * BMt;
+    c.r1 = re < c.r0 + BMt ? re : c.r0 + BMt;
+    c.n0 = nt * OUTN;
+    c.nvalid = N - c.n0 < OUTN ? N - c.n0 : OUTN;
+    return c;
+}
+
+// Large-tile launches split K only from this many K-slices per tile.
+constexpr int SPLIT_MIN_NK = 128;
+
 // A partial accumulator slot holds one fp32 value per accumulator register
 // of each of the 256 threads, stored register-major so each access is a
 // coalesced 16-byte vector per lane.
 
-// Work split of one launch over G persistent workgroups.  By default every
-// tile is handed out whole, round robin (dp = T): workgroups on one die then
-// walk K in near lockstep over shared panels, which is what keeps the die's
-// L2 effective.  With fewer tiles than workgroups and a long K (a few
-// large-K tiles, e.g. one expert's down projection), or always for the
-// weight-streaming small-row kernel (bound by HBM, not by L2 reuse), the
-// K-slices of all tiles are cut into contiguous runs ("stream-K"), so every
-// workgroup gets the same number of slices; partial sums are combined by
-// the last contributor of each tile.
+// Work split of one launch over G persistent workgroups.  Tiles [0, dp) are
+// handed out whole, round robin: workgroups on one die then walk K in near
+// lockstep over shared panels, which is what keeps the die's L2 effective.
+// The K-slices of tiles [dp, T) are cut into G contiguous runs
+// ("stream-K"), so every workgroup gets the same number of slices; partial
+// sums are combined by the last contributor of each tile (small-row tiles,
+// whose partials are small) or by a separate reduction kernel (large tiles:
+// one workgroup reading several 256 KB partials would be bound by what one
+// CU can pull from memory).  Stream-K takes all of the weight-streaming
+// small-row tiles, and large tiles only in a launch of fewer tiles than
+// workgroups with a long K (e.g. one expert's down projection).
 struct WorkSplit {
     int64_t T, dp, iters;  // tiles, whole tiles, K-slices in the stream-K part
     int nk, G, Gsk;        // slices per tile, workgroups, workgroups in the stream-K part
     __device__ WorkSplit(int64_t total, int nk_, int g, bool split_always) : T(total), nk(nk_), G(g)
     {
-        // splitting pays only when a tile has many slices: each split tile
-        // moves its fp32 partial sums through memory once more
-        dp = (split_always || (T < G && nk >= 64)) ? 0 : T;
+        // splitting pays only when a tile has many slices and there are too
+        // few tiles to fill the grid: each split piece moves its fp32 partial
+        // sums through memory, and split pieces lose the lockstep walk over K
+        dp = (split_always || (T < G && nk >= SPLIT_MIN_NK)) ? 0 : T;
         iters = (T - dp) * nk;
         // every stream-K workgroup gets at least one slice, so the workgroups
         // that meet a tile are exactly a consecutive range
@@ -369,6 +506,7 @@ struct GemmArgs {
     int kdiv;
     int64_t a_rows;             // rows of A when row_index is given
     const int32_t *offsets;     // [El+1] expert row ranges
+    const int32_t *split;       // [El] cut of each expert's rows between the tile classes
     int El;
     int64_t cap;
     int N, K;                   // output columns (per part when gated), reduction length
@@ -379,7 +517,9 @@ struct GemmArgs {
 };
 
 // Per tile class: its m-tile prefix over experts, split-K tile counters and
-// partial slots.
+// partial slots.  split[e] cuts expert e's rows between the classes: the
+// large class takes [offsets[e], split[e]), the small (tail) class
+// [split[e], offsets[e+1]).
 struct TileClass {
     const int32_t *tile_prefix;
     int32_t *tile_cnt;
@@ -391,10 +531,11 @@ struct TileClass {
 // workgroup's LDS (at least the class's ring size).  Pointers are restrict
 // parameters so that the inlined body keeps the no-alias facts of kernel
 // arguments (its loads are not reordered around the stores it makes).
-template <int BMt, int BNt, bool GATED, int WM, bool SPLIT_ALWAYS>
+template <int BMt, int BNt, bool GATED, int WM, bool TAIL>
 __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restrict__ A,
                                            const int32_t *__restrict__ row_index, int kdiv, int64_t a_rows,
                                            const int32_t *__restrict__ offsets,
+                                           const int32_t *__restrict__ split,
                                            const int32_t *__restrict__ tile_prefix, int El, int64_t cap,
                                            int N, int K, const uint16_t *__restrict__ W, int64_t w_stride,
                                            int up_off, uint16_t *__restrict__ C,
@@ -417,7 +558,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
     const int wm = wave / WN, wn = wave % WN;
     const int n_tiles = (N + OUTN - 1) / OUTN;
     const int nk = K / BIG_BK;
-    const WorkSplit ws((int64_t)tile_prefix[El] * n_tiles, nk, gridDim.x, SPLIT_ALWAYS);
+    const WorkSplit ws((int64_t)tile_prefix[El] * n_tiles, nk, gridDim.x, TAIL);
     if (ws.T == 0) return;
     // XCD-aware numbering: the 8 dies take workgroups round robin, so the
     // workgroups of one die get consecutive virtual ids and with them a
@@ -465,21 +606,10 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
 
     // One piece of work: K-slices [klo, khi) of tile `tile`.
     auto do_work = [&](int64_t tile, int klo, int khi) {
-        // tile -> (expert, n-tile, m-tile); m-tiles are innermost
-        int lo = 0, hi = El - 1;
-        while (lo < hi) {
-            int mid = (lo + hi + 1) >> 1;
-            if ((int64_t)tile_prefix[mid] * n_tiles <= tile) lo = mid; else hi = mid - 1;
-        }
-        const int e = lo;
-        const int64_t local = tile - (int64_t)tile_prefix[e] * n_tiles;
-        const int mte = tile_prefix[e + 1] - tile_prefix[e];
-        const int nt = (int)(local / mte), mt = (int)(local % mte);
-        const int64_t r0 = clamp_row(offsets[e], cap) + (int64_t)mt * BMt;
-        int64_t r1 = clamp_row(offsets[e + 1], cap);
-        if (r1 > r0 + BMt) r1 = r0 + BMt;
-        const int n0 = nt * OUTN;
-        const int nvalid = N - n0 < OUTN ? N - n0 : OUTN;
+        const TileCoord tc = tile_coord<BMt, OUTN, TAIL>(tile, tile_prefix, El, n_tiles, offsets, split, cap, N);
+        const int e = tc.e;
+        const int64_t r0 = tc.r0, r1 = tc.r1;
+        const int n0 = tc.n0, nvalid = tc.nvalid;
         const uint16_t *We = W + (int64_t)e * w_stride;
 
         // this wave's B rows lie in one part (gate or up) when gated
@@ -616,6 +746,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
             }
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // partial is visible device-wide
             lds_barrier();
+            if constexpr (!TAIL) return;  // large tiles: splitk_reduce combines the partials
             int *flag = reinterpret_cast<int *>(ring);
             if (tid == 0) {
                 const int old = __hip_atomic_fetch_add(&tile_cnt[tile], 1, __ATOMIC_RELAXED,
@@ -628,42 +759,59 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             lds_barrier();
             if (!last) return;
-            // Last contributor: sum the partials in contributor order straight
-            // from memory into the bf16 staging tile (the accumulator
-            // registers are not needed again).
-            uint16_t *stage_out = reinterpret_cast<uint16_t *>(ring);
-            for (int i = 0; i < MB; ++i) {
-                for (int j = 0; j < (GATED ? NB / 2 : NB); ++j) {
-                    const int col = wn * (OUTN / WN) + j * 32 + (lane & 31);
+            // Stream contributor c's partial into the accumulators (assign:
+            // acc = partial, else acc += partial) through LDS: one block row
+            // (NB*4 DMA instructions per wave, 1 KB each) per chunk, two
+            // chunks in flight.  Each wave reads back only what its own loads
+            // wrote, so waiting for its own loads (vmcnt) is enough.
+            const i32x4_t pdesc = buffer_desc(partials, (int64_t)2 * ws.G * SLOT * 4);
+            auto add_partial = [&](int c, bool assign) {
+                constexpr int CH = NB * 4;
+                const uint32_t base_c = (uint32_t)(slot_of(c) * SLOT * 4);
+                auto issue = [&](int i) {
+                    const uint32_t buf = ring_base + (uint32_t)((i & 1) * CH * 4096);
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        float4 g = make_float4(0.f, 0.f, 0.f, 0.f), u = g;
-                        for (int c = vfirst; c <= vlast; ++c) {
-                            const uint32_t base_b = (uint32_t)(slot_of(c) * SLOT * 4);
-                            u32x4_t w = __builtin_amdgcn_raw_buffer_load_b128(
-                                pr, base_b + (uint32_t)((((i * NB + j) * 4 + q) * 256 + tid) * 16), 0, SC1);
-                            const float4 pv = *reinterpret_cast<float4 *>(&w);
-                            g.x += pv.x; g.y += pv.y; g.z += pv.z; g.w += pv.w;
-                            if (GATED) {
-                                u32x4_t w2 = __builtin_amdgcn_raw_buffer_load_b128(
-                                    pr, base_b + (uint32_t)((((i * NB + j + NB / 2) * 4 + q) * 256 + tid) * 16), 0, SC1);
-                                const float4 pu = *reinterpret_cast<float4 *>(&w2);
-                                u.x += pu.x; u.y += pu.y; u.z += pu.z; u.w += pu.w;
-                            }
-                        }
-                        const float gv[4] = {g.x, g.y, g.z, g.w}, uv[4] = {u.x, u.y, u.z, u.w};
+                    for (int jq = 0; jq < CH; ++jq)
+                        dma16_sc1(pdesc, buf + jq * 4096 + wave * 1024, (uint32_t)(jq * 4096 + tid * 16),
+                              base_c + (uint32_t)(i * CH * 4096));
+                };
+                issue(0);
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            const int row = wm * (BMt / WM) + i * 32 + 8 * q + 4 * (lane >> 5) + r;
-                            float o = gv[r];
-                            if (GATED) o = o / (1.0f + __expf(-o)) * uv[r];
-                            stage_out[row * OUTN + col] = bf16_bits(o);
-                        }
+                for (int i = 0; i < MB; ++i) {
+                    if (i + 1 < MB) {
+                        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // chunk i-1 read out
+                        issue(i + 1);
+                        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(CH) : "memory");
+                    } else {
+                        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
                     }
+                    const uint4 *bp = ring + (i & 1) * CH * 256;
+#pragma unroll
+                    for (int j = 0; j < NB; ++j)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const uint4 w = bp[(j * 4 + q) * 256 + tid];
+                            const float pv[4] = {__uint_as_float(w.x), __uint_as_float(w.y),
+                                                 __uint_as_float(w.z), __uint_as_float(w.w)};
+#pragma unroll
+                            for (int r = 0; r < 4; ++r)
+                                acc[i][j][4 * q + r] = assign ? pv[r] : acc[i][j][4 * q + r] + pv[r];
+                        }
                 }
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            };
+            if (vlast - vfirst == 1) {
+                // Two contributors: add the other one's partial (fp32
+                // addition commutes, so the sum does not depend on which of
+                // the two arrived last).
+                add_partial(v == vfirst ? vlast : vfirst, false);
+            } else {
+                // Three or more: rebuild the sum in contributor order from the
+                // stored partials, this workgroup's own included, so the
+                // result does not depend on which contributor arrived last.
+                for (int c = vfirst; c <= vlast; ++c) add_partial(c, c == vfirst);
             }
-            store_staged(r0, r1, n0, nvalid);
-            return;
+            lds_barrier();  // LDS free again for the epilogue's staging
         }
 
         // epilogue: block (i, j) lane holds column (lane & 31), rows
@@ -715,27 +863,87 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
 constexpr int BIGM = 256, BIGN = 256;  // large tiles: 256 rows x 256 weight rows
 constexpr int SMALLM = 32;             // small-row tiles: 32 rows x 256 weight rows
 constexpr int SMALL_MAX = 96;          // experts with at most this many rows use small-row tiles
+constexpr int REDUCE_GRID = 2048;      // workgroups of the split-K reduction
 constexpr int BIG_RING = (A_SLOTS * BIGM + B_SLOTS * BIGN) * CPR;
 // floats per partial slot of each class (one per accumulator register)
 constexpr int SLOT_SMALL = (SMALLM / 32) * (BIGN / 4 / 32) * 16 * 256;
 constexpr int SLOT_BIG = (BIGM / 2 / 32) * (BIGN / 2 / 32) * 16 * 256;
 
-// One grouped GEMM launch: the small-row experts first (32-row tiles,
-// K-split over the whole grid: these stream weights, and spreading them over
-// every CU is what reaches HBM bandwidth), then the large-row experts (256-row
-// tiles) in the same persistent grid.  The classes cover disjoint experts, so
-// a workgroup goes on to the second without waiting for the first.
+// One grouped GEMM launch: the small-row class first (32-row tiles, K-split
+// over the whole grid: these stream weights, and spreading them over every
+// CU is what reaches HBM bandwidth), then the large-tile class (256-row
+// tiles) in the same persistent grid.  The classes cover disjoint rows, so a
+// workgroup goes on to the second without waiting for the first.
 template <bool GATED>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
 void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
 {
     __shared__ uint4 ring[BIG_RING];
-    gemm_class<SMALLM, BIGN, GATED, 1, true>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets,
+    gemm_class<SMALLM, BIGN, GATED, 1, true>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split,
                                              small.tile_prefix, g.El, g.cap, g.N, g.K, g.W, g.w_stride,
                                              g.up_off, g.C, small.tile_cnt, small.partials);
-    gemm_class<BIGM, BIGN, GATED, 2, false>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets,
+    gemm_class<BIGM, BIGN, GATED, 2, false>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split,
                                             large.tile_prefix, g.El, g.cap, g.N, g.K, g.W, g.w_stride,
                                             g.up_off, g.C, large.tile_cnt, large.partials);
+}
+
+// Combines the split-K partials of the large-tile class after its GEMM
+// launch (G persistent workgroups, the same work split): for every split
+// tile, every block of 32x32 outputs of every wave position is one work
+// item, so all CUs share the partial traffic.  Each partial is summed in
+// contributor order (deterministic), then the epilogue of the GEMM is
+// applied (SwiGLU when gated) and the bf16 result written.
+template <bool GATED>
+__global__ __launch_bounds__(256) void splitk_reduce(const int32_t *__restrict__ offsets,
+                                                     const int32_t *__restrict__ split,
+                                                     const int32_t *__restrict__ tile_prefix, int El,
+                                                     int64_t cap, int N, int K, int G,
+                                                     const float *__restrict__ partials,
+                                                     uint16_t *__restrict__ C)
+{
+    constexpr int WM = 2, WN = 2;
+    constexpr int MB = BIGM / WM / 32, NB = BIGN / WN / 32;
+    constexpr int OUTN = GATED ? BIGN / 2 : BIGN;
+    constexpr int JJ = GATED ? NB / 2 : NB;  // output blocks per wave row
+    const int n_tiles = (N + OUTN - 1) / OUTN;
+    const int nk = K / BIG_BK;
+    const WorkSplit ws((int64_t)tile_prefix[El] * n_tiles, nk, G, false);
+    const int64_t items = (ws.T - ws.dp) * MB * JJ;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+    for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
+        const int64_t tile = ws.dp + it / (MB * JJ);
+        const int i = (int)((it / JJ) % MB), j = (int)(it % JJ);
+        const TileCoord tc = tile_coord<BIGM, OUTN, false>(tile, tile_prefix, El, n_tiles, offsets, split, cap, N);
+        const int64_t tb = (tile - ws.dp) * nk;
+        const int vfirst = ws.owner(tb), vlast = ws.owner(tb + nk - 1);
+        float g[16], u[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) g[r] = u[r] = 0.f;
+        for (int c = vfirst; c <= vlast; ++c) {
+            const float4 *slot = reinterpret_cast<const float4 *>(
+                partials + (c * 2 + (ws.begin(c) >= tb ? 0 : 1)) * (int64_t)SLOT_BIG);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float4 pg = slot[((i * NB + j) * 4 + q) * 256 + tid];
+                g[4 * q] += pg.x; g[4 * q + 1] += pg.y; g[4 * q + 2] += pg.z; g[4 * q + 3] += pg.w;
+                if (GATED) {
+                    const float4 pu = slot[((i * NB + j + NB / 2) * 4 + q) * 256 + tid];
+                    u[4 * q] += pu.x; u[4 * q + 1] += pu.y; u[4 * q + 2] += pu.z; u[4 * q + 3] += pu.w;
+                }
+            }
+        }
+        const int col = wn * (OUTN / WN) + j * 32 + (lane & 31);
+        if (col >= tc.nvalid) continue;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int64_t row = tc.r0 + wm * (BIGM / WM) + i * 32 + 8 * (r / 4) + 4 * (lane >> 5) + (r % 4);
+            if (row >= tc.r1) continue;
+            float o = g[r];
+            if (GATED) o = o / (1.0f + __expf(-o)) * u[r];
+            C[row * N + tc.n0 + col] = bf16_bits(o);
+        }
+    }
 }
 
 }  // namespace
@@ -752,7 +960,7 @@ int device_cus()
 }
 
 // Workspace layout of the grouped FFN (every part 256-byte aligned):
-//   prefix large [El+1] | prefix small [El+1] |
+//   prefix large [El+1] | prefix small [El+1] | class cut [El] |
 //   tile counters: large gate-up, large down, small gate-up, small down |
 //   split-K partial slots: small [2*G][SLOT_SMALL], large [2*G][SLOT_BIG] fp32 |
 //   h [cap, I_s] bf16
@@ -762,7 +970,7 @@ struct FfnLayout {
     bool big;
     int64_t t_gu, t_dn, ts_gu, ts_dn;  // tile-count bounds per class and GEMM
     int grid;                          // persistent workgroups of a large-tile launch
-    size_t off_pre_s, off_cnt, off_part_s, off_part, off_h, total;
+    size_t off_pre_s, off_split, off_cnt, off_part_s, off_part, off_h, total;
     FfnLayout(int64_t cap, int El, int H, int Is)
     {
         big = (H % BIG_BK == 0) && (Is % BIG_BK == 0) && H >= 2 * BIG_BK && Is >= 2 * BIG_BK;
@@ -777,7 +985,8 @@ struct FfnLayout {
         grid = device_cus();
         const size_t slots = big ? 2 * (size_t)grid : 0;
         off_pre_s = align256((size_t)(El + 1) * sizeof(int32_t));
-        off_cnt = off_pre_s + align256((size_t)(El + 1) * sizeof(int32_t));
+        off_split = off_pre_s + align256((size_t)(El + 1) * sizeof(int32_t));
+        off_cnt = off_split + align256((size_t)El * sizeof(int32_t));
         off_part_s = off_cnt + align256((size_t)(t_gu + t_dn + ts_gu + ts_dn) * sizeof(int32_t));
         off_part = off_part_s + align256(slots * SLOT_SMALL * sizeof(float));
         off_h = off_part + align256(slots * SLOT_BIG * sizeof(float));
@@ -802,6 +1011,7 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
     char *base = static_cast<char *>(ws);
     int32_t *pre = reinterpret_cast<int32_t *>(base);
     int32_t *pre_s = reinterpret_cast<int32_t *>(base + L.off_pre_s);
+    int32_t *split = reinterpret_cast<int32_t *>(base + L.off_split);
     int32_t *cnt = reinterpret_cast<int32_t *>(base + L.off_cnt);
     float *part_s = reinterpret_cast<float *>(base + L.off_part_s);
     float *part = reinterpret_cast<float *>(base + L.off_part);
@@ -814,7 +1024,9 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
     {
         KernelTimer timer(MOE_K_SCHEDULE, s);
         schedule_kernel<<<dim3(1), dim3(1024), 0, s>>>(
-            offsets, El, cap, big ? BIGM : BM, SMALLM, big ? SMALL_MAX : 0, pre, big ? pre_s : nullptr, cnt,
+            offsets, El, cap, big ? BIGM : BM, SMALLM, big ? SMALL_MAX : 0,
+            SchedShape{(int)ceil_div(Is, BIGN / 2), H / BIG_BK, (int)ceil_div(H, BIGN), Is / BIG_BK, L.grid}, pre,
+            big ? pre_s : nullptr, big ? split : nullptr, cnt,
             big ? L.t_gu + L.t_dn + L.ts_gu + L.ts_dn : 0);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
@@ -822,16 +1034,28 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
         int32_t *c_gu = cnt, *c_dn = cnt + L.t_gu, *cs_gu = c_dn + L.t_dn, *cs_dn = cs_gu + L.ts_gu;
         {
             KernelTimer timer(MOE_K_GATE_UP, s);
-            const GemmArgs g{x, row_index, kdiv, x_rows, offsets, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h};
+            const GemmArgs g{x, row_index, kdiv, x_rows, offsets, split, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h};
             gemm_grouped<true><<<dim3((unsigned)L.grid), dim3(256), 0, s>>>(
                 g, TileClass{pre_s, cs_gu, part_s}, TileClass{pre, c_gu, part});
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
+        if (H / BIG_BK >= SPLIT_MIN_NK) {  // the large tiles may have been split over K
+            KernelTimer timer(MOE_K_SPLITK_REDUCE, s);
+            splitk_reduce<true><<<dim3(REDUCE_GRID), dim3(256), 0, s>>>(offsets, split, pre, El, cap, Is, H, L.grid,
+                                                                     part, h);
+            if ((err = hipGetLastError()) != hipSuccess) return err;
+        }
         {
             KernelTimer timer(MOE_K_DOWN, s);
-            const GemmArgs g{h, nullptr, 1, cap, offsets, El, cap, H, Is, w2, (int64_t)H * Is, 0, y};
+            const GemmArgs g{h, nullptr, 1, cap, offsets, split, El, cap, H, Is, w2, (int64_t)H * Is, 0, y};
             gemm_grouped<false><<<dim3((unsigned)L.grid), dim3(256), 0, s>>>(
                 g, TileClass{pre_s, cs_dn, part_s}, TileClass{pre, c_dn, part});
+            if ((err = hipGetLastError()) != hipSuccess) return err;
+        }
+        if (Is / BIG_BK >= SPLIT_MIN_NK) {
+            KernelTimer timer(MOE_K_SPLITK_REDUCE, s);
+            splitk_reduce<false><<<dim3(REDUCE_GRID), dim3(256), 0, s>>>(offsets, split, pre, El, cap, H, Is, L.grid,
+                                                                      part, y);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         return hipSuccess;

@@ -171,6 +171,18 @@ def test_grouped_ffn_stage(oracle, El, H, Is, T, k):
     assert_close_rel(got, ref, what=f"ffn El={El} H={H} Is={Is}")
 
 
+@pytest.mark.parametrize("El,H,Is,T,k", [(1, 512, 8192, 300, 1), (2, 8192, 256, 200, 1)])
+def test_grouped_ffn_long_k_split(oracle, El, H, Is, T, k):
+    """A long K (at least 128 slices of 64) with fewer large tiles than CUs
+    splits K over workgroups and combines the partials in a second kernel
+    (down projection in the first case, gate-up in the second); the result
+    matches the oracle and is bitwise reproducible."""
+    got, ref = ffn_case(oracle, El, H, Is, T, k, seed=El + H)
+    assert_close_rel(got, ref, what=f"long-K El={El} H={H} Is={Is}")
+    again, _ = ffn_case(oracle, El, H, Is, T, k, seed=El + H)
+    np.testing.assert_array_equal(got, again)
+
+
 @pytest.mark.parametrize("El,E,H,Is,T,k,e0", [(4, 4, 256, 192, 150, 2, 0), (3, 8, 512, 256, 300, 2, 2),
                                               (8, 8, 1024, 512, 257, 2, 0), (2, 16, 136, 72, 99, 3, 6)])
 def test_grouped_ffn_fused_gather(oracle, El, E, H, Is, T, k, e0):
