@@ -159,6 +159,8 @@ moe_status moe_combine(const uint16_t *y, int64_t y_rows, const int32_t *pair_to
  * waits for the recorded events and returns, for one kernel kind, the summed
  * duration in milliseconds and the number of launches since the last reset.
  * Kinds: see enum moe_kernel_kind.  Enabling allocates nothing on the device.
+ * Launches on a stream that is being captured into a HIP graph are not
+ * timed (a captured event record would not time the replay).
  */
 typedef enum moe_kernel_kind {
     MOE_K_ROUTE = 0,
@@ -173,6 +175,9 @@ typedef enum moe_kernel_kind {
 } moe_kernel_kind;
 
 moe_status moe_timing_enable(int enable);
+/* Time only the kinds whose bit (1 << kind) is set in `kinds` (0 disables);
+ * bits at or above MOE_K_COUNT give MOE_ERR_INVALID_ARG. */
+moe_status moe_timing_enable_mask(uint32_t kinds);
 moe_status moe_timing_reset(void);
 moe_status moe_timing_read(int kind, double *total_ms, int64_t *launches);
 

@@ -56,6 +56,7 @@ def lib():
         "moe_grouped_ffn": ([vp, i64, vp, i32, vp, i32, i64, i32, i32, vp, vp, vp, vp, sz, vp], i32),
         "moe_combine": ([vp, i64, vp, vp, i64, i32, i32, vp, i64, i64, i32, vp, vp], i32),
         "moe_timing_enable": ([i32], i32),
+        "moe_timing_enable_mask": ([ctypes.c_uint32], i32),
         "moe_timing_reset": ([], i32),
         "moe_timing_read": ([i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)], i32),
     }
@@ -208,8 +209,15 @@ def combine(y: torch.Tensor, pair_to_row: torch.Tensor, topk_w: torch.Tensor,
 
 
 # ---------------------------------------------------------------- timing
-def timing_enable(on: bool = True) -> None:
-    _check(lib().moe_timing_enable(1 if on else 0))
+def timing_enable(on: bool = True, kinds=None) -> None:
+    """Time every kernel kind (on), none, or only the named `kinds`."""
+    if kinds is None:
+        _check(lib().moe_timing_enable(1 if on else 0))
+    else:
+        mask = 0
+        for k in kinds:
+            mask |= 1 << KERNEL_KINDS[k]
+        _check(lib().moe_timing_enable_mask(mask if on else 0))
 
 
 def timing_reset() -> None:

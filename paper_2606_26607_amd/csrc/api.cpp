@@ -12,11 +12,17 @@ namespace {
 
 thread_local char g_msg[512] = "no error";
 
+moe_status vfail(moe_status st, const char *fmt, va_list ap)
+{
+    vsnprintf(g_msg, sizeof g_msg, fmt, ap);
+    return st;
+}
+
 moe_status fail(moe_status st, const char *fmt, ...)
 {
     va_list ap;
     va_start(ap, fmt);
-    vsnprintf(g_msg, sizeof g_msg, fmt, ap);
+    vfail(st, fmt, ap);
     va_end(ap);
     return st;
 }
@@ -50,6 +56,15 @@ moe_status check_width(const char *name, int v)
 
 }  // namespace
 
+moe_status moe::set_error(moe_status st, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vfail(st, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
 extern "C" const char *moe_status_str(int status)
 {
     switch (status) {
@@ -64,7 +79,7 @@ extern "C" const char *moe_status_str(int status)
 
 extern "C" const char *moe_last_error(void) { return g_msg; }
 
-extern "C" int moe_version(void) { return 2; }
+extern "C" int moe_version(void) { return 3; }
 
 extern "C" moe_status moe_route(const float *logits, int64_t T, int E, int k, int32_t *topk_ids,
                                 float *topk_w, void *stream)

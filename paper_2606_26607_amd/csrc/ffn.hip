@@ -26,6 +26,20 @@ __device__ __forceinline__ int64_t clamp_row(int32_t v, int64_t cap)
     return r > cap ? cap : r;
 }
 
+// SwiGLU of one gate/up pair: silu(g) * u = g / (1 + e^-g) * u, with the
+// hardware reciprocal (the result is rounded to bf16).
+__device__ __forceinline__ float silu_mul(float g, float u)
+{
+    return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
+}
+
+// Large-tile launches split K only from this many K-slices per tile.
+constexpr int SPLIT_MIN_NK = 128;
+// Time of a small-row K-slice relative to a large-tile one (measured: a
+// 32-row slice is bound by its weight rows, a 256-row one by MFMA), as the
+// fraction SMALL_COST_NUM / SMALL_COST_DEN.
+constexpr int SMALL_COST_NUM = 11, SMALL_COST_DEN = 20;
+
 // Block-wide exclusive scan of one value per thread (1024 threads); returns
 // the exclusive prefix and writes the total to *total (thread 1023).
 __device__ __forceinline__ int32_t block_exscan(int32_t v, int32_t *wsum, int32_t *total)
@@ -52,16 +66,30 @@ struct SchedShape {
     int nt_gu, nk_gu, nt_dn, nk_dn, grid;
 };
 
-// Estimated time of one GEMM's large-tile class of `tiles` tiles, in units
-// of one large-tile K-slice on one workgroup: whole rounds of the grid, or
-// the stream-K share (with its partial-sum traffic) when there are fewer
-// tiles than workgroups and K is long.
-__device__ __forceinline__ float large_cost(int64_t tiles, int nk, int grid)
+// Estimated time of one GEMM, in units of one large-tile K-slice on one
+// workgroup, for tl large and ts small-row tiles of nk K-slices: rounds of
+// large tiles (or their stream-K share, with its partial-sum traffic, when
+// there are fewer tiles than workgroups and K is long), plus
+// the small-row share (SMALL_COST_NUM / SMALL_COST_DEN of a large slice per
+// small-row slice) unless it fits on the workgroups the large tiles leave
+// idle in their last round.
+__device__ __forceinline__ float gemm_cost(int64_t tl, int64_t ts, int nk, int grid)
 {
-    if (tiles == 0) return 0.f;
-    const float t = (float)tiles, g = (float)grid;
-    if (tiles < grid && nk >= 64) return 1.25f * t * (float)nk / g;
-    return ceilf(t / g) * (float)nk;
+    const float t = (float)tl, g = (float)grid;
+    const bool split = tl < grid && nk >= SPLIT_MIN_NK;
+    const int rest = (int)(tl % grid);
+    float c = 0.f;
+    if (tl > 0 && split) {
+        c = 1.25f * t * (float)nk / g;
+    } else if (tl > 0) {
+        // a last round with a fraction f of the workgroups busy takes about
+        // 0.6 + 0.4 f of a full one (less contention for L2 and HBM)
+        c = (float)((tl - rest) / grid) * (float)nk;
+        if (rest) c += (0.6f + 0.4f * (float)rest / g) * (float)nk;
+    }
+    const int idle = rest ? grid - rest : 0;
+    if (!split && idle && SMALL_COST_NUM * ts <= (int64_t)SMALL_COST_DEN * idle) return c;
+    return c + (float)SMALL_COST_NUM / (float)SMALL_COST_DEN * (float)ts * (float)nk / g;
 }
 
 // Tile schedule of the grouped FFN.  An expert's rows [a, b) are cut at
@@ -72,8 +100,7 @@ __device__ __forceinline__ float large_cost(int64_t tiles, int nk, int grid)
 // empty large tile costs as much as a full one, while small-row tiles are
 // split evenly over the grid.  Which leftovers move (none, or those of at
 // most 32, 64 or 96 rows) is chosen for the lowest estimated time of both
-// GEMMs under a cost model (large_cost; a small-row K-slice costs 0.8 of a
-// large one).  small_max = 0 disables the small class.
+// GEMMs (gemm_cost).  small_max = 0 disables the small class.
 //   pre[e] / pre_small[e] = m-tiles of that class of the experts before e,
 //   pre[El] / pre_small[El] = totals.
 // Also clears the split-K tile counters (no memset node is needed, so the
@@ -89,6 +116,7 @@ __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restric
     __shared__ int32_t wsum[16];
     __shared__ int32_t part[16][2 * NC];
     __shared__ int32_t chosen;
+    __shared__ float cost[NC];
     const int e = threadIdx.x, lane = e & 63, wv = e >> 6;
     for (int64_t i = e; i < n_counters; i += 1024) counters[i] = 0;
     // rows fit int32: cap < 2^31 is checked on the host
@@ -132,24 +160,24 @@ __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restric
             }
         }
         __syncthreads();
-        if (e == 0) {
-            float best = 0.f;
-            for (int c = 0; c < NC && 32 * c <= small_max; ++c) {
-                int64_t tl = 0, ts = 0;
-                for (int w = 0; w < 16; ++w) {
-                    tl += part[w][2 * c];
-                    ts += part[w][2 * c + 1];
-                }
-                const float cost = large_cost(tl * sh.nt_gu, sh.nk_gu, sh.grid) +
-                                   large_cost(tl * sh.nt_dn, sh.nk_dn, sh.grid) +
-                                   0.8f * (float)(ts * (sh.nt_gu * sh.nk_gu + sh.nt_dn * sh.nk_dn)) /
-                                       (float)sh.grid;
-                if (c == 0 || cost < best) {
-                    best = cost;
-                    th = 32 * c;
-                }
+        // candidate c's estimate on thread c, the cheapest on thread 0 (ties:
+        // fewer moves)
+        if (e < NC) {
+            int64_t tl = 0, ts = 0;
+            for (int w = 0; w < 16; ++w) {
+                tl += part[w][2 * e];
+                ts += part[w][2 * e + 1];
             }
-            chosen = th;
+            cost[e] = 32 * e <= small_max ? gemm_cost(tl * sh.nt_gu, ts * sh.nt_gu, sh.nk_gu, sh.grid) +
+                                                gemm_cost(tl * sh.nt_dn, ts * sh.nt_dn, sh.nk_dn, sh.grid)
+                                          : 3.0e38f;
+        }
+        __syncthreads();
+        if (e == 0) {
+            int b = 0;
+            for (int c = 1; c < NC; ++c)
+                if (cost[c] < cost[b]) b = c;
+            chosen = 32 * b;
         }
         __syncthreads();
         th = chosen;
@@ -247,7 +275,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t *__restrict__ 
             const int64_t row = r0 + wm * 32 + 8 * (i / 4) + 4 * (lane >> 5) + (i % 4);
             if (row < r1 && col < N) {
                 float v = acc_g[i];
-                if (GATED) v = v / (1.0f + expf(-v)) * acc_u[i];
+                if (GATED) v = silu_mul(v, acc_u[i]);
                 C[row * N + col] = f32_to_bf16(v);
             }
         }
@@ -455,9 +483,6 @@ __device__ __forceinline__ TileCoord tile_coord(int64_t tile, const int32_t *__r
     return c;
 }
 
-// Large-tile launches split K only from this many K-slices per tile.
-constexpr int SPLIT_MIN_NK = 128;
-
 // A partial accumulator slot holds one fp32 value per accumulator register
 // of each of the 256 threads, stored register-major so each access is a
 // coalesced 16-byte vector per lane.
@@ -539,7 +564,8 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                                            const int32_t *__restrict__ tile_prefix, int El, int64_t cap,
                                            int N, int K, const uint16_t *__restrict__ W, int64_t w_stride,
                                            int up_off, uint16_t *__restrict__ C,
-                                           int32_t *__restrict__ tile_cnt, float *__restrict__ partials)
+                                           int32_t *__restrict__ tile_cnt, float *__restrict__ partials,
+                                           int grp_base, int grp_size)
 {
     constexpr int A_STAGE = BMt * CPR, B_STAGE = BNt * CPR;  // 16-byte chunks per slot
     constexpr int A_INS = BMt / RPI / 4, B_INS = BNt / RPI / 4;
@@ -558,12 +584,15 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
     const int wm = wave / WN, wn = wave % WN;
     const int n_tiles = (N + OUTN - 1) / OUTN;
     const int nk = K / BIG_BK;
-    const WorkSplit ws((int64_t)tile_prefix[El] * n_tiles, nk, gridDim.x, TAIL);
+    // the class runs on workgroups [grp_base, grp_base + grp_size) of the
+    // XCD-aware numbering below, renumbered from 0
+    const WorkSplit ws((int64_t)tile_prefix[El] * n_tiles, nk, grp_size, TAIL);
     if (ws.T == 0) return;
     // XCD-aware numbering: the 8 dies take workgroups round robin, so the
     // workgroups of one die get consecutive virtual ids and with them a
     // contiguous run of tiles (shared panels in that die's L2).
-    const int v = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+    const int v = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3) - grp_base;
+    if (v < 0 || v >= grp_size) return;
     // This lane's chunk within a DMA instruction: row lane/CPR of the
     // instruction's rows, LDS position lane%CPR, global chunk
     // (lane%CPR) ^ swz(row); swz depends on the instruction only through its
@@ -826,7 +855,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                 for (int q = 0; q < 16; ++q) {
                     const int row = wm * (BMt / WM) + i * 32 + 8 * (q / 4) + 4 * (lane >> 5) + (q % 4);
                     float o = acc[i][j][q];
-                    if (GATED) o = o / (1.0f + __expf(-o)) * acc[i][j + NB / 2][q];
+                    if (GATED) o = silu_mul(o, acc[i][j + NB / 2][q]);
                     stage_out[row * OUTN + col] = bf16_bits(o);
                 }
             }
@@ -869,22 +898,45 @@ constexpr int BIG_RING = (A_SLOTS * BIGM + B_SLOTS * BIGN) * CPR;
 constexpr int SLOT_SMALL = (SMALLM / 32) * (BIGN / 4 / 32) * 16 * 256;
 constexpr int SLOT_BIG = (BIGM / 2 / 32) * (BIGN / 2 / 32) * 16 * 256;
 
-// One grouped GEMM launch: the small-row class first (32-row tiles, K-split
-// over the whole grid: these stream weights, and spreading them over every
-// CU is what reaches HBM bandwidth), then the large-tile class (256-row
-// tiles) in the same persistent grid.  The classes cover disjoint rows, so a
-// workgroup goes on to the second without waiting for the first.
+// Where the small-row class runs: on the workgroups the large tiles leave
+// idle in their last round when its work fits there (its slices, weighted
+// SMALL_COST_NUM / SMALL_COST_DEN, add up to at most one large tile per idle
+// workgroup), else on all workgroups after their large tiles.
+struct SmallGroup {
+    int base, size;
+};
+
+__device__ __forceinline__ SmallGroup small_group(int64_t tl, int64_t ts, int nk, int G)
+{
+    const bool large_dp = !(tl < G && nk >= SPLIT_MIN_NK);
+    if (large_dp && tl > 0 && tl % G != 0) {
+        const int64_t idle = G - tl % G;
+        if (SMALL_COST_NUM * ts <= SMALL_COST_DEN * idle) return SmallGroup{(int)(tl % G), (int)idle};
+    }
+    return SmallGroup{0, G};
+}
+
+// One grouped GEMM launch: the large-tile class (256-row tiles) and the
+// small-row class (32-row tiles, K-split over its workgroups: these stream
+// weights, and spreading them over many CUs is what reaches HBM bandwidth)
+// in the same persistent grid.  The classes cover disjoint rows, so a
+// workgroup goes from its large tiles to its small-row share without
+// waiting for anyone.
 template <bool GATED>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
 void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
 {
     __shared__ uint4 ring[BIG_RING];
-    gemm_class<SMALLM, BIGN, GATED, 1, true>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split,
-                                             small.tile_prefix, g.El, g.cap, g.N, g.K, g.W, g.w_stride,
-                                             g.up_off, g.C, small.tile_cnt, small.partials);
+    constexpr int OUTN = GATED ? BIGN / 2 : BIGN;
+    const int64_t n_tiles = (g.N + OUTN - 1) / OUTN;
+    const SmallGroup sg = small_group((int64_t)large.tile_prefix[g.El] * n_tiles,
+                                      (int64_t)small.tile_prefix[g.El] * n_tiles, g.K / BIG_BK, gridDim.x);
     gemm_class<BIGM, BIGN, GATED, 2, false>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split,
                                             large.tile_prefix, g.El, g.cap, g.N, g.K, g.W, g.w_stride,
-                                            g.up_off, g.C, large.tile_cnt, large.partials);
+                                            g.up_off, g.C, large.tile_cnt, large.partials, 0, gridDim.x);
+    gemm_class<SMALLM, BIGN, GATED, 1, true>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split,
+                                             small.tile_prefix, g.El, g.cap, g.N, g.K, g.W, g.w_stride,
+                                             g.up_off, g.C, small.tile_cnt, small.partials, sg.base, sg.size);
 }
 
 // Combines the split-K partials of the large-tile class after its GEMM
@@ -940,7 +992,7 @@ __global__ __launch_bounds__(256) void splitk_reduce(const int32_t *__restrict__
             const int64_t row = tc.r0 + wm * (BIGM / WM) + i * 32 + 8 * (r / 4) + 4 * (lane >> 5) + (r % 4);
             if (row >= tc.r1) continue;
             float o = g[r];
-            if (GATED) o = o / (1.0f + __expf(-o)) * u[r];
+            if (GATED) o = silu_mul(o, u[r]);
             C[row * N + tc.n0 + col] = bf16_bits(o);
         }
     }

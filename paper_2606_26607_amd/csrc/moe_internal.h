@@ -35,6 +35,9 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
     return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
+// Records a message for moe_last_error() on the calling thread and returns st.
+moe_status set_error(moe_status st, const char *fmt, ...);
+
 // ------------------------------------------------------------- timing
 // Record around every kernel launch when timing is enabled (see timing.cpp).
 struct KernelTimer {

@@ -15,7 +15,7 @@ struct Record {
 constexpr size_t kMaxRecords = 1 << 16;
 
 std::mutex g_mu;
-bool g_enabled = false;
+uint32_t g_mask = 0;  // bit k set: kernels of kind k are timed
 std::vector<Record> g_pool;  // events are created once and reused
 size_t g_used = 0;
 
@@ -24,7 +24,7 @@ size_t g_used = 0;
 KernelTimer::KernelTimer(int kind, hipStream_t stream) : slot(-1), s(stream)
 {
     std::lock_guard<std::mutex> lk(g_mu);
-    if (!g_enabled || g_used >= kMaxRecords) return;
+    if (!((g_mask >> kind) & 1u) || g_used >= kMaxRecords) return;
     if (g_used == g_pool.size()) {
         Record r{kind, nullptr, nullptr};
         if (hipEventCreate(&r.start) != hipSuccess) return;
@@ -34,6 +34,10 @@ KernelTimer::KernelTimer(int kind, hipStream_t stream) : slot(-1), s(stream)
         }
         g_pool.push_back(r);
     }
+    // not under stream capture: a captured record would only order the graph,
+    // it would not time anything
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return;
     Record &r = g_pool[g_used];
     r.kind = kind;
     if (hipEventRecord(r.start, s) != hipSuccess) return;
@@ -54,15 +58,25 @@ using namespace moe;
 extern "C" moe_status moe_timing_enable(int enable)
 {
     std::lock_guard<std::mutex> lk(g_mu);
-    g_enabled = enable != 0;
+    g_mask = enable ? (1u << MOE_K_COUNT) - 1u : 0u;
+    return MOE_OK;
+}
+
+extern "C" moe_status moe_timing_enable_mask(uint32_t kinds)
+{
+    if (kinds >> MOE_K_COUNT) return set_error(MOE_ERR_INVALID_ARG, "moe_timing_enable_mask: 0x%x", kinds);
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_mask = kinds;
     return MOE_OK;
 }
 
 extern "C" moe_status moe_timing_reset(void)
 {
     std::lock_guard<std::mutex> lk(g_mu);
-    for (size_t i = 0; i < g_used; ++i)
-        if (hipEventSynchronize(g_pool[i].stop) != hipSuccess) return MOE_ERR_HIP;
+    for (size_t i = 0; i < g_used; ++i) {
+        const hipError_t err = hipEventSynchronize(g_pool[i].stop);
+        if (err != hipSuccess) return set_error(MOE_ERR_HIP, "moe_timing_reset: %s", hipGetErrorString(err));
+    }
     g_used = 0;
     return MOE_OK;
 }
@@ -70,15 +84,16 @@ extern "C" moe_status moe_timing_reset(void)
 extern "C" moe_status moe_timing_read(int kind, double *total_ms, int64_t *launches)
 {
     if (total_ms == nullptr || launches == nullptr || kind < 0 || kind >= MOE_K_COUNT)
-        return MOE_ERR_INVALID_ARG;
+        return set_error(MOE_ERR_INVALID_ARG, "moe_timing_read: bad kind %d or null output", kind);
     std::lock_guard<std::mutex> lk(g_mu);
     double sum = 0.0;
     int64_t n = 0;
     for (size_t i = 0; i < g_used; ++i) {
         if (g_pool[i].kind != kind) continue;
-        if (hipEventSynchronize(g_pool[i].stop) != hipSuccess) return MOE_ERR_HIP;
+        hipError_t err = hipEventSynchronize(g_pool[i].stop);
         float ms = 0.f;
-        if (hipEventElapsedTime(&ms, g_pool[i].start, g_pool[i].stop) != hipSuccess) return MOE_ERR_HIP;
+        if (err == hipSuccess) err = hipEventElapsedTime(&ms, g_pool[i].start, g_pool[i].stop);
+        if (err != hipSuccess) return set_error(MOE_ERR_HIP, "moe_timing_read: %s", hipGetErrorString(err));
         sum += ms;
         ++n;
     }
