@@ -64,10 +64,11 @@ def kernel_source_sha() -> str:
     return hashlib.sha256(open(path, "rb").read()).hexdigest()
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per gate-up launch from the committed rocprofv3 counter
-    summary (FETCH_SIZE + WRITE_SIZE scaled by the copy-kernel calibration),
-    or None when there is none for this kernel source."""
+def measured_traffic(workload: str, per: str = "dispatch"):
+    """HBM bytes of the gate-up GEMM per launch (per="dispatch") or summed
+    over one step's launches (per="step") from the committed rocprofv3
+    counter summary (FETCH_SIZE + WRITE_SIZE scaled by the copy-kernel
+    calibration), or None when there is none for this kernel source."""
     path = os.path.join(ROOT, "profiles", f"gate_up_{workload}_counters.txt")
     if not os.path.exists(path):
         return None
@@ -79,7 +80,7 @@ def measured_traffic(workload: str):
     if kv.get("kernel_source_sha256") != kernel_source_sha():
         return None
     try:
-        return float(kv["hbm_bytes_per_dispatch"])
+        return float(kv[f"hbm_bytes_per_{per}"])
     except (KeyError, ValueError):
         return None
 
@@ -228,7 +229,7 @@ def main():
         if decode:
             achieved = work["gate_up_bytes"] / dur_s / 1e9
             roof = dict(bound="hbm", achieved=achieved, peak=PEAK_HBM_GBS, unit="GB/s",
-                        frac=achieved / PEAK_HBM_GBS, traffic=measured_traffic(cfg.name), kernel=dom,
+                        frac=achieved / PEAK_HBM_GBS, traffic=measured_traffic(cfg.name, "step"), kernel=dom,
                         launches_per_step=gu["launches"] // args.steps,
                         algorithmic_per_step=work["gate_up_bytes"])
         else:
