@@ -308,7 +308,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t *__restrict__ 
 constexpr int BIG_BK = 64;        // K per slice
 constexpr int CPR = BIG_BK / 8;   // 16-byte chunks per LDS row
 constexpr int RPI = 64 / CPR;     // rows per DMA instruction
-constexpr int A_SLOTS = 2, B_SLOTS = 3;
+constexpr int A_SLOTS = 2, B_SLOTS = 3;        // large tiles: A(s+1), B(s+2) in flight
+constexpr int SA_SLOTS = 3, SB_SLOTS = 4;      // small-row tiles: A(s+2), B(s+3) in flight
+constexpr int BIG_RING_CHUNKS = (A_SLOTS * 256 + B_SLOTS * 256) * CPR;  // 160 KB of 16-byte chunks
+constexpr int GEMM_WAVES = 8;                  // waves per workgroup: two per SIMD
+constexpr int GEMM_THREADS = GEMM_WAVES * 64;
 
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
@@ -381,14 +385,14 @@ struct SliceSrc {
 template <int BMt>
 __device__ __forceinline__ void issue_a(const SliceSrc &a, uint32_t slot, int k0, int q)
 {
-    constexpr int A_INS = BMt / RPI / 4;
+    constexpr int A_INS = BMt / RPI / GEMM_WAVES;
     dma16(a.ra, slot + (a.wave * A_INS + q) * 1024, a.voa[q], (uint32_t)k0 * 2u);
 }
 
 template <int BNt>
 __device__ __forceinline__ void issue_b(const SliceSrc &a, uint32_t slot, int k0, int q)
 {
-    constexpr int B_INS = BNt / RPI / 4;
+    constexpr int B_INS = BNt / RPI / GEMM_WAVES;
     dma16(a.rb, slot + (a.wave * B_INS + q) * 1024, a.vob[q], (uint32_t)k0 * 2u);
 }
 
@@ -556,7 +560,7 @@ struct TileClass {
 // workgroup's LDS (at least the class's ring size).  Pointers are restrict
 // parameters so that the inlined body keeps the no-alias facts of kernel
 // arguments (its loads are not reordered around the stores it makes).
-template <int BMt, int BNt, bool GATED, int WM, bool TAIL>
+template <int BMt, int BNt, bool GATED, int WM, bool TAIL, int ASL, int BSL>
 __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restrict__ A,
                                            const int32_t *__restrict__ row_index, int kdiv, int64_t a_rows,
                                            const int32_t *__restrict__ offsets,
@@ -568,16 +572,21 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                                            int grp_base, int grp_size)
 {
     constexpr int A_STAGE = BMt * CPR, B_STAGE = BNt * CPR;  // 16-byte chunks per slot
-    constexpr int A_INS = BMt / RPI / 4, B_INS = BNt / RPI / 4;
-    constexpr int WN = 4 / WM;                      // waves in a WM x WN grid
+    constexpr int A_INS = BMt / RPI / GEMM_WAVES, B_INS = BNt / RPI / GEMM_WAVES;
+    constexpr int WN = GEMM_WAVES / WM;             // waves in a WM x WN grid
     constexpr int MB = BMt / WM / 32;               // 32-row blocks per wave
     constexpr int NB = BNt / WN / 32;               // 32-col blocks per wave (gate+up when gated)
     constexpr int OUTN = GATED ? BNt / 2 : BNt;     // output columns per tile
     static_assert(MB >= 1 && NB >= (GATED ? 2 : 1), "tile too small for the wave grid");
-    constexpr int RING = A_SLOTS * A_STAGE + B_SLOTS * B_STAGE;
+    // ring slots: ASL for A, BSL for B; under slice s go out A(s+LA) and
+    // B(s+LA+1)
+    constexpr int LA = ASL - 1;
+    static_assert(BSL == ASL + 1 && (LA == 1 || LA == 2), "ring depths");
+    constexpr int RING = ASL * A_STAGE + BSL * B_STAGE;
+    static_assert(RING <= BIG_RING_CHUNKS, "rings exceed the workgroup's LDS");
     static_assert(A_INS >= 1 && B_INS >= 2 && B_INS % 2 == 0, "DMA instruction split");
     static_assert(BMt * OUTN * 2 <= RING * 16, "epilogue staging must fit the rings");
-    constexpr int SLOT = MB * NB * 16 * 256;        // floats per partial slot
+    constexpr int SLOT = MB * NB * 16 * GEMM_THREADS;  // floats per partial slot
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
@@ -600,7 +609,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
     const int lrow = lane >> 3;
     const uint32_t ring_base = lds_addr(ring);
     const uint4 *const a_ring = ring;
-    const uint4 *const b_ring = ring + A_SLOTS * A_STAGE;
+    const uint4 *const b_ring = ring + ASL * A_STAGE;
 
     // this lane's LDS rows for its MFMA fragments
     int arow[MB], brow[NB];
@@ -624,7 +633,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
         const uint4 *so = ring;
         constexpr int CH_ROW = OUTN / 8;
         const int rows = (int)(r1 - r0);
-        for (int c = tid; c < BMt * CH_ROW; c += 256) {
+        for (int c = tid; c < BMt * CH_ROW; c += GEMM_THREADS) {
             const int row = c / CH_ROW, cc = c % CH_ROW;
             if (row < rows && cc * 8 < nvalid)
                 *reinterpret_cast<uint4 *>(C + (r0 + row) * N + n0 + cc * 8) = so[c];
@@ -677,67 +686,77 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
             for (int j = 0; j < NB; ++j) acc[i][j] = f32x16_t{};
         Frags<MB, NB> f;
 
-        // Slices klo..khi-1 (local index j): A(j) in A slot j % 2, B(j) in B
-        // slot j % 3.  Under slice s go out A(s+1) (k-steps 0-1) and B(s+2)
-        // (k-steps 2-3), into the slots that slice s-1 freed.
+        // Slices klo..khi-1 (local index j): A(j) in A slot j % ASL, B(j) in
+        // B slot j % BSL.  Loads go out in pairs (A(t), B(t+1)) after B(0):
+        // the prologue issues pairs t < LA, slice s issues pair s+LA (A under
+        // k-steps 0-1, B under k-steps 2-3) into the slots slice s-1 freed.
         const int ns = khi - klo;  // slices in this piece (>= 1)
         auto kof = [&](int j) { return (klo + j) * BIG_BK; };
-        auto a_slot = [&](int j) { return ring_base + (uint32_t)((j % A_SLOTS) * A_STAGE * 16); };
-        auto b_slot = [&](int j) { return ring_base + (uint32_t)((A_SLOTS * A_STAGE + (j % B_SLOTS) * B_STAGE) * 16); };
-        auto a_ptr = [&](int j) { return a_ring + (j % A_SLOTS) * A_STAGE; };
-        auto b_ptr = [&](int j) { return b_ring + (j % B_SLOTS) * B_STAGE; };
-        // prologue: B(0), A(0), B(1); wait for the first two
+        auto a_slot = [&](int j) { return ring_base + (uint32_t)((j % ASL) * A_STAGE * 16); };
+        auto b_slot = [&](int j) { return ring_base + (uint32_t)((ASL * A_STAGE + (j % BSL) * B_STAGE) * 16); };
+        auto a_ptr = [&](int j) { return a_ring + (j % ASL) * A_STAGE; };
+        auto b_ptr = [&](int j) { return b_ring + (j % BSL) * B_STAGE; };
+        // prologue: B(0), then (A(t), B(t+1)) for t < LA; wait for A(0), B(0)
 #pragma unroll
         for (int q = 0; q < B_INS; ++q) issue_b<BNt>(src, b_slot(0), kof(0), q);
 #pragma unroll
-        for (int q = 0; q < A_INS; ++q) issue_a<BMt>(src, a_slot(0), kof(0), q);
-        if (ns > 1) {
+        for (int t = 0; t < LA; ++t) {
+            if (t < ns) {
 #pragma unroll
-            for (int q = 0; q < B_INS; ++q) issue_b<BNt>(src, b_slot(1), kof(1), q);
-            asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(B_INS) : "memory");
-        } else {
-            asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+                for (int q = 0; q < A_INS; ++q) issue_a<BMt>(src, a_slot(t), kof(t), q);
+            }
+            if (t + 1 < ns) {
+#pragma unroll
+                for (int q = 0; q < B_INS; ++q) issue_b<BNt>(src, b_slot(t + 1), kof(t + 1), q);
+            }
         }
+        // issued after A(0): B(1), then the pairs 1 .. LA-1
+        if (ns > LA) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(B_INS + (LA - 1) * (A_INS + B_INS)) : "memory");
+        else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
         lds_barrier();
         load_frags(f, 0, a_ptr(0), b_ptr(0), 0, arow, brow);
 
-        // One slice.  HAVE_A: A(s+1) exists; HAVE_B: B(s+2) exists; A and B
-        // loads absent at the tail keep the MFMA runs free of branches.
+        // One slice.  HAVE_A: A(s+LA) exists; HAVE_B: B(s+LA+1) exists; loads
+        // absent at the tail keep the MFMA runs free of branches.
         auto slice = [&](int s, auto have_a, auto have_b) {
             constexpr bool HA = decltype(have_a)::value, HB = decltype(have_b)::value;
+            // loads issued after A(s+1) when this slice hands over: B(s+2) ..
+            // B(s+LA), A(s+2) .. A(s+LA) and the first half of B(s+LA+1)
+            constexpr int AFTER = HA ? (LA - 1) * (A_INS + B_INS) + (HB ? B_INS / 2 : 0) : 0;
             const uint4 *sa = a_ptr(s), *sb = b_ptr(s);
             load_frags(f, 1, sa, sb, 1, arow, brow);
             __builtin_amdgcn_sched_barrier(0);
-            mfma_step<0, HA ? A_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 0, src, a_slot(s + 1), kof(s + 1), 0);
+            mfma_step<0, HA ? A_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 0, src, a_slot(s + LA), kof(s + LA), 0);
             __builtin_amdgcn_sched_barrier(0);
             load_frags(f, 0, sa, sb, 2, arow, brow);
             __builtin_amdgcn_sched_barrier(0);
-            mfma_step<0, HA ? A_INS - A_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 1, src, a_slot(s + 1), kof(s + 1),
-                                                                   A_INS / 2);
+            mfma_step<0, HA ? A_INS - A_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 1, src, a_slot(s + LA),
+                                                                   kof(s + LA), A_INS / 2);
             __builtin_amdgcn_sched_barrier(0);
             load_frags(f, 1, sa, sb, 3, arow, brow);
             __builtin_amdgcn_sched_barrier(0);
-            mfma_step<1, HB ? B_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 0, src, b_slot(s + 2), kof(s + 2), 0);
+            mfma_step<1, HB ? B_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 0, src, b_slot(s + LA + 1), kof(s + LA + 1),
+                                                           0);
             __builtin_amdgcn_sched_barrier(0);
-            if (HA) {
-                // hand over to slice s+1: A(s+1) and B(s+1) have landed when at
-                // most the B(s+2) loads just issued are outstanding
-                if (HB) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(B_INS / 2) : "memory");
+            if (HA || s + 1 < ns) {
+                // hand over to slice s+1 once A(s+1) (and B(s+1), issued before
+                // it) have landed
+                if (AFTER > 0) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(AFTER) : "memory");
                 else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
                 lds_barrier();
                 load_frags(f, 0, a_ptr(s + 1), b_ptr(s + 1), 0, arow, brow);
                 __builtin_amdgcn_sched_barrier(0);
             }
-            mfma_step<1, HB ? B_INS - B_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 1, src, b_slot(s + 2), kof(s + 2),
-                                                                   B_INS / 2);
+            mfma_step<1, HB ? B_INS - B_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 1, src, b_slot(s + LA + 1),
+                                                                   kof(s + LA + 1), B_INS / 2);
             __builtin_amdgcn_sched_barrier(0);
         };
         using T_ = std::true_type;
         using F_ = std::false_type;
         int s = 0;
-        for (; s + 2 < ns; ++s) slice(s, T_{}, T_{});
-        if (s + 1 < ns) slice(s++, T_{}, F_{});
-        slice(s, F_{}, F_{});
+        for (; s + LA + 1 < ns; ++s) slice(s, T_{}, T_{});
+        for (; s + LA < ns; ++s) slice(s, T_{}, F_{});
+        for (; s < ns; ++s) slice(s, F_{}, F_{});
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         lds_barrier();  // every wave is done with the ring before it is reused
 
@@ -770,7 +789,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                                                     acc[i][j][4 * q + 3]);
                             __builtin_amdgcn_raw_buffer_store_b128(
                                 *reinterpret_cast<u32x4_t *>(&pv), pr,
-                                base_b + (uint32_t)((((i * NB + j) * 4 + q) * 256 + tid) * 16), 0, SC1);
+                                base_b + (uint32_t)((((i * NB + j) * 4 + q) * GEMM_THREADS + tid) * 16), 0, SC1);
                         }
             }
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // partial is visible device-wide
@@ -797,12 +816,13 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
             auto add_partial = [&](int c, bool assign) {
                 constexpr int CH = NB * 4;
                 const uint32_t base_c = (uint32_t)(slot_of(c) * SLOT * 4);
+                constexpr int JQ = GEMM_THREADS * 16;  // bytes of one (j, q) chunk of the slot
                 auto issue = [&](int i) {
-                    const uint32_t buf = ring_base + (uint32_t)((i & 1) * CH * 4096);
+                    const uint32_t buf = ring_base + (uint32_t)((i & 1) * CH * JQ);
 #pragma unroll
                     for (int jq = 0; jq < CH; ++jq)
-                        dma16_sc1(pdesc, buf + jq * 4096 + wave * 1024, (uint32_t)(jq * 4096 + tid * 16),
-                              base_c + (uint32_t)(i * CH * 4096));
+                        dma16_sc1(pdesc, buf + jq * JQ + wave * 1024, (uint32_t)(jq * JQ + tid * 16),
+                                  base_c + (uint32_t)(i * CH * JQ));
                 };
                 issue(0);
 #pragma unroll
@@ -814,12 +834,12 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                     } else {
                         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
                     }
-                    const uint4 *bp = ring + (i & 1) * CH * 256;
+                    const uint4 *bp = ring + (i & 1) * CH * GEMM_THREADS;
 #pragma unroll
                     for (int j = 0; j < NB; ++j)
 #pragma unroll
                         for (int q = 0; q < 4; ++q) {
-                            const uint4 w = bp[(j * 4 + q) * 256 + tid];
+                            const uint4 w = bp[(j * 4 + q) * GEMM_THREADS + tid];
                             const float pv[4] = {__uint_as_float(w.x), __uint_as_float(w.y),
                                                  __uint_as_float(w.z), __uint_as_float(w.w)};
 #pragma unroll
@@ -890,13 +910,15 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
 }
 
 constexpr int BIGM = 256, BIGN = 256;  // large tiles: 256 rows x 256 weight rows
-constexpr int SMALLM = 32;             // small-row tiles: 32 rows x 256 weight rows
+constexpr int BIG_WM = 4;              // ... 4 x 2 waves of 64 x 128
+constexpr int SMALLM = 64;             // small-row tiles: 64 rows x 256 weight rows
+constexpr int SMALL_WM = 2;            // ... 2 x 4 waves of 32 x 64
 constexpr int SMALL_MAX = 96;          // experts with at most this many rows use small-row tiles
 constexpr int REDUCE_GRID = 2048;      // workgroups of the split-K reduction
-constexpr int BIG_RING = (A_SLOTS * BIGM + B_SLOTS * BIGN) * CPR;
+constexpr int BIG_RING = BIG_RING_CHUNKS;
 // floats per partial slot of each class (one per accumulator register)
-constexpr int SLOT_SMALL = (SMALLM / 32) * (BIGN / 4 / 32) * 16 * 256;
-constexpr int SLOT_BIG = (BIGM / 2 / 32) * (BIGN / 2 / 32) * 16 * 256;
+constexpr int SLOT_SMALL = (SMALLM / SMALL_WM / 32) * (BIGN / (GEMM_WAVES / SMALL_WM) / 32) * 16 * GEMM_THREADS;
+constexpr int SLOT_BIG = (BIGM / BIG_WM / 32) * (BIGN / (GEMM_WAVES / BIG_WM) / 32) * 16 * GEMM_THREADS;
 
 // Where the small-row class runs: on the workgroups the large tiles leave
 // idle in their last round when its work fits there (its slices, weighted
@@ -923,7 +945,7 @@ __device__ __forceinline__ SmallGroup small_group(int64_t tl, int64_t ts, int nk
 // workgroup goes from its large tiles to its small-row share without
 // waiting for anyone.
 template <bool GATED>
-__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
+__global__ __attribute__((amdgpu_flat_work_group_size(GEMM_THREADS, GEMM_THREADS), amdgpu_waves_per_eu(2, 2)))
 void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
 {
     __shared__ uint4 ring[BIG_RING];
@@ -931,10 +953,10 @@ void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
     const int64_t n_tiles = (g.N + OUTN - 1) / OUTN;
     const SmallGroup sg = small_group((int64_t)large.tile_prefix[g.El] * n_tiles,
                                       (int64_t)small.tile_prefix[g.El] * n_tiles, g.K / BIG_BK, gridDim.x);
-    gemm_class<BIGM, BIGN, GATED, 2, false>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split,
+    gemm_class<BIGM, BIGN, GATED, BIG_WM, false, A_SLOTS, B_SLOTS>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split,
                                             large.tile_prefix, g.El, g.cap, g.N, g.K, g.W, g.w_stride,
                                             g.up_off, g.C, large.tile_cnt, large.partials, 0, gridDim.x);
-    gemm_class<SMALLM, BIGN, GATED, 1, true>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split,
+    gemm_class<SMALLM, BIGN, GATED, SMALL_WM, true, SA_SLOTS, SB_SLOTS>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split,
                                              small.tile_prefix, g.El, g.cap, g.N, g.K, g.W, g.w_stride,
                                              g.up_off, g.C, small.tile_cnt, small.partials, sg.base, sg.size);
 }
@@ -946,14 +968,14 @@ void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
 // contributor order (deterministic), then the epilogue of the GEMM is
 // applied (SwiGLU when gated) and the bf16 result written.
 template <bool GATED>
-__global__ __launch_bounds__(256) void splitk_reduce(const int32_t *__restrict__ offsets,
+__global__ __launch_bounds__(GEMM_THREADS) void splitk_reduce(const int32_t *__restrict__ offsets,
                                                      const int32_t *__restrict__ split,
                                                      const int32_t *__restrict__ tile_prefix, int El,
                                                      int64_t cap, int N, int K, int G,
                                                      const float *__restrict__ partials,
                                                      uint16_t *__restrict__ C)
 {
-    constexpr int WM = 2, WN = 2;
+    constexpr int WM = BIG_WM, WN = GEMM_WAVES / BIG_WM;
     constexpr int MB = BIGM / WM / 32, NB = BIGN / WN / 32;
     constexpr int OUTN = GATED ? BIGN / 2 : BIGN;
     constexpr int JJ = GATED ? NB / 2 : NB;  // output blocks per wave row
@@ -977,10 +999,10 @@ __global__ __launch_bounds__(256) void splitk_reduce(const int32_t *__restrict__
                 partials + (c * 2 + (ws.begin(c) >= tb ? 0 : 1)) * (int64_t)SLOT_BIG);
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                const float4 pg = slot[((i * NB + j) * 4 + q) * 256 + tid];
+                const float4 pg = slot[((i * NB + j) * 4 + q) * GEMM_THREADS + tid];
                 g[4 * q] += pg.x; g[4 * q + 1] += pg.y; g[4 * q + 2] += pg.z; g[4 * q + 3] += pg.w;
                 if (GATED) {
-                    const float4 pu = slot[((i * NB + j + NB / 2) * 4 + q) * 256 + tid];
+                    const float4 pu = slot[((i * NB + j + NB / 2) * 4 + q) * GEMM_THREADS + tid];
                     u[4 * q] += pu.x; u[4 * q + 1] += pu.y; u[4 * q + 2] += pu.z; u[4 * q + 3] += pu.w;
                 }
             }
@@ -1087,26 +1109,26 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
         {
             KernelTimer timer(MOE_K_GATE_UP, s);
             const GemmArgs g{x, row_index, kdiv, x_rows, offsets, split, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h};
-            gemm_grouped<true><<<dim3((unsigned)L.grid), dim3(256), 0, s>>>(
+            gemm_grouped<true><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
                 g, TileClass{pre_s, cs_gu, part_s}, TileClass{pre, c_gu, part});
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         if (H / BIG_BK >= SPLIT_MIN_NK) {  // the large tiles may have been split over K
             KernelTimer timer(MOE_K_SPLITK_REDUCE, s);
-            splitk_reduce<true><<<dim3(REDUCE_GRID), dim3(256), 0, s>>>(offsets, split, pre, El, cap, Is, H, L.grid,
+            splitk_reduce<true><<<dim3(REDUCE_GRID), dim3(GEMM_THREADS), 0, s>>>(offsets, split, pre, El, cap, Is, H, L.grid,
                                                                      part, h);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         {
             KernelTimer timer(MOE_K_DOWN, s);
             const GemmArgs g{h, nullptr, 1, cap, offsets, split, El, cap, H, Is, w2, (int64_t)H * Is, 0, y};
-            gemm_grouped<false><<<dim3((unsigned)L.grid), dim3(256), 0, s>>>(
+            gemm_grouped<false><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
                 g, TileClass{pre_s, cs_dn, part_s}, TileClass{pre, c_dn, part});
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         if (Is / BIG_BK >= SPLIT_MIN_NK) {
             KernelTimer timer(MOE_K_SPLITK_REDUCE, s);
-            splitk_reduce<false><<<dim3(REDUCE_GRID), dim3(256), 0, s>>>(offsets, split, pre, El, cap, H, Is, L.grid,
+            splitk_reduce<false><<<dim3(REDUCE_GRID), dim3(GEMM_THREADS), 0, s>>>(offsets, split, pre, El, cap, H, Is, L.grid,
                                                                       part, y);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
