@@ -51,42 +51,66 @@ __global__ __launch_bounds__(64) void count_kernel(const int32_t *__restrict__ i
 }
 
 // One block of 1024 threads.  chunk_cnt [nchunks, El] is rewritten in place
-// with each (chunk, expert)'s first output row.
+// with each (chunk, expert)'s first output row.  Each expert gets a group of
+// L lanes (L = the largest power of two <= 1024/El, at most 64, so a group
+// lies in one wavefront); lane j of the group owns a contiguous run of
+// chunks.  Runs are summed, scanned across the group with shuffles, the
+// expert totals scanned across the block, and each lane then writes its
+// chunks' first rows.
 __global__ __launch_bounds__(1024) void scan_kernel(int32_t *__restrict__ chunk_cnt, int64_t nchunks,
-                                                    int El, int32_t *__restrict__ counts,
+                                                    int El, int L, int32_t *__restrict__ counts,
                                                     int32_t *__restrict__ offsets)
 {
     __shared__ int32_t tot[1024];
     __shared__ int32_t wsum[16];
-    const int e = threadIdx.x;
+    const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+    const int e = t / L, j = t % L;
+    const bool active = e < El;
+    const int64_t per = (nchunks + L - 1) / L;
+    const int64_t c0 = (int64_t)j * per;
+    const int64_t c1 = c0 + per < nchunks ? c0 + per : nchunks;
     int32_t run = 0;
-    if (e < El) {
-        for (int64_t c = 0; c < nchunks; ++c) {
-            int32_t v = chunk_cnt[c * El + e];
-            chunk_cnt[c * El + e] = run;
-            run += v;
-        }
-        counts[e] = run;
-    }
-    // exclusive scan of the per-expert totals over e (block-wide)
-    const int lane = e & 63, wv = e >> 6;
+    if (active)
+        for (int64_t c = c0; c < c1; ++c) run += chunk_cnt[c * El + e];
+    // exclusive scan of the runs over the L lanes of the expert's group
     int32_t incl = run;
+    for (int off = 1; off < L; off <<= 1) {
+        const int32_t o = __shfl_up(incl, off, L);
+        if (j >= off) incl += o;
+    }
+    const int32_t seg_before = incl - run;
+    const int32_t expert_total = __shfl(incl, L - 1, L);
+    // exclusive scan of the expert totals over the block: thread e holds
+    // expert e's total
+    if (active && j == L - 1) tot[e] = expert_total;
+    __syncthreads();
+    const int32_t mine = t < El ? tot[t] : 0;
+    __syncthreads();
+    int32_t ein = mine;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
-        int32_t o = __shfl_up(incl, off, 64);
-        if (lane >= off) incl += o;
+        const int32_t o = __shfl_up(ein, off, 64);
+        if (lane >= off) ein += o;
     }
-    if (lane == 63) wsum[wv] = incl;
+    if (lane == 63) wsum[wv] = ein;
     __syncthreads();
     int32_t before = 0;
     for (int i = 0; i < wv; ++i) before += wsum[i];
-    int32_t excl = before + incl - run;
-    tot[e] = excl;
-    if (e < El) offsets[e] = excl;
-    if (e == 1023) offsets[El] = before + incl;  // total over all experts
+    const int32_t eexcl = before + ein - mine;
+    if (t < El) {
+        counts[t] = mine;
+        offsets[t] = eexcl;
+        tot[t] = eexcl;
+    }
+    if (t == 1023) offsets[El] = before + ein;  // total over all experts
     __syncthreads();
-    if (e < El) {
-        for (int64_t c = 0; c < nchunks; ++c) chunk_cnt[c * El + e] += tot[e];
+    if (active) {
+        int32_t row = tot[e] + seg_before;
+        for (int64_t c = c0; c < c1; ++c) {
+            const int32_t v = chunk_cnt[c * El + e];
+            chunk_cnt[c * El + e] = row;
+            row += v;
+        }
     }
 }
 
@@ -170,7 +194,9 @@ hipError_t launch_permute(const int32_t *ids, int64_t T, int k, int e0, int El, 
                 ids, npairs, e0, El, ws);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
-        scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(ws, nchunks, El, counts, offsets);
+        int L = 1;
+        while (L < 64 && 2 * L * El <= 1024) L *= 2;
+        scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(ws, nchunks, El, L, counts, offsets);
         if ((err = hipGetLastError()) != hipSuccess) return err;
         if (nchunks > 0) {
             scatter_kernel<<<dim3((unsigned)nchunks), dim3(64), El * sizeof(int32_t), s>>>(

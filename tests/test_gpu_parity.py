@@ -60,7 +60,8 @@ def test_route_configs(oracle, name, seed):
 
 @pytest.mark.parametrize("T,E,k", [(1, 1, 1), (3, 8, 8), (257, 16, 4), (100, 33, 5), (64, 64, 16),
                                    (1000, 128, 8), (513, 256, 8), (77, 1000, 16), (64, 1024, 16),
-                                   (40000, 8, 2)])
+                                   (40000, 8, 2), (4096, 33, 5), (5000, 64, 16), (4097, 256, 8),
+                                   (4100, 512, 16)])
 def test_route_ties_and_signed_zeros(oracle, T, E, k):
     g = np.random.default_rng(T * 7 + E)
     lg = g.integers(-2, 3, (T, E)).astype(np.float32)
