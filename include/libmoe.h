@@ -134,6 +134,32 @@ moe_status moe_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *row
                            void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * Grouped FFN with a shared expert in the same launches (the shared-expert
+ * models of Sec. 8: a dense expert every token of the rank's data-parallel
+ * share goes through, beside the routed ones).  Computes exactly what
+ * moe_grouped_ffn computes for the routed experts (row_to_pair is required
+ * here) and, in the same kernels, the SwiGLU FFN of the shared expert on
+ * token rows [shared_begin, shared_begin + shared_count) of x:
+ *   shared_y[i] = FFN(x[shared_begin + i]; shared_w13, shared_w2)
+ *   shared_w13 [2*I_s, H] bf16 (gate rows, then up rows), shared_w2 [H, I_s]
+ *   bf16, shared_y [shared_count, H] bf16 out.
+ * The shared expert has the routed experts' intermediate width I_s.  One
+ * launch per GEMM streams the routed and the shared weights together, which
+ * matters in decode, where both are read from HBM once per step.
+ * Limits: with shared_count > 0, H and I_s are multiples of 64 and at least
+ * 128, n_local_experts + 1 <= 1024 and cap_rows + shared_count < 2^31
+ * (MOE_ERR_UNSUPPORTED otherwise); shared_begin + shared_count <= x_rows.
+ * workspace: at least moe_ffn_workspace_size(cap_rows + shared_count,
+ * n_local_experts + (shared_count > 0), H, I_s) bytes, 256-byte aligned.
+ */
+moe_status moe_grouped_ffn_shared(const uint16_t *x, int64_t x_rows, const int32_t *row_to_pair, int k,
+                                  const int32_t *offsets, int n_local_experts, int64_t cap_rows, int H,
+                                  int I_s, const uint16_t *w13, const uint16_t *w2, uint16_t *y,
+                                  int64_t shared_begin, int64_t shared_count, const uint16_t *shared_w13,
+                                  const uint16_t *shared_w2, uint16_t *shared_y, void *workspace,
+                                  size_t workspace_bytes, void *stream);
+
+/*
  * Combine (unpermute and gate-weighted reduce).  For every token t:
  *   out[t] = (accumulate ? out[t] : 0)
  *          + (shared_begin <= t < shared_begin + shared_count ? shared_y[t - shared_begin] : 0)

@@ -3,10 +3,11 @@
 The compute lives in libmoe.so (HIP kernels for gfx950 behind the C ABI in
 include/libmoe.h); this package only binds it.
 """
-from .binding import (MoeError, MoeLayer, combine, ffn_workspace_size, grouped_ffn, lib,  # noqa: F401
+from .binding import (MoeError, MoeLayer, combine, ffn_workspace_size, grouped_ffn,  # noqa: F401
+                     grouped_ffn_shared, lib,
                      permute, permute_workspace_size, route, timing_enable, timing_read,
                      timing_reset)
 
-__all__ = ["MoeError", "MoeLayer", "route", "permute", "grouped_ffn", "combine", "lib",
+__all__ = ["MoeError", "MoeLayer", "route", "permute", "grouped_ffn", "grouped_ffn_shared", "combine", "lib",
            "permute_workspace_size", "ffn_workspace_size", "timing_enable", "timing_read",
            "timing_reset"]

@@ -54,6 +54,8 @@ def lib():
         "moe_permute": ([vp, i64, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, vp, vp, sz, vp], i32),
         "moe_ffn_workspace_size": ([i64, i32, i32, i32], sz),
         "moe_grouped_ffn": ([vp, i64, vp, i32, vp, i32, i64, i32, i32, vp, vp, vp, vp, sz, vp], i32),
+        "moe_grouped_ffn_shared": ([vp, i64, vp, i32, vp, i32, i64, i32, i32, vp, vp, vp, i64, i64, vp, vp, vp,
+                                    vp, sz, vp], i32),
         "moe_combine": ([vp, i64, vp, vp, i64, i32, i32, vp, i64, i64, i32, vp, vp], i32),
         "moe_timing_enable": ([i32], i32),
         "moe_timing_enable_mask": ([ctypes.c_uint32], i32),
@@ -185,6 +187,50 @@ def grouped_ffn(x: torch.Tensor, offsets: torch.Tensor, w13: torch.Tensor, w2: t
     return y
 
 
+def grouped_ffn_shared(x: torch.Tensor, offsets: torch.Tensor, w13: torch.Tensor, w2: torch.Tensor,
+                       row_to_pair: torch.Tensor, k: int, cap_rows: int, shared_begin: int,
+                       shared_count: int, sw13: torch.Tensor, sw2: torch.Tensor,
+                       y: Optional[torch.Tensor] = None, shared_y: Optional[torch.Tensor] = None,
+                       workspace: Optional[torch.Tensor] = None, stream=None):
+    """The routed experts' FFN (rows gathered through `row_to_pair`) and the
+    shared expert's FFN on x[shared_begin : shared_begin + shared_count], in
+    the same launches.  Returns (y, shared_y)."""
+    _need(x, torch.bfloat16, "x", 2)
+    _need(offsets, torch.int32, "offsets", 1)
+    _need(w13, torch.bfloat16, "w13", 3)
+    _need(w2, torch.bfloat16, "w2", 3)
+    _need(row_to_pair, torch.int32, "row_to_pair", 1)
+    _need(sw13, torch.bfloat16, "sw13", 2)
+    _need(sw2, torch.bfloat16, "sw2", 2)
+    x_rows, H = x.shape
+    El = offsets.numel() - 1
+    I_s = w2.shape[2]
+    if tuple(w13.shape) != (El, 2 * I_s, H) or tuple(w2.shape) != (El, H, I_s):
+        raise ValueError(f"weight shapes {tuple(w13.shape)}, {tuple(w2.shape)} do not match "
+                         f"El={El}, H={H}, I_s={I_s}")
+    if tuple(sw13.shape) != (2 * I_s, H) or tuple(sw2.shape) != (H, I_s):
+        raise ValueError("the shared expert must have the routed experts' shapes")
+    if row_to_pair.numel() < cap_rows:
+        raise ValueError("row_to_pair must hold cap_rows entries")
+    if y is None:
+        y = torch.empty((max(cap_rows, 1), H), dtype=torch.bfloat16, device=x.device)
+    if shared_y is None:
+        shared_y = torch.empty((max(shared_count, 1), H), dtype=torch.bfloat16, device=x.device)
+    _need(y, torch.bfloat16, "y", 2)
+    _need(shared_y, torch.bfloat16, "shared_y", 2)
+    if y.shape[0] < cap_rows or y.shape[1] != H or shared_y.shape[0] < shared_count or shared_y.shape[1] != H:
+        raise ValueError("y must be [cap_rows, H] and shared_y [shared_count, H]")
+    ne = El + (1 if shared_count > 0 else 0)
+    if workspace is None:
+        workspace = torch.empty(ffn_workspace_size(cap_rows + shared_count, ne, H, I_s), dtype=torch.uint8,
+                                device=x.device)
+    _check(lib().moe_grouped_ffn_shared(_ptr(x), x_rows, _ptr(row_to_pair), k, _ptr(offsets), El, cap_rows,
+                                        H, I_s, _ptr(w13), _ptr(w2), _ptr(y), shared_begin, shared_count,
+                                        _ptr(sw13), _ptr(sw2), _ptr(shared_y), _ptr(workspace),
+                                        workspace.numel(), _stream(stream)))
+    return y, shared_y
+
+
 def combine(y: torch.Tensor, pair_to_row: torch.Tensor, topk_w: torch.Tensor,
             out: Optional[torch.Tensor] = None, shared_y: Optional[torch.Tensor] = None,
             shared_begin: int = 0, accumulate: bool = False, stream=None) -> torch.Tensor:
@@ -270,25 +316,42 @@ class MoeLayer:
         self.out = torch.empty((T, self.H), dtype=torch.bfloat16, device=dev)
         self.sw13, self.sw2 = sw13, sw2
         self.sb, self.sc = shared_begin, shared_count if sw13 is not None else 0
+        # the shared expert joins the routed experts' launches when it has their
+        # width and the large-tile kernels serve the shapes, else it is a
+        # grouped FFN call of its own
+        self.fused_shared = False
         if self.sc:
             sIs = sw2.shape[2]
-            self.s_offsets = torch.tensor([0, self.sc], dtype=torch.int32, device=dev)
             self.s_y = torch.empty((self.sc, self.H), dtype=torch.bfloat16, device=dev)
-            self.ws_sh = torch.empty(ffn_workspace_size(self.sc, 1, self.H, sIs), dtype=torch.uint8,
-                                     device=dev)
+            self.fused_shared = (sIs == self.I_s and self.H % 64 == 0 and self.I_s % 64 == 0
+                                 and self.H >= 128 and self.I_s >= 128)
+            if self.fused_shared:
+                self.sw13_2d, self.sw2_2d = sw13.reshape(2 * sIs, self.H), sw2.reshape(self.H, sIs)
+                self.ws_ffn = torch.empty(ffn_workspace_size(cap1 + self.sc, self.El + 1, self.H, self.I_s),
+                                          dtype=torch.uint8, device=dev)
+            else:
+                self.s_offsets = torch.tensor([0, self.sc], dtype=torch.int32, device=dev)
+                self.ws_sh = torch.empty(ffn_workspace_size(self.sc, 1, self.H, sIs), dtype=torch.uint8,
+                                         device=dev)
 
     def forward(self, x: torch.Tensor, logits: torch.Tensor, stream=None) -> torch.Tensor:
         route(logits, self.k, self.topk_ids, self.topk_w, stream=stream)
         # the permutation's row gather is fused into the gate-up GEMM
         permute(self.topk_ids, self.E, self.e0, self.El, out=self.bufs, workspace=self.ws_perm,
                 stream=stream)
-        grouped_ffn(x, self.bufs["offsets"], self.w13, self.w2, row_to_pair=self.bufs["row_to_pair"],
-                    k=self.k, cap_rows=self.cap, y=self.y, workspace=self.ws_ffn, stream=stream)
         shared_y = None
-        if self.sc:
-            grouped_ffn(x[self.sb:self.sb + self.sc], self.s_offsets, self.sw13, self.sw2, y=self.s_y,
-                        workspace=self.ws_sh, stream=stream)
+        if self.fused_shared:
+            grouped_ffn_shared(x, self.bufs["offsets"], self.w13, self.w2, self.bufs["row_to_pair"], self.k,
+                               self.cap, self.sb, self.sc, self.sw13_2d, self.sw2_2d, y=self.y,
+                               shared_y=self.s_y, workspace=self.ws_ffn, stream=stream)
             shared_y = self.s_y
+        else:
+            grouped_ffn(x, self.bufs["offsets"], self.w13, self.w2, row_to_pair=self.bufs["row_to_pair"],
+                        k=self.k, cap_rows=self.cap, y=self.y, workspace=self.ws_ffn, stream=stream)
+            if self.sc:
+                grouped_ffn(x[self.sb:self.sb + self.sc], self.s_offsets, self.sw13, self.sw2, y=self.s_y,
+                            workspace=self.ws_sh, stream=stream)
+                shared_y = self.s_y
         combine(self.y, self.bufs["pair_to_row"], self.topk_w, out=self.out, shared_y=shared_y,
                 shared_begin=self.sb, stream=stream)
         return self.out

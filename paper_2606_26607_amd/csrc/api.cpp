@@ -79,7 +79,7 @@ extern "C" const char *moe_status_str(int status)
 
 extern "C" const char *moe_last_error(void) { return g_msg; }
 
-extern "C" int moe_version(void) { return 3; }
+extern "C" int moe_version(void) { return 4; }
 
 extern "C" moe_status moe_route(const float *logits, int64_t T, int E, int k, int32_t *topk_ids,
                                 float *topk_w, void *stream)
@@ -135,39 +135,99 @@ extern "C" size_t moe_ffn_workspace_size(int64_t cap_rows, int n_local_experts, 
     return ffn_workspace_bytes(cap_rows, n_local_experts, H, I_s);
 }
 
+namespace {
+
+// Checks shared by both grouped-FFN entry points (the routed experts' part).
+moe_status check_ffn(const char *fn, const uint16_t *x, int64_t x_rows, const int32_t *row_to_pair, int k,
+                     const int32_t *offsets, int n_local_experts, int64_t cap_rows, int H, int I_s,
+                     const uint16_t *w13, const uint16_t *w2, const uint16_t *y)
+{
+    moe_status st;
+    if (n_local_experts < 1) return fail(MOE_ERR_INVALID_ARG, "%s: n_local_experts=%d", fn, n_local_experts);
+    if (n_local_experts > MOE_MAX_EXPERTS)
+        return fail(MOE_ERR_UNSUPPORTED, "%s: n_local_experts=%d exceeds %d", fn, n_local_experts,
+                    MOE_MAX_EXPERTS);
+    if (cap_rows < 0) return fail(MOE_ERR_INVALID_ARG, "%s: cap_rows=%lld", fn, (long long)cap_rows);
+    if (cap_rows >= ((int64_t)1 << 31)) return fail(MOE_ERR_UNSUPPORTED, "%s: cap_rows too large", fn);
+    if (x_rows < 0) return fail(MOE_ERR_INVALID_ARG, "%s: x_rows=%lld", fn, (long long)x_rows);
+    if ((st = check_width("H", H)) != MOE_OK) return st;
+    if ((st = check_width("I_s", I_s)) != MOE_OK) return st;
+    if (!offsets) return fail(MOE_ERR_INVALID_ARG, "%s: null offsets", fn);
+    if (row_to_pair) {
+        if (k < 1) return fail(MOE_ERR_INVALID_ARG, "%s: k=%d must be >= 1 with row_to_pair", fn, k);
+    } else if (x_rows < cap_rows) {
+        return fail(MOE_ERR_INVALID_ARG, "%s: x_rows=%lld < cap_rows=%lld for a permuted x", fn,
+                    (long long)x_rows, (long long)cap_rows);
+    }
+    if (cap_rows > 0 && (!x || !w13 || !w2 || !y)) return fail(MOE_ERR_INVALID_ARG, "%s: null pointer", fn);
+    if (!aligned16(x) || !aligned16(w13) || !aligned16(w2) || !aligned16(y))
+        return fail(MOE_ERR_INVALID_ARG, "%s: tensors must be 16-byte aligned", fn);
+    return MOE_OK;
+}
+
+moe_status check_workspace(const char *fn, const void *workspace, size_t workspace_bytes, size_t need)
+{
+    if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u))
+        return fail(MOE_ERR_WORKSPACE, "%s: workspace %zu < %zu bytes or misaligned", fn, workspace_bytes, need);
+    return MOE_OK;
+}
+
+}  // namespace
+
 extern "C" moe_status moe_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *row_to_pair,
                                       int k, const int32_t *offsets, int n_local_experts,
                                       int64_t cap_rows, int H, int I_s, const uint16_t *w13,
                                       const uint16_t *w2, uint16_t *y, void *workspace,
                                       size_t workspace_bytes, void *stream)
 {
-    moe_status st;
-    if (n_local_experts < 1) return fail(MOE_ERR_INVALID_ARG, "n_local_experts=%d", n_local_experts);
-    if (n_local_experts > MOE_MAX_EXPERTS)
-        return fail(MOE_ERR_UNSUPPORTED, "n_local_experts=%d exceeds %d", n_local_experts, MOE_MAX_EXPERTS);
-    if (cap_rows < 0) return fail(MOE_ERR_INVALID_ARG, "cap_rows=%lld", (long long)cap_rows);
-    if (cap_rows >= ((int64_t)1 << 31)) return fail(MOE_ERR_UNSUPPORTED, "cap_rows too large");
-    if (x_rows < 0) return fail(MOE_ERR_INVALID_ARG, "x_rows=%lld", (long long)x_rows);
-    if ((st = check_width("H", H)) != MOE_OK) return st;
-    if ((st = check_width("I_s", I_s)) != MOE_OK) return st;
-    if (!offsets) return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn: null offsets");
-    if (row_to_pair) {
-        if (k < 1) return fail(MOE_ERR_INVALID_ARG, "k=%d must be >= 1 with row_to_pair", k);
-    } else if (x_rows < cap_rows) {
-        return fail(MOE_ERR_INVALID_ARG, "x_rows=%lld < cap_rows=%lld for a permuted x",
-                    (long long)x_rows, (long long)cap_rows);
-    }
-    if (cap_rows > 0 && (!x || !w13 || !w2 || !y))
-        return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn: null pointer");
-    if (!aligned16(x) || !aligned16(w13) || !aligned16(w2) || !aligned16(y))
-        return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn: tensors must be 16-byte aligned");
+    static const char fn[] = "moe_grouped_ffn";
+    moe_status st = check_ffn(fn, x, x_rows, row_to_pair, k, offsets, n_local_experts, cap_rows, H, I_s, w13,
+                              w2, y);
+    if (st != MOE_OK) return st;
     const size_t need = moe_ffn_workspace_size(cap_rows, n_local_experts, H, I_s);
-    if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u))
-        return fail(MOE_ERR_WORKSPACE, "moe_grouped_ffn: workspace %zu < %zu bytes or misaligned",
-                    workspace_bytes, need);
-    return hip_status(launch_grouped_ffn(x, x_rows, row_to_pair, k, offsets, n_local_experts, cap_rows,
-                                         H, I_s, w13, w2, y, workspace, (hipStream_t)stream),
+    if ((st = check_workspace(fn, workspace, workspace_bytes, need)) != MOE_OK) return st;
+    return hip_status(launch_grouped_ffn(x, x_rows, row_to_pair, k, offsets, n_local_experts, cap_rows, H, I_s,
+                                         w13, w2, y, 0, 0, nullptr, nullptr, nullptr, workspace,
+                                         (hipStream_t)stream),
                       "moe_grouped_ffn launch");
+}
+
+extern "C" moe_status moe_grouped_ffn_shared(const uint16_t *x, int64_t x_rows, const int32_t *row_to_pair,
+                                             int k, const int32_t *offsets, int n_local_experts,
+                                             int64_t cap_rows, int H, int I_s, const uint16_t *w13,
+                                             const uint16_t *w2, uint16_t *y, int64_t shared_begin,
+                                             int64_t shared_count, const uint16_t *shared_w13,
+                                             const uint16_t *shared_w2, uint16_t *shared_y, void *workspace,
+                                             size_t workspace_bytes, void *stream)
+{
+    static const char fn[] = "moe_grouped_ffn_shared";
+    moe_status st = check_ffn(fn, x, x_rows, row_to_pair, k, offsets, n_local_experts, cap_rows, H, I_s, w13,
+                              w2, y);
+    if (st != MOE_OK) return st;
+    if (!row_to_pair) return fail(MOE_ERR_INVALID_ARG, "%s: row_to_pair is required", fn);
+    if (shared_begin < 0 || shared_count < 0 || shared_begin + shared_count > x_rows)
+        return fail(MOE_ERR_INVALID_ARG, "%s: shared rows [%lld, +%lld) outside the %lld rows of x", fn,
+                    (long long)shared_begin, (long long)shared_count, (long long)x_rows);
+    if (shared_count > 0) {
+        if (!x || !shared_w13 || !shared_w2 || !shared_y) return fail(MOE_ERR_INVALID_ARG, "%s: null pointer", fn);
+        if (!aligned16(x) || !aligned16(shared_w13) || !aligned16(shared_w2) || !aligned16(shared_y))
+            return fail(MOE_ERR_INVALID_ARG, "%s: tensors must be 16-byte aligned", fn);
+        if (n_local_experts + 1 > MOE_MAX_EXPERTS)
+            return fail(MOE_ERR_UNSUPPORTED, "%s: n_local_experts + 1 exceeds %d", fn, MOE_MAX_EXPERTS);
+        if (cap_rows + shared_count >= ((int64_t)1 << 31))
+            return fail(MOE_ERR_UNSUPPORTED, "%s: cap_rows + shared_count too large", fn);
+        if (!ffn_large_tiles(x_rows, cap_rows + shared_count, H, I_s))
+            return fail(MOE_ERR_UNSUPPORTED,
+                        "%s: H=%d and I_s=%d must be multiples of 64, at least 128, with operands under 4 GiB",
+                        fn, H, I_s);
+    }
+    const int ne = n_local_experts + (shared_count > 0 ? 1 : 0);
+    const size_t need = moe_ffn_workspace_size(cap_rows + shared_count, ne, H, I_s);
+    if ((st = check_workspace(fn, workspace, workspace_bytes, need)) != MOE_OK) return st;
+    return hip_status(launch_grouped_ffn(x, x_rows, row_to_pair, k, offsets, n_local_experts, cap_rows, H, I_s,
+                                         w13, w2, y, shared_begin, shared_count, shared_w13, shared_w2, shared_y,
+                                         workspace, (hipStream_t)stream),
+                      "moe_grouped_ffn_shared launch");
 }
 
 extern "C" moe_status moe_combine(const uint16_t *y, int64_t y_rows, const int32_t *pair_to_row,

@@ -26,6 +26,20 @@ __device__ __forceinline__ int64_t clamp_row(int32_t v, int64_t cap)
     return r > cap ? cap : r;
 }
 
+// Row range of expert e in one call's row space: a routed expert e < El holds
+// [offsets[e], offsets[e+1]) clamped to [0, cap]; the shared expert (e == El,
+// present when the call has shared rows) holds [cap, cap + shared_rows).
+__device__ __forceinline__ int64_t expert_begin(const int32_t *__restrict__ offsets, int El, int64_t cap, int e)
+{
+    return e < El ? clamp_row(offsets[e], cap) : cap;
+}
+
+__device__ __forceinline__ int64_t expert_end(const int32_t *__restrict__ offsets, int El, int64_t cap,
+                                              int64_t shared_rows, int e)
+{
+    return e < El ? clamp_row(offsets[e + 1], cap) : cap + shared_rows;
+}
+
 // SwiGLU of one gate/up pair: silu(g) * u = g / (1 + e^-g) * u, with the
 // hardware reciprocal (the result is rounded to bf16).
 __device__ __forceinline__ float silu_mul(float g, float u)
@@ -102,11 +116,13 @@ __device__ __forceinline__ float gemm_cost(int64_t tl, int64_t ts, int nk, int g
 // most 32, 64 or 96 rows) is chosen for the lowest estimated time of both
 // GEMMs (gemm_cost).  small_max = 0 disables the small class.
 //   pre[e] / pre_small[e] = m-tiles of that class of the experts before e,
-//   pre[El] / pre_small[El] = totals.
+//   pre[ne] / pre_small[ne] = totals (ne experts: the routed ones, then the
+//   shared one if the call has shared rows).
 // Also clears the split-K tile counters (no memset node is needed, so the
 // chain stays graph-capturable).
 __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restrict__ offsets, int El,
-                                                        int64_t cap, int bm, int bm_small, int small_max,
+                                                        int64_t cap, int64_t shared_rows, int bm, int bm_small,
+                                                        int small_max,
                                                         SchedShape sh, int32_t *__restrict__ pre,
                                                         int32_t *__restrict__ pre_small,
                                                         int32_t *__restrict__ split,
@@ -119,11 +135,13 @@ __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restric
     __shared__ float cost[NC];
     const int e = threadIdx.x, lane = e & 63, wv = e >> 6;
     for (int64_t i = e; i < n_counters; i += 1024) counters[i] = 0;
-    // rows fit int32: cap < 2^31 is checked on the host
+    // experts: the El routed ones, then the shared one when there are shared
+    // rows; rows fit int32 (cap + shared rows < 2^31 is checked on the host)
+    const int ne = El + (shared_rows > 0 ? 1 : 0);
     int32_t a = 0, n = 0;
-    if (e < El) {
-        a = (int32_t)clamp_row(offsets[e], cap);
-        const int32_t b = (int32_t)clamp_row(offsets[e + 1], cap);
+    if (e < ne) {
+        a = (int32_t)expert_begin(offsets, El, cap, e);
+        const int32_t b = (int32_t)expert_end(offsets, El, cap, shared_rows, e);
         n = b > a ? b - a : 0;
     }
     // m-tiles of both classes (x: large, y: small) for a leftover threshold th
@@ -184,12 +202,12 @@ __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restric
     }
     const int2 r = tiles_for(th);
     const int32_t mt = r.x, mts = r.y;
-    if (split && e < El) split[e] = a + (mts ? mt * bm : n);
-    const int32_t x = block_exscan(mt, wsum, &pre[El]);
-    if (e < El) pre[e] = x;
+    if (split && e < ne) split[e] = a + (mts ? mt * bm : n);
+    const int32_t x = block_exscan(mt, wsum, &pre[ne]);
+    if (e < ne) pre[e] = x;
     if (pre_small) {
-        const int32_t xs = block_exscan(mts, wsum, &pre_small[El]);
-        if (e < El) pre_small[e] = xs;
+        const int32_t xs = block_exscan(mts, wsum, &pre_small[ne]);
+        if (e < ne) pre_small[e] = xs;
     }
 }
 
@@ -453,10 +471,10 @@ __device__ __forceinline__ uint16_t bf16_bits(float f)
 }
 
 // Coordinates of tile `tile` of a tile class: expert e, rows [r0, r1) and
-// output columns [n0, n0 + nvalid).  Tiles are numbered expert by expert,
-// then by n-tile, with m-tiles innermost; the class's rows of expert e are
-// [offsets[e], split[e]) for the large class and [split[e], offsets[e+1])
-// for the tail class.
+// output columns [n0, n0 + nvalid).  Tiles are numbered expert by expert
+// (ne experts), then by n-tile, with m-tiles innermost; the class's rows of
+// expert e are [begin(e), split[e]) for the large class and
+// [split[e], end(e)) for the tail class.
 struct TileCoord {
     int e;
     int64_t r0, r1;
@@ -464,11 +482,12 @@ struct TileCoord {
 };
 
 template <int BMt, int OUTN, bool TAIL>
-__device__ __forceinline__ TileCoord tile_coord(int64_t tile, const int32_t *__restrict__ tile_prefix, int El,
-                                                int n_tiles, const int32_t *__restrict__ offsets,
-                                                const int32_t *__restrict__ split, int64_t cap, int N)
+__device__ __forceinline__ TileCoord tile_coord(int64_t tile, const int32_t *__restrict__ tile_prefix, int ne,
+                                                int n_tiles, const int32_t *__restrict__ offsets, int El,
+                                                int64_t shared_rows, const int32_t *__restrict__ split,
+                                                int64_t cap, int N)
 {
-    int lo = 0, hi = El - 1;
+    int lo = 0, hi = ne - 1;
     while (lo < hi) {
         int mid = (lo + hi + 1) >> 1;
         if ((int64_t)tile_prefix[mid] * n_tiles <= tile) lo = mid; else hi = mid - 1;
@@ -478,8 +497,8 @@ __device__ __forceinline__ TileCoord tile_coord(int64_t tile, const int32_t *__r
     const int64_t local = tile - (int64_t)tile_prefix[lo] * n_tiles;
     const int mte = tile_prefix[lo + 1] - tile_prefix[lo];
     const int nt = (int)(local / mte), mt = (int)(local % mte);
-    const int64_t rb = TAIL ? clamp_row(split[lo], cap) : clamp_row(offsets[lo], cap);
-    const int64_t re = TAIL ? clamp_row(offsets[lo + 1], cap) : clamp_row(split[lo], cap);
+    const int64_t rb = TAIL ? split[lo] : expert_begin(offsets, El, cap, lo);
+    const int64_t re = TAIL ? expert_end(offsets, El, cap, shared_rows, lo) : split[lo];
     c.r0 = rb + (int64_t)mt * BMt;
     c.r1 = re < c.r0 + BMt ? re : c.r0 + BMt;
     c.n0 = nt * OUTN;
@@ -534,15 +553,18 @@ struct GemmArgs {
     const int32_t *row_index;   // row -> pair index (divided by kdiv gives the token), or null
     int kdiv;
     int64_t a_rows;             // rows of A when row_index is given
-    const int32_t *offsets;     // [El+1] expert row ranges
-    const int32_t *split;       // [El] cut of each expert's rows between the tile classes
-    int El;
-    int64_t cap;
+    const int32_t *offsets;     // [El+1] routed experts' row ranges
+    const int32_t *split;       // [ne] cut of each expert's rows between the tile classes
+    int El, ne;                 // routed experts; all experts (+1 with a shared expert)
+    int64_t cap;                // routed rows; the shared expert's rows follow at cap
+    int64_t shared_rows, shared_begin;  // shared expert: rows, first token
     int N, K;                   // output columns (per part when gated), reduction length
     const uint16_t *W;          // [El] weight blocks of w_stride elements, rows K-contiguous
     int64_t w_stride;
+    const uint16_t *Wsh;        // the shared expert's weight block
     int up_off;                 // first up row when gated
-    uint16_t *C;                // [cap, N] bf16 out
+    uint16_t *C;                // [cap, N] bf16 out (routed rows)
+    uint16_t *Csh;              // [shared_rows, N] bf16 out (shared rows)
 };
 
 // Per tile class: its m-tile prefix over experts, split-K tile counters and
@@ -565,9 +587,11 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                                            const int32_t *__restrict__ row_index, int kdiv, int64_t a_rows,
                                            const int32_t *__restrict__ offsets,
                                            const int32_t *__restrict__ split,
-                                           const int32_t *__restrict__ tile_prefix, int El, int64_t cap,
+                                           const int32_t *__restrict__ tile_prefix, int El, int ne,
+                                           int64_t cap, int64_t shared_rows, int64_t shared_begin,
                                            int N, int K, const uint16_t *__restrict__ W, int64_t w_stride,
-                                           int up_off, uint16_t *__restrict__ C,
+                                           const uint16_t *__restrict__ Wsh, int up_off,
+                                           uint16_t *__restrict__ C, uint16_t *__restrict__ Csh,
                                            int32_t *__restrict__ tile_cnt, float *__restrict__ partials,
                                            int grp_base, int grp_size)
 {
@@ -595,7 +619,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
     const int nk = K / BIG_BK;
     // the class runs on workgroups [grp_base, grp_base + grp_size) of the
     // XCD-aware numbering below, renumbered from 0
-    const WorkSplit ws((int64_t)tile_prefix[El] * n_tiles, nk, grp_size, TAIL);
+    const WorkSplit ws((int64_t)tile_prefix[ne] * n_tiles, nk, grp_size, TAIL);
     if (ws.T == 0) return;
     // XCD-aware numbering: the 8 dies take workgroups round robin, so the
     // workgroups of one die get consecutive virtual ids and with them a
@@ -626,8 +650,9 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
         }
     }
 
-    // Write the staged bf16 tile [BM][OUTN] from LDS with 16-byte stores.
-    auto store_staged = [&](int64_t r0, int64_t r1, int n0, int nvalid) {
+    // Write the staged bf16 tile [BM][OUTN] from LDS with 16-byte stores to
+    // rows [r0, r1), whose first row is at Cb.
+    auto store_staged = [&](uint16_t *Cb, int64_t r0, int64_t r1, int n0, int nvalid) {
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         lds_barrier();
         const uint4 *so = ring;
@@ -636,7 +661,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
         for (int c = tid; c < BMt * CH_ROW; c += GEMM_THREADS) {
             const int row = c / CH_ROW, cc = c % CH_ROW;
             if (row < rows && cc * 8 < nvalid)
-                *reinterpret_cast<uint4 *>(C + (r0 + row) * N + n0 + cc * 8) = so[c];
+                *reinterpret_cast<uint4 *>(Cb + row * N + n0 + cc * 8) = so[c];
         }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         lds_barrier();  // staging reads done before the next piece's loads
@@ -644,11 +669,14 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
 
     // One piece of work: K-slices [klo, khi) of tile `tile`.
     auto do_work = [&](int64_t tile, int klo, int khi) {
-        const TileCoord tc = tile_coord<BMt, OUTN, TAIL>(tile, tile_prefix, El, n_tiles, offsets, split, cap, N);
+        const TileCoord tc = tile_coord<BMt, OUTN, TAIL>(tile, tile_prefix, ne, n_tiles, offsets, El, shared_rows,
+                                                         split, cap, N);
         const int e = tc.e;
         const int64_t r0 = tc.r0, r1 = tc.r1;
         const int n0 = tc.n0, nvalid = tc.nvalid;
-        const uint16_t *We = W + (int64_t)e * w_stride;
+        // the shared expert (e == El) has its own weights and output rows
+        const uint16_t *We = e < El ? W + (int64_t)e * w_stride : Wsh;
+        uint16_t *Cb = e < El ? C + r0 * N : Csh + (r0 - cap) * N;
 
         // this wave's B rows lie in one part (gate or up) when gated
         const int bpart = GATED ? ((wave * B_INS * RPI) / (BNt / 2)) : 0;
@@ -668,7 +696,11 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
             const int64_t r = r0 + trow;
             int64_t off;
             if (r >= r1) off = a_bytes;                            // past the expert: zeros
-            else if (row_index) off = ((int64_t)(row_index[r] / kdiv) * K + kc * 8) * 2;
+            else if (row_index) {
+                // the shared expert's rows are tokens shared_begin, ...
+                const int64_t tok = r < cap ? (int64_t)(row_index[r] / kdiv) : shared_begin + (r - cap);
+                off = (tok * K + kc * 8) * 2;
+            }
             else off = ((int64_t)trow * K + kc * 8) * 2;
             src.voa[q] = (uint32_t)off;
         }
@@ -777,6 +809,12 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
             const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(
                 partials, (short)0, (int)((int64_t)2 * ws.G * SLOT * 4), 0x00020000);
             constexpr int SC1 = 0x10;
+            // Small-row tiles move only the 8-row groups of a wave that hold
+            // rows of the tile (decode tiles are mostly padding); the group
+            // test is uniform over the wave, so writer and reader agree.
+            // Large tiles move everything (splitk_reduce reads whole slots).
+            const int nrows = (int)(r1 - r0);
+            auto live = [&](int i, int q) { return !TAIL || wm * (BMt / WM) + i * 32 + 8 * q < nrows; };
             {
                 const uint32_t base_b = (uint32_t)(slot_of(v) * SLOT * 4);
 #pragma unroll
@@ -785,6 +823,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                     for (int j = 0; j < NB; ++j)
 #pragma unroll
                         for (int q = 0; q < 4; ++q) {
+                            if (!live(i, q)) continue;
                             float4 pv = make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
                                                     acc[i][j][4 * q + 3]);
                             __builtin_amdgcn_raw_buffer_store_b128(
@@ -821,8 +860,9 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                     const uint32_t buf = ring_base + (uint32_t)((i & 1) * CH * JQ);
 #pragma unroll
                     for (int jq = 0; jq < CH; ++jq)
-                        dma16_sc1(pdesc, buf + jq * JQ + wave * 1024, (uint32_t)(jq * JQ + tid * 16),
-                                  base_c + (uint32_t)(i * CH * JQ));
+                        if (live(i, jq % 4))
+                            dma16_sc1(pdesc, buf + jq * JQ + wave * 1024, (uint32_t)(jq * JQ + tid * 16),
+                                      base_c + (uint32_t)(i * CH * JQ));
                 };
                 issue(0);
 #pragma unroll
@@ -830,7 +870,9 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                     if (i + 1 < MB) {
                         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // chunk i-1 read out
                         issue(i + 1);
-                        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(CH) : "memory");
+                        // with groups skipped the count of chunk i+1 varies
+                        if (TAIL) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+                        else asm volatile("s_waitcnt vmcnt(%0)" ::"n"(CH) : "memory");
                     } else {
                         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
                     }
@@ -839,6 +881,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                     for (int j = 0; j < NB; ++j)
 #pragma unroll
                         for (int q = 0; q < 4; ++q) {
+                            if (!live(i, q)) continue;  // rows past the tile: never stored
                             const uint4 w = bp[(j * 4 + q) * GEMM_THREADS + tid];
                             const float pv[4] = {__uint_as_float(w.x), __uint_as_float(w.y),
                                                  __uint_as_float(w.z), __uint_as_float(w.w)};
@@ -880,7 +923,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                 }
             }
         }
-        store_staged(r0, r1, n0, nvalid);
+        store_staged(Cb, r0, r1, n0, nvalid);
     };
 
     // This workgroup's work items, in order: whole tiles v, v+G, ... below
@@ -951,14 +994,16 @@ void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
     __shared__ uint4 ring[BIG_RING];
     constexpr int OUTN = GATED ? BIGN / 2 : BIGN;
     const int64_t n_tiles = (g.N + OUTN - 1) / OUTN;
-    const SmallGroup sg = small_group((int64_t)large.tile_prefix[g.El] * n_tiles,
-                                      (int64_t)small.tile_prefix[g.El] * n_tiles, g.K / BIG_BK, gridDim.x);
-    gemm_class<BIGM, BIGN, GATED, BIG_WM, false, A_SLOTS, B_SLOTS>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split,
-                                            large.tile_prefix, g.El, g.cap, g.N, g.K, g.W, g.w_stride,
-                                            g.up_off, g.C, large.tile_cnt, large.partials, 0, gridDim.x);
-    gemm_class<SMALLM, BIGN, GATED, SMALL_WM, true, SA_SLOTS, SB_SLOTS>(ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split,
-                                             small.tile_prefix, g.El, g.cap, g.N, g.K, g.W, g.w_stride,
-                                             g.up_off, g.C, small.tile_cnt, small.partials, sg.base, sg.size);
+    const SmallGroup sg = small_group((int64_t)large.tile_prefix[g.ne] * n_tiles,
+                                      (int64_t)small.tile_prefix[g.ne] * n_tiles, g.K / BIG_BK, gridDim.x);
+    gemm_class<BIGM, BIGN, GATED, BIG_WM, false, A_SLOTS, B_SLOTS>(
+        ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, large.tile_prefix, g.El, g.ne, g.cap,
+        g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh, large.tile_cnt,
+        large.partials, 0, gridDim.x);
+    gemm_class<SMALLM, BIGN, GATED, SMALL_WM, true, SA_SLOTS, SB_SLOTS>(
+        ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, small.tile_prefix, g.El, g.ne, g.cap,
+        g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh, small.tile_cnt,
+        small.partials, sg.base, sg.size);
 }
 
 // Combines the split-K partials of the large-tile class after its GEMM
@@ -970,10 +1015,10 @@ void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
 template <bool GATED>
 __global__ __launch_bounds__(GEMM_THREADS) void splitk_reduce(const int32_t *__restrict__ offsets,
                                                      const int32_t *__restrict__ split,
-                                                     const int32_t *__restrict__ tile_prefix, int El,
-                                                     int64_t cap, int N, int K, int G,
+                                                     const int32_t *__restrict__ tile_prefix, int El, int ne,
+                                                     int64_t cap, int64_t shared_rows, int N, int K, int G,
                                                      const float *__restrict__ partials,
-                                                     uint16_t *__restrict__ C)
+                                                     uint16_t *__restrict__ C, uint16_t *__restrict__ Csh)
 {
     constexpr int WM = BIG_WM, WN = GEMM_WAVES / BIG_WM;
     constexpr int MB = BIGM / WM / 32, NB = BIGN / WN / 32;
@@ -981,14 +1026,16 @@ __global__ __launch_bounds__(GEMM_THREADS) void splitk_reduce(const int32_t *__r
     constexpr int JJ = GATED ? NB / 2 : NB;  // output blocks per wave row
     const int n_tiles = (N + OUTN - 1) / OUTN;
     const int nk = K / BIG_BK;
-    const WorkSplit ws((int64_t)tile_prefix[El] * n_tiles, nk, G, false);
+    const WorkSplit ws((int64_t)tile_prefix[ne] * n_tiles, nk, G, false);
     const int64_t items = (ws.T - ws.dp) * MB * JJ;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
     for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
         const int64_t tile = ws.dp + it / (MB * JJ);
         const int i = (int)((it / JJ) % MB), j = (int)(it % JJ);
-        const TileCoord tc = tile_coord<BIGM, OUTN, false>(tile, tile_prefix, El, n_tiles, offsets, split, cap, N);
+        const TileCoord tc = tile_coord<BIGM, OUTN, false>(tile, tile_prefix, ne, n_tiles, offsets, El, shared_rows,
+                                                           split, cap, N);
+        uint16_t *Cb = tc.e < El ? C + tc.r0 * N : Csh + (tc.r0 - cap) * N;
         const int64_t tb = (tile - ws.dp) * nk;
         const int vfirst = ws.owner(tb), vlast = ws.owner(tb + nk - 1);
         float g[16], u[16];
@@ -1011,11 +1058,11 @@ __global__ __launch_bounds__(GEMM_THREADS) void splitk_reduce(const int32_t *__r
         if (col >= tc.nvalid) continue;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const int64_t row = tc.r0 + wm * (BIGM / WM) + i * 32 + 8 * (r / 4) + 4 * (lane >> 5) + (r % 4);
-            if (row >= tc.r1) continue;
+            const int64_t row = wm * (BIGM / WM) + i * 32 + 8 * (r / 4) + 4 * (lane >> 5) + (r % 4);
+            if (tc.r0 + row >= tc.r1) continue;
             float o = g[r];
             if (GATED) o = silu_mul(o, u[r]);
-            C[row * N + tc.n0 + col] = bf16_bits(o);
+            Cb[row * N + tc.n0 + col] = bf16_bits(o);
         }
     }
 }
@@ -1075,13 +1122,27 @@ size_t ffn_workspace_bytes(int64_t cap, int El, int H, int Is)
     return FfnLayout(cap, El, H, Is).total;
 }
 
+bool ffn_large_tiles(int64_t x_rows, int64_t rows, int H, int Is)
+{
+    // K a multiple of 64 with at least two slices, and every operand
+    // addressable with 32-bit buffer offsets
+    if (H % BIG_BK || Is % BIG_BK || H < 2 * BIG_BK || Is < 2 * BIG_BK) return false;
+    const int64_t lim = ((int64_t)1 << 32) - 4 * (int64_t)(H > Is ? H : Is);
+    return x_rows * (int64_t)H * 2 < lim && rows * (int64_t)H * 2 < lim && rows * (int64_t)Is * 2 < lim;
+}
+
 hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *row_index, int kdiv,
                               const int32_t *offsets, int El, int64_t cap, int H, int Is,
-                              const uint16_t *w13, const uint16_t *w2, uint16_t *y, void *ws,
-                              hipStream_t s)
+                              const uint16_t *w13, const uint16_t *w2, uint16_t *y, int64_t shared_begin,
+                              int64_t shared_rows, const uint16_t *sw13, const uint16_t *sw2,
+                              uint16_t *shared_y, void *ws, hipStream_t s)
 {
-    if (cap == 0) return hipSuccess;
-    const FfnLayout L(cap, El, H, Is);
+    // row space: the routed rows [0, cap), then the shared expert's rows
+    const int64_t sc = shared_rows;
+    const int ne = El + (sc > 0 ? 1 : 0);
+    const int64_t rows = cap + sc;
+    if (rows == 0) return hipSuccess;
+    const FfnLayout L(rows, ne, H, Is);
     char *base = static_cast<char *>(ws);
     int32_t *pre = reinterpret_cast<int32_t *>(base);
     int32_t *pre_s = reinterpret_cast<int32_t *>(base + L.off_pre_s);
@@ -1090,15 +1151,14 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
     float *part_s = reinterpret_cast<float *>(base + L.off_part_s);
     float *part = reinterpret_cast<float *>(base + L.off_part);
     uint16_t *h = reinterpret_cast<uint16_t *>(base + L.off_h);
-    // the large-tile kernels address operands with 32-bit buffer offsets
-    const int64_t lim = ((int64_t)1 << 32) - 4 * (int64_t)(H > Is ? H : Is);
-    const bool big = L.big && (row_index ? x_rows : cap) * (int64_t)H * 2 < lim &&
-                     cap * (int64_t)Is * 2 < lim;
+    uint16_t *h_sh = h + cap * Is;  // the shared expert's h rows
+    const bool big = ffn_large_tiles(row_index ? x_rows : rows, rows, H, Is);
+    if (sc > 0 && !big) return hipErrorNotSupported;  // the host API checks this first
     hipError_t err;
     {
         KernelTimer timer(MOE_K_SCHEDULE, s);
         schedule_kernel<<<dim3(1), dim3(1024), 0, s>>>(
-            offsets, El, cap, big ? BIGM : BM, SMALLM, big ? SMALL_MAX : 0,
+            offsets, El, cap, sc, big ? BIGM : BM, SMALLM, big ? SMALL_MAX : 0,
             SchedShape{(int)ceil_div(Is, BIGN / 2), H / BIG_BK, (int)ceil_div(H, BIGN), Is / BIG_BK, L.grid}, pre,
             big ? pre_s : nullptr, big ? split : nullptr, cnt,
             big ? L.t_gu + L.t_dn + L.ts_gu + L.ts_dn : 0);
@@ -1108,28 +1168,30 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
         int32_t *c_gu = cnt, *c_dn = cnt + L.t_gu, *cs_gu = c_dn + L.t_dn, *cs_dn = cs_gu + L.ts_gu;
         {
             KernelTimer timer(MOE_K_GATE_UP, s);
-            const GemmArgs g{x, row_index, kdiv, x_rows, offsets, split, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h};
+            const GemmArgs g{x,   row_index, kdiv, x_rows, offsets, split, El, ne, cap, sc, shared_begin,
+                             Is,  H,         w13,  (int64_t)2 * Is * H, sw13, Is, h, h_sh};
             gemm_grouped<true><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
                 g, TileClass{pre_s, cs_gu, part_s}, TileClass{pre, c_gu, part});
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         if (H / BIG_BK >= SPLIT_MIN_NK) {  // the large tiles may have been split over K
             KernelTimer timer(MOE_K_SPLITK_REDUCE, s);
-            splitk_reduce<true><<<dim3(REDUCE_GRID), dim3(GEMM_THREADS), 0, s>>>(offsets, split, pre, El, cap, Is, H, L.grid,
-                                                                     part, h);
+            splitk_reduce<true><<<dim3(REDUCE_GRID), dim3(GEMM_THREADS), 0, s>>>(
+                offsets, split, pre, El, ne, cap, sc, Is, H, L.grid, part, h, h_sh);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         {
             KernelTimer timer(MOE_K_DOWN, s);
-            const GemmArgs g{h, nullptr, 1, cap, offsets, split, El, cap, H, Is, w2, (int64_t)H * Is, 0, y};
+            const GemmArgs g{h, nullptr, 1, rows, offsets, split, El, ne, cap, sc, shared_begin,
+                             H, Is,      w2, (int64_t)H * Is, sw2, 0, y, shared_y};
             gemm_grouped<false><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
                 g, TileClass{pre_s, cs_dn, part_s}, TileClass{pre, c_dn, part});
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         if (Is / BIG_BK >= SPLIT_MIN_NK) {
             KernelTimer timer(MOE_K_SPLITK_REDUCE, s);
-            splitk_reduce<false><<<dim3(REDUCE_GRID), dim3(GEMM_THREADS), 0, s>>>(offsets, split, pre, El, cap, H, Is, L.grid,
-                                                                      part, y);
+            splitk_reduce<false><<<dim3(REDUCE_GRID), dim3(GEMM_THREADS), 0, s>>>(
+                offsets, split, pre, El, ne, cap, sc, H, Is, L.grid, part, y, shared_y);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         return hipSuccess;

@@ -59,10 +59,16 @@ hipError_t launch_permute(const int32_t *ids, int64_t T, int k, int e0, int El, 
                           hipStream_t s);
 
 size_t ffn_workspace_bytes(int64_t cap, int El, int H, int Is);
+// Whether the 64-wide-K large-tile kernels serve these sizes (x_rows: rows of
+// the activation operand; rows: all rows of the call).  A call with a shared
+// expert needs them.
+bool ffn_large_tiles(int64_t x_rows, int64_t rows, int H, int Is);
+// shared_rows = 0: no shared expert (sw13, sw2, shared_y unused).
 hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *row_index, int kdiv,
                               const int32_t *offsets, int El, int64_t cap, int H, int Is,
-                              const uint16_t *w13, const uint16_t *w2, uint16_t *y, void *ws,
-                              hipStream_t s);
+                              const uint16_t *w13, const uint16_t *w2, uint16_t *y, int64_t shared_begin,
+                              int64_t shared_rows, const uint16_t *sw13, const uint16_t *sw2,
+                              uint16_t *shared_y, void *ws, hipStream_t s);
 
 hipError_t launch_combine(const uint16_t *y, int64_t y_rows, const int32_t *pair_to_row,
                           const float *w, int64_t T, int k, int H, const uint16_t *shared_y,

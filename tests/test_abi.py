@@ -102,6 +102,30 @@ def test_ffn_rejects():
     assert call(r2p=FAKE, k=0) == INVALID                    # gather without a slot count
 
 
+def test_ffn_shared_rejects():
+    L = moe.lib()
+    big = 1 << 30
+
+    def call(xr=64, r2p=FAKE, El=8, cap=64, H=256, Is=128, sb=0, sc=16, sw13=FAKE, sw2=FAKE, sy=FAKE, wsb=big):
+        return L.moe_grouped_ffn_shared(FAKE, xr, r2p, 2, FAKE, El, cap, H, Is, FAKE, FAKE, FAKE, sb, sc, sw13,
+                                        sw2, sy, FAKE, wsb, None)
+    assert call(r2p=None) == INVALID                          # the shared variant gathers rows
+    assert call(sb=60, sc=16) == INVALID                      # shared rows beyond x
+    assert call(sb=-1) == INVALID
+    assert call(sc=-1) == INVALID
+    assert call(sw2=None) == INVALID
+    assert call(sy=ctypes.c_void_p(0x100004)) == INVALID      # not 16-byte aligned
+    assert call(H=200) == UNSUPPORTED                         # shared path needs 64-multiples
+    assert call(Is=64) == UNSUPPORTED                         # ... and K of at least 128
+    assert call(El=1024) == UNSUPPORTED                       # one more expert than allowed
+    assert call(El=0) == INVALID
+    assert call(wsb=100) == WORKSPACE
+    # the workspace must hold the shared rows and the extra expert
+    need = L.moe_ffn_workspace_size(64 + 16, 9, 256, 128)
+    assert need > L.moe_ffn_workspace_size(64, 8, 256, 128)
+    assert call(wsb=need - 1) == WORKSPACE
+
+
 def test_combine_rejects():
     L = moe.lib()
 

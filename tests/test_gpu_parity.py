@@ -206,6 +206,40 @@ def test_grouped_ffn_fused_gather(oracle, El, E, H, Is, T, k, e0):
     assert_close_rel(got, ref, what=f"fused El={El} H={H} Is={Is}")
 
 
+@pytest.mark.parametrize("El,E,H,Is,T,k,e0,sb,sc", [(4, 8, 256, 192, 150, 2, 2, 10, 40),
+                                                    (3, 3, 512, 256, 300, 1, 0, 0, 300),
+                                                    (1, 2, 512, 8192, 300, 1, 0, 50, 250),
+                                                    (8, 8, 256, 128, 200, 2, 0, 0, 0),
+                                                    (2, 16, 7168 // 4, 512, 64, 8, 6, 56, 8)])
+def test_grouped_ffn_shared(oracle, El, E, H, Is, T, k, e0, sb, sc):
+    """Routed experts and a shared expert in the same launches: the routed
+    rows equal moe_grouped_ffn's result (oracle on the gathered rows), the
+    shared rows the shared expert's FFN on x[sb:sb+sc].  Covers a shared
+    expert in the small-row class, in the large class, in a long-K split
+    (the separate reduction writes its rows) and none at all."""
+    ids = mi.random_topk_ids(T, E, k, seed=T + H + sc)
+    _, offs, r2p, _ = oracle.permute(ids, e0, El)
+    n = int(offs[-1])
+    x = mi.random_bf16((T, H), seed=T, tag=47)
+    w13 = mi.random_bf16((El, 2 * Is, H), seed=T, tag=48, std=0.05)
+    w2 = mi.random_bf16((El, H, Is), seed=T, tag=49, std=0.05)
+    sw13 = mi.random_bf16((2 * Is, H), seed=T, tag=50, std=0.05)
+    sw2 = mi.random_bf16((H, Is), seed=T, tag=51, std=0.05)
+    cap = T * min(k, El)
+    r2p_dev = torch.full((cap,), -1, dtype=torch.int32)
+    r2p_dev[:n] = torch.from_numpy(r2p)
+    y, sy = moe.grouped_ffn_shared(dev_bf16(x), torch.from_numpy(offs).cuda(), dev_bf16(w13), dev_bf16(w2),
+                                   r2p_dev.cuda(), k, cap, sb, sc, dev_bf16(sw13), dev_bf16(sw2))
+    torch.cuda.synchronize()
+    got = bf16_f64(host_bf16(y)[:n])
+    ref = oracle.grouped_ffn(x[r2p // k], offs, w13, w2)
+    assert_close_rel(got, ref, what=f"routed El={El} H={H} Is={Is}")
+    if sc:
+        got_s = bf16_f64(host_bf16(sy)[:sc])
+        ref_s = oracle.grouped_ffn(x[sb:sb + sc], np.array([0, sc], np.int32), sw13[None], sw2[None])
+        assert_close_rel(got_s, ref_s, what=f"shared sb={sb} sc={sc}")
+
+
 def test_grouped_ffn_skewed_and_empty_experts(oracle):
     got, ref = ffn_case(oracle, 8, 256, 128, 700, 2, seed=3, hot=5)
     assert_close_rel(got, ref, what="skewed")
