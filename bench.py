@@ -128,6 +128,10 @@ def main():
                          "a replay of the K steps from one captured HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cold-steps", type=int, default=10,
+                    help="steps timed one by one after writing a 512 MiB buffer (caches flushed); 0 skips")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the vendor-GEMM and device-copy reference measurements")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -211,6 +215,22 @@ def main():
         torch.cuda.synchronize()
         ms_per_step = (time.perf_counter() - t_start) * 1e3 / args.steps
 
+    # Cold steps: a 512 MiB buffer is written before each step (outside the
+    # timed span), so the step finds no weights in L2 or the 256 MB MALL.
+    cold_ms = None
+    if args.cold_steps > 0:
+        scratch = torch.empty(256 << 20, dtype=torch.int16, device=dev)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.cold_steps)]
+        for i, (a, b) in enumerate(ev):
+            scratch.fill_(i)
+            a.record()
+            step()
+            b.record()
+        torch.cuda.synchronize()
+        cold_ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+        del scratch
+
     kern = {}
     for kind in moe.binding.KERNEL_KINDS:
         ms, n = moe.timing_read(kind)
@@ -241,6 +261,41 @@ def main():
     else:
         roof = None
 
+    # Measured ceilings on this GPU (references, not part of the path): the
+    # vendor GEMM (torch.matmul, hipBLASLt) on the dense shape of the
+    # gate-up GEMM, and a device-to-device copy.
+    ceilings = None
+    if not args.no_ceilings:
+        def timed(fn, reps=20):
+            fn()
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(reps):
+                fn()
+            b.record()
+            torch.cuda.synchronize()
+            return a.elapsed_time(b) / reps * 1e-3
+        ceilings = {}
+        m = max(work["n"], 1)
+        if not decode:
+            A = torch.randn(m, cfg.H, device=dev).to(torch.bfloat16)
+            B = torch.randn(cfg.H, 2 * cfg.I_s, device=dev).to(torch.bfloat16).contiguous()
+            t = timed(lambda: torch.matmul(A, B))
+            ceilings["vendor_gemm_tflops"] = 2.0 * m * cfg.H * 2 * cfg.I_s / t / 1e12
+            ceilings["vendor_gemm_shape"] = [m, 2 * cfg.I_s, cfg.H]
+            del A, B
+        src = torch.empty(256 << 20, dtype=torch.int16, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        t = timed(lambda: dst.copy_(src), reps=10)
+        ceilings["copy_gbs"] = 2.0 * src.numel() * 2 / t / 1e9
+        del src, dst
+        if roof is not None:
+            if roof["bound"] == "mfma" and "vendor_gemm_tflops" in ceilings:
+                roof["frac_of_vendor_gemm"] = roof["achieved"] / ceilings["vendor_gemm_tflops"]
+            if roof["bound"] == "hbm":
+                roof["frac_of_copy"] = roof["achieved"] / ceilings["copy_gbs"]
+
     step_s = ms_per_step * 1e-3
     result = {
         "metric": METRIC,
@@ -261,12 +316,15 @@ def main():
                    "shared_expert": cfg.shared, "global_batch": cfg.T, "parallelism": "single-gpu-slice",
                    "graph": not args.eager, "seed": cfg.seed},
         "slice_tokens_per_s": cfg.T / step_s,
+        "pairs_per_s": work["n"] / step_s,
         "chain_tflops": work["flops"] / step_s / 1e12,
         "chain_frac_mfma": work["flops"] / step_s / 1e12 / PEAK_BF16_TFLOPS,
         "chain_gbs": work["bytes"] / step_s / 1e9,
         "chain_frac_hbm": work["bytes"] / step_s / 1e9 / PEAK_HBM_GBS,
         "kernels_us": {k: round(v["avg_us"], 2) for k, v in kern.items()},
         "eager_ms_per_step": eager_ms,
+        "cold_ms_per_step": cold_ms,
+        "ceilings": ceilings,
         "roofline": roof,
         "cpu_baseline": None,
     }
