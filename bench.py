@@ -116,6 +116,75 @@ def cpu_baseline(inp, target_s: float):
                        f"routing+permutation of all tokens scaled by {S}/{cfg.T}; fp64; {dt:.1f} s", seconds=dt, slice_tokens_per_s=S / dt)
 
 
+# xGMI of one MI355X: 7 links of about 153 GB/s each way to the 7 peers of
+# an 8-GPU node.  Start-up cost of one collective: a stated model parameter.
+XGMI_GBS = 7 * 153.0
+ALLREDUCE_US = 10.0
+ALLTOALL_US = 15.0
+
+
+def crossover(args, torch, mi, moe):
+    """TP slice vs EP slice of the same layer (P = 8) over batch sizes B:
+    the measured MoE compute of one rank (the whole four-call chain,
+    replayed from a HIP graph) plus the exchange each layout needs, modelled
+    from xGMI bandwidth: TP all-reduces out [B, H] (2 (P-1)/P B H 2 bytes
+    per GPU); EP dispatches each rank's B/P tokens' k rows to the expert
+    owners and combines them back ((P-1)/P (B/P) k H 2 bytes each way).
+    Under EP each rank routes only its own B/P tokens; here the slice routes
+    all B (a few microseconds more), and its local pairs are the B k / P
+    that land on its 16 experts."""
+    dev = torch.device("cuda:0")
+    batches = [8, 16, 32, 64, 128, 256, 512, 1024, 2048]
+
+    def up(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    for layout in ("tp", "ep"):
+        base = mi.qwen3_layer(batches[0], layout)
+        t0 = time.time()
+        inp = mi.make_inputs(base)
+        w13, w2 = up(inp.w13), up(inp.w2)
+        log(f"[crossover] {layout} weights in {time.time() - t0:.1f}s")
+        for B in batches:
+            cfg = mi.qwen3_layer(B, layout)
+            x = mi.make_x(cfg)
+            lg = mi.make_logits(cfg, x)
+            xd, lgd = up(x), torch.from_numpy(lg).to(dev)
+            layer = moe.MoeLayer(cfg.T, cfg.E, cfg.k, cfg.e0, w13, w2)
+            for _ in range(3):
+                layer.forward(xd, lgd)
+            torch.cuda.synchronize()
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                layer.forward(xd, lgd)
+            torch.cuda.current_stream().wait_stream(side)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                for _ in range(args.steps):
+                    layer.forward(xd, lgd)
+            graph.replay()
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            graph.replay()
+            b.record()
+            torch.cuda.synchronize()
+            us = a.elapsed_time(b) * 1e3 / args.steps
+            counts = layer.bufs["counts"].cpu().numpy()
+            P, H, k = cfg.P, cfg.H, cfg.k
+            if layout == "tp":
+                comm = ALLREDUCE_US + 2 * (P - 1) / P * B * H * 2 / (XGMI_GBS * 1e3)
+            else:
+                comm = 2 * (ALLTOALL_US + (P - 1) / P * (B / P) * k * H * 2 / (XGMI_GBS * 1e3))
+            print(json.dumps({"crossover": layout, "workload": cfg.name, "B": B, "moe_us": us,
+                              "comm_model_us": comm, "total_us": us + comm,
+                              "local_pairs": int(counts.sum()), "active_experts": int((counts > 0).sum()),
+                              "weight_gb_read": float((counts > 0).sum() * 3 * H * cfg.I_s * 2 / 1e9)}),
+                  flush=True)
+            del graph, layer
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -132,6 +201,9 @@ def main():
                     help="steps timed one by one after writing a 512 MiB buffer (caches flushed); 0 skips")
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the vendor-GEMM and device-copy reference measurements")
+    ap.add_argument("--crossover", action="store_true",
+                    help="instead of one workload: time the TP and the EP slice of a Qwen3-235B-shaped "
+                         "layer over a range of batch sizes (one JSON line per batch size)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -146,6 +218,9 @@ def main():
     import paper_2606_26607_amd as moe
 
     assert torch.cuda.is_available(), "bench needs a GPU"
+    if args.crossover:
+        crossover(args, torch, mi, moe)
+        return
     cfg = mi.CONFIGS[args.config]
     cfg = cfg.with_(seed=cfg.seed + args.seed)
     t0 = time.time()

@@ -171,6 +171,15 @@ def _cols(tag: int, seed: int, e: int, c0: int, c1: int, H: int, std: float, ch:
 
 
 # ---------------------------------------------------------------- inputs
+def qwen3_layer(B: int, layout: str, rank: int = 0) -> MoeConfig:
+    """One rank's slice (TP or EP, P = 8) of a Qwen3-235B-shaped MoE layer
+    (H 4096, 128 experts, top-8, expert intermediate 1536; dimensions from
+    the public model configuration) for a step of B tokens.  The weights do
+    not depend on B."""
+    return MoeConfig(f"qwen3-235b-{layout}8-b{B}", T=B, H=4096, E=128, k=8, I=1536, P=8,
+                     layout=layout, rank=rank, seed=1100)
+
+
 @dataclasses.dataclass
 class MoeInputs:
     cfg: MoeConfig

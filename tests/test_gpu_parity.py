@@ -327,6 +327,22 @@ def test_layer_configs(oracle, name):
     assert np.all(out[~local] == 0)
 
 
+@pytest.mark.parametrize("layout,B", [("tp", 16), ("ep", 16), ("tp", 256), ("ep", 256)])
+def test_layer_qwen3_slices(oracle, layout, B):
+    """The TP and EP slices of the Qwen3-235B-shaped layer that the layout
+    crossover sweep times (128 experts, top-8, I_s = 192 under TP)."""
+    cfg = mi.qwen3_layer(B, layout)
+    inp = mi.make_inputs(cfg)
+    layer, out = layer_on_gpu(inp)
+    rid, rw = oracle.route(inp.logits, cfg.k)
+    np.testing.assert_array_equal(layer.topk_ids.cpu().numpy(), rid)
+    c, o, r2p, p2r = oracle.permute(rid, cfg.e0, cfg.E_l)
+    np.testing.assert_array_equal(layer.bufs["offsets"].cpu().numpy(), o)
+    toks = np.arange(cfg.T) if B <= 16 else sample_tokens(cfg, rid)
+    ref = oracle.layer_tokens(inp.x, rid, rw, cfg.e0, cfg.E_l, inp.w13, inp.w2, toks, None, None, 0, 0)
+    assert_close_rel(bf16_f64(out[toks]), ref, what=cfg.name)
+
+
 @pytest.mark.parametrize("layout,P", [("tp", 4), ("ep", 4)])
 def test_layer_slices_sum_to_unsliced(oracle, layout, P):
     base = mi.MoeConfig("small", T=130, H=256, E=8, k=2, I=512, seed=77)
