@@ -185,6 +185,58 @@ def crossover(args, torch, mi, moe):
             del graph, layer
 
 
+def reshard_bench(args, torch, mi, moe):
+    """Expert-weight reshard of one Qwen3-235B-shaped layer (128 experts,
+    H 4096, I 1536, P 8) for rank 0, both directions: the part a switch keeps
+    on the GPU (its own 1/P) and the whole destination view (all P sources in
+    this GPU's memory, standing in for peers' buffers).  Each element is read
+    once and written once: bytes = 2 x copied bytes, against the HBM peak and
+    a measured device copy."""
+    dev = torch.device("cuda:0")
+    base = mi.qwen3_layer(8, "ep")
+    E, H, I, P = base.E, base.H, base.I, base.P
+    El, Is = E // P, I // P
+    g = torch.Generator(device=dev).manual_seed(7)
+    rnd = lambda *shape: torch.randint(-32768, 32767, shape, generator=g, dtype=torch.int16,  # noqa: E731
+                                       device=dev).view(torch.bfloat16)
+    ep13 = [rnd(El, 2 * I, H) for _ in range(P)]
+    ep2 = [rnd(El, H, I) for _ in range(P)]
+    tp13 = [rnd(E, 2 * Is, H) for _ in range(P)]
+    tp2 = [rnd(E, H, Is) for _ in range(P)]
+    slot_bytes = (ep13[0].numel() + ep2[0].numel()) * 2
+
+    def timed(fn, reps=10):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps * 1e-3
+
+    src = torch.empty(slot_bytes // 2, dtype=torch.int16, device=dev)
+    dst = torch.empty_like(src)
+    copy_gbs = 2 * slot_bytes / timed(lambda: dst.copy_(src)) / 1e9
+    del src, dst
+    r = 0
+    for direction, name in ((moe.EP_TO_TP, "ep_to_tp"), (moe.TP_TO_EP, "tp_to_ep")):
+        s13, s2 = (ep13, ep2) if direction == moe.EP_TO_TP else (tp13, tp2)
+        d13, d2 = (torch.empty_like(tp13[0]), torch.empty_like(tp2[0])) if direction == moe.EP_TO_TP else \
+            (torch.empty_like(ep13[0]), torch.empty_like(ep2[0]))
+        for part in ("own", "all"):
+            a13 = [t if (part == "all" or q == r) else None for q, t in enumerate(s13)]
+            a2 = [t if (part == "all" or q == r) else None for q, t in enumerate(s2)]
+            t = timed(lambda: moe.reshard_experts(direction, r, E, H, I, a13, a2, d13, d2))
+            moved = slot_bytes if part == "all" else slot_bytes // P
+            gbs = 2 * moved / t / 1e9
+            print(json.dumps({"reshard": name, "part": part, "workload": "qwen3-235b-shaped-layer",
+                              "E": E, "H": H, "I": I, "P": P, "rank": r, "bytes_copied": moved,
+                              "us": t * 1e6, "hbm_gbs": gbs, "frac_hbm_peak": gbs / PEAK_HBM_GBS,
+                              "frac_of_copy": gbs / copy_gbs, "copy_gbs": copy_gbs}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -204,6 +256,9 @@ def main():
     ap.add_argument("--crossover", action="store_true",
                     help="instead of one workload: time the TP and the EP slice of a Qwen3-235B-shaped "
                          "layer over a range of batch sizes (one JSON line per batch size)")
+    ap.add_argument("--reshard", action="store_true",
+                    help="instead of one workload: time the expert-weight reshard (EP <-> TP) of a "
+                         "Qwen3-235B-shaped layer (one JSON line per case)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -220,6 +275,9 @@ def main():
     assert torch.cuda.is_available(), "bench needs a GPU"
     if args.crossover:
         crossover(args, torch, mi, moe)
+        return
+    if args.reshard:
+        reshard_bench(args, torch, mi, moe)
         return
     cfg = mi.CONFIGS[args.config]
     cfg = cfg.with_(seed=cfg.seed + args.seed)

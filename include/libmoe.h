@@ -58,6 +58,7 @@ typedef enum moe_status {
 
 #define MOE_MAX_TOPK 16
 #define MOE_MAX_EXPERTS 1024
+#define MOE_MAX_RESHARD_RANKS 16
 
 /* Static name of a status code ("MOE_OK", ...). */
 const char *moe_status_str(int status);
@@ -179,6 +180,33 @@ moe_status moe_combine(const uint16_t *y, int64_t y_rows, const int32_t *pair_to
                        uint16_t *out, void *stream);
 
 /*
+ * Expert-weight resharding between the EP and TP views (Sec. 3.1; the
+ * layout switch of Sec. 4.2-4.3), for one destination rank.  With E experts,
+ * P ranks, hidden size H and expert intermediate size I:
+ *   EP view of rank q: w13 [E/P, 2I, H] (gate rows [0, I), up rows [I, 2I) of
+ *     experts q*E/P ..), w2 [E/P, H, I];
+ *   TP view of rank r: w13 [E, 2I/P, H] (for every expert, gate rows
+ *     [r*I/P, (r+1)*I/P) then the matching up rows), w2 [E, H, I/P].
+ * MOE_EP_TO_TP writes rank `rank`'s TP view from EP views; MOE_TP_TO_EP
+ * writes its EP view from TP views.  src_w13 / src_w2 are HOST arrays of P
+ * device pointers, the views of ranks 0..P-1 (read during the call only);
+ * an entry pair left NULL is skipped, and the part of the destination it
+ * would supply is left untouched.  Passing only src[rank] copies the 1/P
+ * that stays on the GPU in a switch; passing all P (e.g. peers' buffers
+ * mapped into this process) writes the whole destination.  Every element is
+ * copied once, bit-exact.  The destination must not overlap a given source
+ * (the caller's slot scheme guarantees that: one spare slot per rank, EP
+ * layer i in slot i+1, TP layer i in slot i, EP->TP walking layers upward
+ * and TP->EP downward).
+ * Limits: 1 <= P <= MOE_MAX_RESHARD_RANKS, E and I multiples of P, H and
+ * I/P multiples of 8, 16-byte aligned tensors.
+ */
+typedef enum moe_reshard_dir { MOE_EP_TO_TP = 0, MOE_TP_TO_EP = 1 } moe_reshard_dir;
+moe_status moe_reshard_experts(int direction, int P, int rank, int E, int H, int I,
+                               const uint16_t *const *src_w13, const uint16_t *const *src_w2,
+                               uint16_t *dst_w13, uint16_t *dst_w2, void *stream);
+
+/*
  * Per-kernel timing for measurement.  While enabled, every kernel the
  * library launches is bracketed by HIP events on its own stream (this adds
  * event records to the stream; it never synchronises).  moe_timing_read
@@ -197,7 +225,8 @@ typedef enum moe_kernel_kind {
     MOE_K_DOWN = 5,      /* down GEMM (both tile classes, split-K reduction included) */
     MOE_K_COMBINE = 6,
     MOE_K_SPLITK_REDUCE = 7, /* combination of split-K partials of the large tiles (long K only) */
-    MOE_K_COUNT = 8
+    MOE_K_RESHARD = 8,       /* expert-weight resharding */
+    MOE_K_COUNT = 9
 } moe_kernel_kind;
 
 moe_status moe_timing_enable(int enable);

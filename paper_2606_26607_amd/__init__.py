@@ -4,10 +4,10 @@ The compute lives in libmoe.so (HIP kernels for gfx950 behind the C ABI in
 include/libmoe.h); this package only binds it.
 """
 from .binding import (MoeError, MoeLayer, combine, ffn_workspace_size, grouped_ffn,  # noqa: F401
-                     grouped_ffn_shared, lib,
+                     grouped_ffn_shared, lib, ExpertSlots, reshard_experts, EP_TO_TP, TP_TO_EP,
                      permute, permute_workspace_size, route, timing_enable, timing_read,
                      timing_reset)
 
-__all__ = ["MoeError", "MoeLayer", "route", "permute", "grouped_ffn", "grouped_ffn_shared", "combine", "lib",
+__all__ = ["MoeError", "MoeLayer", "ExpertSlots", "reshard_experts", "EP_TO_TP", "TP_TO_EP", "route", "permute", "grouped_ffn", "grouped_ffn_shared", "combine", "lib",
            "permute_workspace_size", "ffn_workspace_size", "timing_enable", "timing_read",
            "timing_reset"]

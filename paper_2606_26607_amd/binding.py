@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(_HERE, "libmoe.so")
 MAX_TOPK = 16
 MAX_EXPERTS = 1024
 KERNEL_KINDS = {"route": 0, "permute": 1, "gather": 2, "schedule": 3, "gate_up": 4, "down": 5,
-                "combine": 6, "splitk_reduce": 7}
+                "combine": 6, "splitk_reduce": 7, "reshard": 8}
+EP_TO_TP, TP_TO_EP = 0, 1
 
 
 class MoeError(RuntimeError):
@@ -57,6 +58,7 @@ def lib():
         "moe_grouped_ffn_shared": ([vp, i64, vp, i32, vp, i32, i64, i32, i32, vp, vp, vp, i64, i64, vp, vp, vp,
                                     vp, sz, vp], i32),
         "moe_combine": ([vp, i64, vp, vp, i64, i32, i32, vp, i64, i64, i32, vp, vp], i32),
+        "moe_reshard_experts": ([i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp], i32),
         "moe_timing_enable": ([i32], i32),
         "moe_timing_enable_mask": ([ctypes.c_uint32], i32),
         "moe_timing_reset": ([], i32),
@@ -252,6 +254,77 @@ def combine(y: torch.Tensor, pair_to_row: torch.Tensor, topk_w: torch.Tensor,
                              _ptr(shared_y), shared_begin, sc, 1 if accumulate else 0, _ptr(out),
                              _stream(stream)))
     return out
+
+
+# ------------------------------------------------------------ resharding
+def reshard_experts(direction: int, rank: int, E: int, H: int, I: int, src_w13: list, src_w2: list,
+                    dst_w13: torch.Tensor, dst_w2: torch.Tensor, stream=None) -> None:
+    """Write rank `rank`'s TP view (direction EP_TO_TP) or EP view
+    (TP_TO_EP) of the expert weights from the other layout's views of ranks
+    0..P-1 (P = len(src_w13)); a None source is skipped and the part of the
+    destination it would supply is left as it was."""
+    P = len(src_w13)
+    if len(src_w2) != P:
+        raise ValueError("src_w13 and src_w2 must list the same ranks")
+    for t in list(src_w13) + list(src_w2):
+        if t is not None:
+            _need(t, torch.bfloat16, "source view", t.dim())
+    _need(dst_w13, torch.bfloat16, "dst_w13", 3)
+    _need(dst_w2, torch.bfloat16, "dst_w2", 3)
+    arr = ctypes.c_void_p * max(P, 1)
+    a13 = arr(*[_ptr(t) for t in src_w13])
+    a2 = arr(*[_ptr(t) for t in src_w2])
+    _check(lib().moe_reshard_experts(direction, P, rank, E, H, I, a13, a2, _ptr(dst_w13), _ptr(dst_w2),
+                                     _stream(stream)))
+
+
+class ExpertSlots:
+    """One rank's expert weights for n_layers MoE layers in n_layers + 1
+    fixed slots of one buffer, viewed either way: layer i's TP view lives in
+    slot i and its EP view in slot i + 1, so a switch moves every layer into
+    a slot other than the one it reads (EP->TP walks layers upward, TP->EP
+    downward) and no buffer is allocated while switching.  Both views of a
+    slot hold w13 then w2 (the same element counts)."""
+
+    def __init__(self, n_layers: int, E: int, H: int, I: int, P: int, rank: int, device):
+        self.n_layers, self.E, self.H, self.I, self.P, self.rank = n_layers, E, H, I, P, rank
+        self.El, self.Is = E // P, I // P
+        self.n13 = self.El * 2 * I * H
+        self.slot = self.n13 + self.El * H * I
+        self.buf = torch.empty((n_layers + 1) * self.slot, dtype=torch.bfloat16, device=device)
+
+    def _views(self, s: int, layout: str):
+        base = self.buf[s * self.slot:(s + 1) * self.slot]
+        w13, w2 = base[:self.n13], base[self.n13:]
+        if layout == "ep":
+            return w13.view(self.El, 2 * self.I, self.H), w2.view(self.El, self.H, self.I)
+        return w13.view(self.E, 2 * self.Is, self.H), w2.view(self.E, self.H, self.Is)
+
+    def ep(self, layer: int):
+        """(w13 [E/P, 2I, H], w2 [E/P, H, I]) of `layer` in the EP layout."""
+        return self._views(layer + 1, "ep")
+
+    def tp(self, layer: int):
+        """(w13 [E, 2I/P, H], w2 [E, H, I/P]) of `layer` in the TP layout."""
+        return self._views(layer, "tp")
+
+    @staticmethod
+    def switch(ranks: list, direction: int, stream=None) -> None:
+        """Reshard every layer of every rank in `ranks` (all P ranks' slots,
+        reachable from this process) into the other layout, in place."""
+        first = ranks[0]
+        layers = range(first.n_layers) if direction == EP_TO_TP else range(first.n_layers - 1, -1, -1)
+        for i in layers:
+            if direction == EP_TO_TP:
+                srcs = [r.ep(i) for r in ranks]
+                for r in ranks:
+                    reshard_experts(direction, r.rank, r.E, r.H, r.I, [s[0] for s in srcs],
+                                    [s[1] for s in srcs], *r.tp(i), stream=stream)
+            else:
+                srcs = [r.tp(i) for r in ranks]
+                for r in ranks:
+                    reshard_experts(direction, r.rank, r.E, r.H, r.I, [s[0] for s in srcs],
+                                    [s[1] for s in srcs], *r.ep(i), stream=stream)
 
 
 # ---------------------------------------------------------------- timing

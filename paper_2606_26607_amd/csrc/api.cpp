@@ -79,7 +79,7 @@ extern "C" const char *moe_status_str(int status)
 
 extern "C" const char *moe_last_error(void) { return g_msg; }
 
-extern "C" int moe_version(void) { return 4; }
+extern "C" int moe_version(void) { return 5; }
 
 extern "C" moe_status moe_route(const float *logits, int64_t T, int E, int k, int32_t *topk_ids,
                                 float *topk_w, void *stream)
@@ -228,6 +228,36 @@ extern "C" moe_status moe_grouped_ffn_shared(const uint16_t *x, int64_t x_rows, 
                                          w13, w2, y, shared_begin, shared_count, shared_w13, shared_w2, shared_y,
                                          workspace, (hipStream_t)stream),
                       "moe_grouped_ffn_shared launch");
+}
+
+extern "C" moe_status moe_reshard_experts(int direction, int P, int rank, int E, int H, int I,
+                                          const uint16_t *const *src_w13, const uint16_t *const *src_w2,
+                                          uint16_t *dst_w13, uint16_t *dst_w2, void *stream)
+{
+    static const char fn[] = "moe_reshard_experts";
+    moe_status st;
+    if (direction != MOE_EP_TO_TP && direction != MOE_TP_TO_EP)
+        return fail(MOE_ERR_INVALID_ARG, "%s: direction=%d", fn, direction);
+    if (P < 1) return fail(MOE_ERR_INVALID_ARG, "%s: P=%d", fn, P);
+    if (P > MOE_MAX_RESHARD_RANKS) return fail(MOE_ERR_UNSUPPORTED, "%s: P=%d exceeds %d", fn, P, MOE_MAX_RESHARD_RANKS);
+    if (rank < 0 || rank >= P) return fail(MOE_ERR_INVALID_ARG, "%s: rank=%d not in [0, %d)", fn, rank, P);
+    if (E < P || E % P) return fail(MOE_ERR_INVALID_ARG, "%s: E=%d is not a positive multiple of P=%d", fn, E, P);
+    if (I < P || I % P) return fail(MOE_ERR_INVALID_ARG, "%s: I=%d is not a positive multiple of P=%d", fn, I, P);
+    if ((st = check_width("H", H)) != MOE_OK) return st;
+    if ((I / P) % 8) return fail(MOE_ERR_UNSUPPORTED, "%s: I/P=%d is not a multiple of 8", fn, I / P);
+    if (!src_w13 || !src_w2) return fail(MOE_ERR_INVALID_ARG, "%s: null source arrays", fn);
+    if (!dst_w13 || !dst_w2) return fail(MOE_ERR_INVALID_ARG, "%s: null destination", fn);
+    if (!aligned16(dst_w13) || !aligned16(dst_w2))
+        return fail(MOE_ERR_INVALID_ARG, "%s: destination not 16-byte aligned", fn);
+    for (int q = 0; q < P; ++q) {
+        if (!src_w13[q] != !src_w2[q])
+            return fail(MOE_ERR_INVALID_ARG, "%s: source %d has only one of w13, w2", fn, q);
+        if (!aligned16(src_w13[q]) || !aligned16(src_w2[q]))
+            return fail(MOE_ERR_INVALID_ARG, "%s: source %d not 16-byte aligned", fn, q);
+    }
+    return hip_status(launch_reshard(direction, P, rank, E, H, I, src_w13, src_w2, dst_w13, dst_w2,
+                                     (hipStream_t)stream),
+                      "moe_reshard_experts launch");
 }
 
 extern "C" moe_status moe_combine(const uint16_t *y, int64_t y_rows, const int32_t *pair_to_row,

@@ -70,6 +70,11 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
                               int64_t shared_rows, const uint16_t *sw13, const uint16_t *sw2,
                               uint16_t *shared_y, void *ws, hipStream_t s);
 
+// dir: MOE_EP_TO_TP or MOE_TP_TO_EP; src arrays are host arrays of P device
+// pointers (NULL pairs skipped).
+hipError_t launch_reshard(int dir, int P, int r, int E, int H, int I, const uint16_t *const *src_w13,
+                          const uint16_t *const *src_w2, uint16_t *dst_w13, uint16_t *dst_w2, hipStream_t s);
+
 hipError_t launch_combine(const uint16_t *y, int64_t y_rows, const int32_t *pair_to_row,
                           const float *w, int64_t T, int k, int H, const uint16_t *shared_y,
                           int64_t sb, int64_t sc, int accumulate, uint16_t *out, hipStream_t s);

@@ -126,6 +126,28 @@ def test_ffn_shared_rejects():
     assert call(wsb=need - 1) == WORKSPACE
 
 
+def test_reshard_rejects():
+    L = moe.lib()
+    arr = ctypes.c_void_p * 4
+    srcs = arr(FAKE, FAKE, FAKE, FAKE)
+
+    def call(d=0, P=4, r=0, E=16, H=64, I=256, s13=srcs, s2=srcs, d13=FAKE, d2=FAKE):
+        return L.moe_reshard_experts(d, P, r, E, H, I, s13, s2, d13, d2, None)
+    assert call(d=2) == INVALID
+    assert call(P=0) == INVALID
+    assert call(P=17) == UNSUPPORTED
+    assert call(r=4) == INVALID
+    assert call(E=10) == INVALID                       # not a multiple of P
+    assert call(I=102) == INVALID                      # not a multiple of P
+    assert call(I=100) == UNSUPPORTED                  # I/P = 25, not a multiple of 8
+    assert call(H=12) == UNSUPPORTED
+    assert call(s13=None) == INVALID
+    assert call(d2=None) == INVALID
+    assert call(d13=ctypes.c_void_p(0x100002)) == INVALID
+    half = arr(FAKE, None, FAKE, FAKE)
+    assert call(s2=half) == INVALID                    # a source with only one of its two tensors
+
+
 def test_combine_rejects():
     L = moe.lib()
 
