@@ -237,6 +237,96 @@ def reshard_bench(args, torch, mi, moe):
                               "frac_of_copy": gbs / copy_gbs, "copy_gbs": copy_gbs}), flush=True)
 
 
+def kvmove_bench(args, torch, moe):
+    """KV-cache moves of one layer for an EP->TP switch of a decode batch:
+    256 requests of 500..3500 tokens (seeded) over 8 EP ranks, 4 KV heads of
+    128 (two TP ranks per head), 16-token pages in shuffled order.  Rank 0's
+    TP pool receives head r*4/8 of every request: `own` moves the part that
+    comes from its own EP pool, `all` the whole pool from the 8 EP pools
+    (held in this GPU's memory, standing in for peers') in one launch.  The
+    page tables serve every layer, so their expansion into slot vectors
+    (two kv_slots calls) is timed once per switch and the per-layer figure
+    is one kv_move launch for K and V; bytes moved = 2 x the copied bytes."""
+    dev = torch.device("cuda:0")
+    P, Hkv, D, ps = 8, 4, 128, 16
+    rng = np.random.default_rng(2606)
+    lengths = rng.integers(500, 3501, 256)
+    owner = rng.integers(0, P, 256)
+    n_tok = int(lengths.sum())
+    width = int(max(-(-int(n) // ps) for n in lengths))
+
+    def tables(ls, n_pages):
+        perm = rng.permutation(n_pages).astype(np.int32)
+        tab = np.zeros((max(len(ls), 1), width), np.int32)
+        k = 0
+        for q, n in enumerate(ls):
+            m = -(-int(n) // ps)
+            tab[q, :m] = perm[k:k + m]
+            k += m
+        return tab
+
+    pages_ep = [int(sum(-(-int(n) // ps) for n in lengths[owner == q])) + 8 for q in range(P)]
+    ep_k = [torch.empty((pg * ps, Hkv, D), dtype=torch.bfloat16, device=dev) for pg in pages_ep]
+    ep_v = [torch.empty_like(t) for t in ep_k]
+    # the EP owners' page tables stacked in owner order (row i indexes its owner's pool)
+    ep_tab = np.concatenate([tables(lengths[owner == q], pages_ep[q])[:int((owner == q).sum())]
+                             for q in range(P)])
+    pages_tp = int(sum(-(-int(n) // ps) for n in lengths)) + 8
+    tp_k = torch.empty((pages_tp * ps, 1, D), dtype=torch.bfloat16, device=dev)
+    tp_v = torch.empty_like(tp_k)
+    order = np.concatenate([np.nonzero(owner == q)[0] for q in range(P)])
+    tp_tab = tables(lengths[order], pages_tp)         # rank 0's TP table, rows in owner order
+    counts = [int(lengths[owner == q].sum()) for q in range(P)]
+    n_req0 = int((owner == 0).sum())
+    cases = {"own": (1, counts[0], ep_tab[:n_req0], tp_tab[:n_req0], lengths[order][:n_req0]),
+             "all": (P, n_tok, ep_tab, tp_tab, lengths[order])}
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 20
+    csrc = torch.empty(n_tok * D * 2, dtype=torch.int16, device=dev)     # the "all" part's K and V bytes
+    cdst = torch.empty_like(csrc)
+    cdst.copy_(csrc)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(reps):
+        cdst.copy_(csrc)
+    b.record()
+    torch.cuda.synchronize()
+    copy_gbs = 2 * csrc.numel() * 2 / (a.elapsed_time(b) / reps * 1e-3) / 1e9
+    del csrc, cdst
+    for part, (n_src, toks, tab_s, tab_d, ls) in cases.items():
+        first = torch.from_numpy(np.concatenate([[0], np.cumsum(ls)]).astype(np.int32)).to(dev)
+        tab_s, tab_d = torch.from_numpy(tab_s).to(dev), torch.from_numpy(tab_d).to(dev)
+        slots_s = torch.empty(toks, dtype=torch.int32, device=dev)
+        slots_d = torch.empty(toks, dtype=torch.int32, device=dev)
+
+        def expand():
+            moe.kv_slots(tab_s, first, ps, out=slots_s)
+            moe.kv_slots(tab_d, first, ps, out=slots_d)
+
+        def move():
+            moe.kv_move(ep_k[:n_src], ep_v[:n_src], tp_k, tp_v, slots_s, slots_d, 0, 0, 1,
+                        src_tokens=counts[:n_src])
+
+        times = {}
+        for name, fn in (("slots", expand), ("move", move)):
+            fn()
+            torch.cuda.synchronize()
+            a.record()
+            for _ in range(reps):
+                fn()
+            b.record()
+            torch.cuda.synchronize()
+            times[name] = a.elapsed_time(b) / reps * 1e-3
+        copied = toks * D * 2 * 2
+        gbs = 2 * copied / times["move"] / 1e9
+        print(json.dumps({"kvmove": "ep_to_tp", "part": part, "sources": n_src, "requests": len(ls),
+                          "tokens": toks, "kv_heads": Hkv, "head_dim": D, "page_size": ps, "P": P,
+                          "bytes_copied": copied, "us_per_layer": times["move"] * 1e6,
+                          "slots_us_per_switch": times["slots"] * 1e6, "hbm_gbs": gbs,
+                          "frac_hbm_peak": gbs / PEAK_HBM_GBS, "copy_gbs": copy_gbs,
+                          "frac_of_copy": gbs / copy_gbs}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -259,6 +349,9 @@ def main():
     ap.add_argument("--reshard", action="store_true",
                     help="instead of one workload: time the expert-weight reshard (EP <-> TP) of a "
                          "Qwen3-235B-shaped layer (one JSON line per case)")
+    ap.add_argument("--kvmove", action="store_true",
+                    help="instead of one workload: time the paged KV head moves of an EP->TP switch "
+                         "for a decode batch (one JSON line per case)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -278,6 +371,9 @@ def main():
         return
     if args.reshard:
         reshard_bench(args, torch, mi, moe)
+        return
+    if args.kvmove:
+        kvmove_bench(args, torch, moe)
         return
     cfg = mi.CONFIGS[args.config]
     cfg = cfg.with_(seed=cfg.seed + args.seed)

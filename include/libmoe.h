@@ -59,6 +59,7 @@ typedef enum moe_status {
 #define MOE_MAX_TOPK 16
 #define MOE_MAX_EXPERTS 1024
 #define MOE_MAX_RESHARD_RANKS 16
+#define MOE_MAX_KV_SOURCES 16
 
 /* Static name of a status code ("MOE_OK", ...). */
 const char *moe_status_str(int status);
@@ -207,6 +208,53 @@ moe_status moe_reshard_experts(int direction, int P, int rank, int E, int H, int
                                uint16_t *dst_w13, uint16_t *dst_w2, void *stream);
 
 /*
+ * Paged KV-cache head moves for a layout switch (Sec. 3.2), driven by
+ * page-indexed work descriptors (Sec. 4.3).  Under EP a rank
+ * holds every KV head of its own requests; under TP it holds its head shard
+ * of every request (a head shared by several ranks when there are fewer KV
+ * heads than ranks).  A pool of one layer is [slots, heads, head_dim] bf16
+ * (a paged pool [pages, page_size, heads, head_dim] is the same memory, slot
+ * = page * page_size + offset); its tokens are found through page tables.
+ *
+ * moe_kv_slots: one slot per token of n_req requests, in request order:
+ *   slots[first[q] + t] = page_table[q * pt_stride + t / page_size] *
+ *   page_size + t % page_size  for t < first[q+1] - first[q];
+ *   first [n_req + 1] int32 (device): exclusive prefix of the request
+ *   lengths; page_table [n_req, pt_stride] int32 (device); slots [capacity]
+ *   int32 out.  Tokens at or past `capacity` are not written; a token whose
+ *   page index reaches pt_stride gets slot -1.
+ *
+ * moe_kv_move: copies, for every token i, heads [src_head0, src_head0 +
+ *   n_heads) of slot src_slot[i] of its source pool into heads [dst_head0,
+ *   dst_head0 + n_heads) of slot dst_slot[i] of the destination pool, for K
+ *   and, when src_v / dst_v are given (both or neither), for V.  Tokens
+ *   [src_first[q], src_first[q+1]) come from source pool q (q < n_src <=
+ *   MOE_MAX_KV_SOURCES), e.g. the pools of the EP ranks whose requests move,
+ *   so one launch moves a layer; src_k / src_v / src_slots are HOST arrays
+ *   of n_src entries (device pools and their slot counts), src_first a HOST
+ *   array of n_src + 1 token offsets (non-decreasing, from 0).  All source
+ *   pools have src_heads heads.  src_slot / dst_slot: device int32 slot
+ *   vectors of at least src_first[n_src] entries (e.g. from moe_kv_slots).
+ *   Entries with a slot outside [0, slots) of their pool are skipped.
+ *   Bit-exact copies; destinations of different tokens must not overlap.
+ *   A source that supplies no tokens may be NULL; with no tokens at all
+ *   nothing is launched.
+ * Both calls only read and write the caller's buffers (no allocation) and
+ * are asynchronous on `stream`.  Errors: MOE_ERR_INVALID_ARG for null or
+ * misaligned pointers, negative sizes, decreasing offsets or head ranges
+ * outside the pools; MOE_ERR_UNSUPPORTED for head_dim not a multiple of 8 or
+ * n_src above MOE_MAX_KV_SOURCES.
+ * Limits: head_dim a positive multiple of 8; 16-byte aligned pools.
+ */
+moe_status moe_kv_slots(const int32_t *page_table, int64_t pt_stride, const int32_t *first, int n_req,
+                        int page_size, int32_t *slots, int64_t capacity, void *stream);
+moe_status moe_kv_move(int n_src, const uint16_t *const *src_k, const uint16_t *const *src_v,
+                       const int64_t *src_slots, const int64_t *src_first, int src_heads, uint16_t *dst_k,
+                       uint16_t *dst_v, int64_t dst_slots, int dst_heads, int head_dim, int src_head0,
+                       int dst_head0, int n_heads, const int32_t *src_slot, const int32_t *dst_slot,
+                       void *stream);
+
+/*
  * Per-kernel timing for measurement.  While enabled, every kernel the
  * library launches is bracketed by HIP events on its own stream (this adds
  * event records to the stream; it never synchronises).  moe_timing_read
@@ -226,7 +274,8 @@ typedef enum moe_kernel_kind {
     MOE_K_COMBINE = 6,
     MOE_K_SPLITK_REDUCE = 7, /* combination of split-K partials of the large tiles (long K only) */
     MOE_K_RESHARD = 8,       /* expert-weight resharding */
-    MOE_K_COUNT = 9
+    MOE_K_KV_MOVE = 9,       /* paged KV head moves (and their slot expansion) */
+    MOE_K_COUNT = 10
 } moe_kernel_kind;
 
 moe_status moe_timing_enable(int enable);

@@ -5,9 +5,10 @@ include/libmoe.h); this package only binds it.
 """
 from .binding import (MoeError, MoeLayer, combine, ffn_workspace_size, grouped_ffn,  # noqa: F401
                      grouped_ffn_shared, lib, ExpertSlots, reshard_experts, EP_TO_TP, TP_TO_EP,
+                     kv_slots, kv_move,
                      permute, permute_workspace_size, route, timing_enable, timing_read,
                      timing_reset)
 
-__all__ = ["MoeError", "MoeLayer", "ExpertSlots", "reshard_experts", "EP_TO_TP", "TP_TO_EP", "route", "permute", "grouped_ffn", "grouped_ffn_shared", "combine", "lib",
+__all__ = ["MoeError", "MoeLayer", "kv_slots", "kv_move", "ExpertSlots", "reshard_experts", "EP_TO_TP", "TP_TO_EP", "route", "permute", "grouped_ffn", "grouped_ffn_shared", "combine", "lib",
            "permute_workspace_size", "ffn_workspace_size", "timing_enable", "timing_read",
            "timing_reset"]

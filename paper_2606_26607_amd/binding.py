@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libmoe.so")
 MAX_TOPK = 16
 MAX_EXPERTS = 1024
 KERNEL_KINDS = {"route": 0, "permute": 1, "gather": 2, "schedule": 3, "gate_up": 4, "down": 5,
-                "combine": 6, "splitk_reduce": 7, "reshard": 8}
+                "combine": 6, "splitk_reduce": 7, "reshard": 8, "kv_move": 9}
 EP_TO_TP, TP_TO_EP = 0, 1
 
 
@@ -59,6 +59,8 @@ def lib():
                                     vp, sz, vp], i32),
         "moe_combine": ([vp, i64, vp, vp, i64, i32, i32, vp, i64, i64, i32, vp, vp], i32),
         "moe_reshard_experts": ([i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp], i32),
+        "moe_kv_slots": ([vp, i64, vp, i32, i32, vp, i64, vp], i32),
+        "moe_kv_move": ([i32, vp, vp, vp, vp, i32, vp, vp, i64, i32, i32, i32, i32, i32, vp, vp, vp], i32),
         "moe_timing_enable": ([i32], i32),
         "moe_timing_enable_mask": ([ctypes.c_uint32], i32),
         "moe_timing_reset": ([], i32),
@@ -325,6 +327,87 @@ class ExpertSlots:
                 for r in ranks:
                     reshard_experts(direction, r.rank, r.E, r.H, r.I, [s[0] for s in srcs],
                                     [s[1] for s in srcs], *r.ep(i), stream=stream)
+
+
+# ------------------------------------------------------------- KV moves
+def kv_slots(page_table: torch.Tensor, first: torch.Tensor, page_size: int,
+             out: Optional[torch.Tensor] = None, capacity: Optional[int] = None, stream=None) -> torch.Tensor:
+    """Slot of every token of the requests (request order) from their page
+    tables: page_table [n_req, pages_per_req] int32, first [n_req + 1] int32
+    (exclusive prefix of the lengths); out [capacity] int32."""
+    _need(page_table, torch.int32, "page_table", 2)
+    _need(first, torch.int32, "first", 1)
+    n_req = first.numel() - 1
+    if page_table.shape[0] < n_req:
+        raise ValueError("page_table has fewer rows than requests")
+    if out is None:
+        if capacity is None:
+            raise ValueError("give out or capacity")
+        out = torch.empty(max(capacity, 1), dtype=torch.int32, device=page_table.device)
+    _need(out, torch.int32, "out", 1)
+    cap = out.numel() if capacity is None else capacity
+    _check(lib().moe_kv_slots(_ptr(page_table), page_table.stride(0), _ptr(first), n_req, page_size, _ptr(out),
+                              cap, _stream(stream)))
+    return out
+
+
+def kv_move(src_k, src_v, dst_k: torch.Tensor, dst_v: Optional[torch.Tensor],
+            src_slot: torch.Tensor, dst_slot: torch.Tensor, src_head0: int, dst_head0: int, n_heads: int,
+            src_tokens=None, stream=None) -> None:
+    """Copy heads [src_head0, +n_heads) of the listed source slots into heads
+    [dst_head0, +n_heads) of the listed destination slots (pools [slots,
+    heads, head_dim] bf16), for K and optionally V, in one launch.
+
+    src_k / src_v: one pool or a list of pools (at most 16); with a list,
+    src_tokens gives how many consecutive entries of the slot vectors each
+    pool supplies.  With one pool src_tokens is that count (default: all
+    entries)."""
+    many = isinstance(src_k, (list, tuple))
+    ks = list(src_k) if many else [src_k]
+    vs = None if src_v is None else (list(src_v) if many else [src_v])
+    if vs is not None and len(vs) != len(ks):
+        raise ValueError("src_k and src_v must list the same pools")
+    _need(src_slot, torch.int32, "src_slot", 1)
+    _need(dst_slot, torch.int32, "dst_slot", 1)
+    avail = min(src_slot.numel(), dst_slot.numel())
+    if src_tokens is None:
+        if many and len(ks) > 1:
+            raise ValueError("give src_tokens for several source pools")
+        counts = [avail]
+    else:
+        counts = list(src_tokens) if many else [src_tokens]
+    if len(counts) != len(ks):
+        raise ValueError("src_tokens needs one count per source pool")
+    first = [0]
+    for c in counts:
+        if c < 0:
+            raise ValueError("negative token count")
+        first.append(first[-1] + int(c))
+    if first[-1] > avail:
+        raise ValueError("token counts exceed the slot vectors")
+    _need(dst_k, torch.bfloat16, "dst_k", 3)
+    if dst_v is not None:
+        _need(dst_v, torch.bfloat16, "dst_v", 3)
+        if dst_v.shape != dst_k.shape:
+            raise ValueError("K and V pools must have the same shape")
+    for q, k in enumerate(ks):
+        _need(k, torch.bfloat16, "src_k", 3)
+        if k.shape[1:] != ks[0].shape[1:]:
+            raise ValueError("source pools must share heads and head_dim")
+        if vs is not None:
+            _need(vs[q], torch.bfloat16, "src_v", 3)
+            if vs[q].shape != k.shape:
+                raise ValueError("K and V pools must have the same shape")
+    if ks[0].shape[2] != dst_k.shape[2]:
+        raise ValueError("source and destination head_dim differ")
+    n = len(ks)
+    ak = (ctypes.c_void_p * n)(*[_ptr(t) for t in ks])
+    av = None if vs is None else (ctypes.c_void_p * n)(*[_ptr(t) for t in vs])
+    sl = (ctypes.c_int64 * n)(*[t.shape[0] for t in ks])
+    fi = (ctypes.c_int64 * (n + 1))(*first)
+    _check(lib().moe_kv_move(n, ak, av, sl, fi, ks[0].shape[1], _ptr(dst_k), _ptr(dst_v), dst_k.shape[0],
+                             dst_k.shape[1], ks[0].shape[2], src_head0, dst_head0, n_heads, _ptr(src_slot),
+                             _ptr(dst_slot), _stream(stream)))
 
 
 # ---------------------------------------------------------------- timing

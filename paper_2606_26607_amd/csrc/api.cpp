@@ -79,7 +79,7 @@ extern "C" const char *moe_status_str(int status)
 
 extern "C" const char *moe_last_error(void) { return g_msg; }
 
-extern "C" int moe_version(void) { return 5; }
+extern "C" int moe_version(void) { return 6; }
 
 extern "C" moe_status moe_route(const float *logits, int64_t T, int E, int k, int32_t *topk_ids,
                                 float *topk_w, void *stream)
@@ -258,6 +258,60 @@ extern "C" moe_status moe_reshard_experts(int direction, int P, int rank, int E,
     return hip_status(launch_reshard(direction, P, rank, E, H, I, src_w13, src_w2, dst_w13, dst_w2,
                                      (hipStream_t)stream),
                       "moe_reshard_experts launch");
+}
+
+extern "C" moe_status moe_kv_slots(const int32_t *page_table, int64_t pt_stride, const int32_t *first, int n_req,
+                                   int page_size, int32_t *slots, int64_t capacity, void *stream)
+{
+    static const char fn[] = "moe_kv_slots";
+    if (n_req < 0 || capacity < 0 || pt_stride < 0)
+        return fail(MOE_ERR_INVALID_ARG, "%s: negative n_req, capacity or pt_stride", fn);
+    if (page_size < 1) return fail(MOE_ERR_INVALID_ARG, "%s: page_size=%d", fn, page_size);
+    if (n_req == 0 || capacity == 0) return MOE_OK;
+    if (!page_table || !first || !slots) return fail(MOE_ERR_INVALID_ARG, "%s: null pointer", fn);
+    return hip_status(launch_kv_slots(page_table, pt_stride, first, n_req, page_size, capacity, slots,
+                                      (hipStream_t)stream),
+                      "moe_kv_slots launch");
+}
+
+extern "C" moe_status moe_kv_move(int n_src, const uint16_t *const *src_k, const uint16_t *const *src_v,
+                                  const int64_t *src_slots, const int64_t *src_first, int src_heads, uint16_t *dst_k,
+                                  uint16_t *dst_v, int64_t dst_slots, int dst_heads, int head_dim, int src_head0,
+                                  int dst_head0, int n_heads, const int32_t *src_slot, const int32_t *dst_slot,
+                                  void *stream)
+{
+    static const char fn[] = "moe_kv_move";
+    moe_status st;
+    if (n_src < 1) return fail(MOE_ERR_INVALID_ARG, "%s: n_src=%d", fn, n_src);
+    if (n_src > MOE_MAX_KV_SOURCES)
+        return fail(MOE_ERR_UNSUPPORTED, "%s: n_src=%d exceeds %d", fn, n_src, MOE_MAX_KV_SOURCES);
+    if (!src_k || !src_slots || !src_first) return fail(MOE_ERR_INVALID_ARG, "%s: null source arrays", fn);
+    if (dst_slots < 0) return fail(MOE_ERR_INVALID_ARG, "%s: negative dst_slots", fn);
+    if ((st = check_width("head_dim", head_dim)) != MOE_OK) return st;
+    if (n_heads < 1 || src_heads < 1 || dst_heads < 1 || src_head0 < 0 || dst_head0 < 0 ||
+        src_head0 + n_heads > src_heads || dst_head0 + n_heads > dst_heads)
+        return fail(MOE_ERR_INVALID_ARG, "%s: head ranges [%d, +%d) / [%d, +%d) outside %d / %d heads", fn,
+                    src_head0, n_heads, dst_head0, n_heads, src_heads, dst_heads);
+    if (!src_v != !dst_v) return fail(MOE_ERR_INVALID_ARG, "%s: give both V sides or neither", fn);
+    if (src_first[0] != 0) return fail(MOE_ERR_INVALID_ARG, "%s: src_first[0] must be 0", fn);
+    for (int q = 0; q < n_src; ++q) {
+        if (src_first[q + 1] < src_first[q])
+            return fail(MOE_ERR_INVALID_ARG, "%s: src_first must not decrease", fn);
+        if (src_slots[q] < 0) return fail(MOE_ERR_INVALID_ARG, "%s: negative src_slots[%d]", fn, q);
+        if (src_first[q + 1] > src_first[q]) {
+            if (!src_k[q] || (src_v && !src_v[q])) return fail(MOE_ERR_INVALID_ARG, "%s: null source pool %d", fn, q);
+            if (!aligned16(src_k[q]) || (src_v && !aligned16(src_v[q])))
+                return fail(MOE_ERR_INVALID_ARG, "%s: source pool %d not 16-byte aligned", fn, q);
+        }
+    }
+    if (src_first[n_src] == 0) return MOE_OK;
+    if (!dst_k || !src_slot || !dst_slot) return fail(MOE_ERR_INVALID_ARG, "%s: null pointer", fn);
+    if (!aligned16(dst_k) || !aligned16(dst_v))
+        return fail(MOE_ERR_INVALID_ARG, "%s: destination pools must be 16-byte aligned", fn);
+    return hip_status(launch_kv_move(n_src, src_k, src_v, src_slots, src_first, src_heads, dst_k, dst_v, dst_slots,
+                                     dst_heads, head_dim, src_head0, dst_head0, n_heads, src_slot, dst_slot,
+                                     (hipStream_t)stream),
+                      "moe_kv_move launch");
 }
 
 extern "C" moe_status moe_combine(const uint16_t *y, int64_t y_rows, const int32_t *pair_to_row,

@@ -75,6 +75,13 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
 hipError_t launch_reshard(int dir, int P, int r, int E, int H, int I, const uint16_t *const *src_w13,
                           const uint16_t *const *src_w2, uint16_t *dst_w13, uint16_t *dst_w2, hipStream_t s);
 
+hipError_t launch_kv_slots(const int32_t *page_table, int64_t stride, const int32_t *first, int n_req,
+                           int page_size, int64_t max_tokens, int32_t *slots, hipStream_t s);
+hipError_t launch_kv_move(int n_src, const uint16_t *const *sk, const uint16_t *const *sv, const int64_t *s_slots,
+                          const int64_t *first, int s_heads, uint16_t *dk, uint16_t *dv, int64_t d_slots, int d_heads,
+                          int head_dim, int hs0, int hd0, int nh, const int32_t *src_slot, const int32_t *dst_slot,
+                          hipStream_t s);
+
 hipError_t launch_combine(const uint16_t *y, int64_t y_rows, const int32_t *pair_to_row,
                           const float *w, int64_t T, int k, int H, const uint16_t *shared_y,
                           int64_t sb, int64_t sc, int accumulate, uint16_t *out, hipStream_t s);

@@ -148,6 +148,40 @@ def test_reshard_rejects():
     assert call(s2=half) == INVALID                    # a source with only one of its two tensors
 
 
+def test_kv_rejects():
+    L = moe.lib()
+
+    def move(ns=64, sh=8, nd=64, dh=4, D=128, s0=0, d0=0, n=2, sv=None, dv=None, ntok=5, sk=FAKE, dk=FAKE,
+             nsrc=1, first=None):
+        vp = ctypes.c_void_p * 2
+        k = vp(sk, FAKE)
+        v = None if sv is None else vp(sv, FAKE)
+        slots = (ctypes.c_int64 * 2)(ns, ns)
+        f = (ctypes.c_int64 * 3)(*(first or (0, ntok, ntok)))
+        return L.moe_kv_move(nsrc, k, v, slots, f, sh, dk, dv, nd, dh, D, s0, d0, n, FAKE, FAKE, None)
+    assert move(D=12) == UNSUPPORTED
+    assert move(D=0) == INVALID
+    assert move(s0=7) == INVALID                       # source heads past the pool
+    assert move(d0=3) == INVALID
+    assert move(n=0) == INVALID
+    assert move(sv=FAKE) == INVALID                    # V given on one side only
+    assert move(ntok=-1) == INVALID                    # token offsets decrease
+    assert move(first=(1, 5, 5)) == INVALID            # offsets start at 0
+    assert move(sk=None) == INVALID
+    assert move(sk=ctypes.c_void_p(0x100004)) == INVALID
+    assert move(dk=ctypes.c_void_p(0x100008)) == INVALID
+    assert move(ns=-1) == INVALID
+    assert move(nsrc=0) == INVALID
+    assert move(nsrc=17) == UNSUPPORTED
+    assert move(nsrc=2, first=(0, 3, 2)) == INVALID
+    assert move(ntok=0) == OK                          # nothing to do, nothing launched
+    assert move(sk=None, ntok=0) == OK                 # an empty source may be null
+    assert L.moe_kv_slots(FAKE, 4, FAKE, 2, 0, FAKE, 8, None) == INVALID      # page_size 0
+    assert L.moe_kv_slots(FAKE, 4, FAKE, -1, 16, FAKE, 8, None) == INVALID
+    assert L.moe_kv_slots(None, 4, FAKE, 2, 16, FAKE, 8, None) == INVALID
+    assert L.moe_kv_slots(FAKE, 4, FAKE, 0, 16, FAKE, 8, None) == OK          # no requests
+
+
 def test_combine_rejects():
     L = moe.lib()
 
