@@ -15,6 +15,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import platform
 import sys
@@ -135,6 +136,7 @@ def crossover(args, torch, mi, moe):
     that land on its 16 experts."""
     dev = torch.device("cuda:0")
     batches = [8, 16, 32, 64, 128, 256, 512, 1024, 2048]
+    total = {"tp": {}, "ep": {}}
 
     def up(a):
         return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
@@ -182,7 +184,12 @@ def crossover(args, torch, mi, moe):
                               "local_pairs": int(counts.sum()), "active_experts": int((counts > 0).sum()),
                               "weight_gb_read": float((counts > 0).sum() * 3 * H * cfg.I_s * 2 / 1e9)}),
                   flush=True)
+            total[layout][B] = us + comm
             del graph, layer
+    # the coordinator's start-up calibration: the probed crossover is the initial threshold
+    th = moe.policy_crossover(batches, [total["tp"][B] for B in batches], [total["ep"][B] for B in batches])
+    print(json.dumps({"calibrated_t_high": th if math.isfinite(th) else None, "probed_batches": batches,
+                      "cost": "moe_us + comm_model_us"}), flush=True)
 
 
 def reshard_bench(args, torch, mi, moe):

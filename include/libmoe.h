@@ -255,6 +255,64 @@ moe_status moe_kv_move(int n_src, const uint16_t *const *src_k, const uint16_t *
                        void *stream);
 
 /*
+ * Layout-switch control (host only: arguments are host pointers, no device
+ * is touched, nothing is enqueued).  These calls allocate host memory for
+ * their own sorting and are safe to call from several threads on distinct
+ * policy objects.
+ *
+ * moe_policy: the switch coordinator's state (Sec. 4.5), owned by the
+ *   caller; set it up with moe_policy_init and feed moe_policy_step the
+ *   global in-flight request count once per decode iteration, between
+ *   steps.  In TP it switches to EP as soon as the latest count exceeds
+ *   t_high; in EP it switches back to TP only when the mean count over the
+ *   last `window` iterations (fewer at start) falls below t_low <= t_high.
+ *   After a switch, and after a cancelled attempt, no attempt is made for
+ *   cooldown_s seconds (times are the caller's clock, e.g. seconds since
+ *   start).  target_fits tells whether the other mode can hold the live
+ *   KV cache (moe_kv_fits); if not the switch is cancelled (decision
+ *   MOE_SWITCH_CANCELLED) and the mode stays.  Paper values: t_high = 256,
+ *   cooldown 5 s; interactive serving t_low = 0.8 t_high, window 8;
+ *   rollout t_low = t_high, window 1.
+ * moe_partition_requests: the deterministic TP->EP ownership (Sec. 3.2):
+ *   requests by decreasing length (ties in input order), each placed on the
+ *   rank with the least load tokens_r / T + requests_r / N (ties to the
+ *   lower rank), in exact integer arithmetic so every rank computes the
+ *   same owners.  tokens [n] (>= 0), owner [n] out; rank_tokens [P] and
+ *   rank_requests [P] out, optional (NULL).
+ * moe_kv_fits: whether every rank's KV pool, `capacity` (page, head) units,
+ *   holds the live requests in `mode`: a request of t tokens takes
+ *   ceil(t / page_size) pages of every head its rank holds; under EP a rank
+ *   holds all n_kv_heads of its own requests (owner [n] required), under TP
+ *   max(1, n_kv_heads / P) heads of every request (a head is replicated
+ *   over P / n_kv_heads ranks when there are fewer heads than ranks).
+ *   n_kv_heads and P must divide one another (else MOE_ERR_UNSUPPORTED).
+ * moe_policy_crossover: the initial threshold from decode costs probed in
+ *   both modes at n distinct batch sizes (Sec. 4.5): the smallest probed
+ *   size from which EP is no slower than TP at every larger probed size;
+ *   HUGE_VAL if EP is slower at the largest.
+ */
+#define MOE_POLICY_MAX_WINDOW 1024
+typedef enum moe_mode { MOE_MODE_TP = 0, MOE_MODE_EP = 1 } moe_mode;
+typedef enum moe_decision { MOE_STAY = 0, MOE_SWITCH = 1, MOE_SWITCH_CANCELLED = 2 } moe_decision;
+typedef struct moe_policy {
+    double t_high, t_low, cooldown_s;
+    int32_t window, mode;        /* mode: moe_mode, the current layout */
+    int32_t n_hist, head;        /* ring of the last `window` counts */
+    int32_t has_event, reserved;
+    double last_event_s;         /* last switch or cancelled attempt */
+    int64_t hist_sum;
+    int64_t hist[MOE_POLICY_MAX_WINDOW];
+} moe_policy;
+moe_status moe_policy_init(moe_policy *pol, double t_high, double t_low, int window, double cooldown_s, int mode);
+moe_status moe_policy_step(moe_policy *pol, int64_t in_flight, double now_s, int target_fits, int *decision);
+moe_status moe_partition_requests(const int64_t *tokens, int n, int P, int32_t *owner, int64_t *rank_tokens,
+                                  int32_t *rank_requests);
+moe_status moe_kv_fits(int mode, const int64_t *tokens, int n, const int32_t *owner, int P, int n_kv_heads,
+                       int page_size, int64_t capacity, int *fits);
+moe_status moe_policy_crossover(const int64_t *batch, const double *tp_cost, const double *ep_cost, int n,
+                                double *threshold);
+
+/*
  * Per-kernel timing for measurement.  While enabled, every kernel the
  * library launches is bracketed by HIP events on its own stream (this adds
  * event records to the stream; it never synchronises).  moe_timing_read

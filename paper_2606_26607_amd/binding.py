@@ -22,6 +22,18 @@ MAX_EXPERTS = 1024
 KERNEL_KINDS = {"route": 0, "permute": 1, "gather": 2, "schedule": 3, "gate_up": 4, "down": 5,
                 "combine": 6, "splitk_reduce": 7, "reshard": 8, "kv_move": 9}
 EP_TO_TP, TP_TO_EP = 0, 1
+MODE_TP, MODE_EP = 0, 1
+STAY, SWITCH, SWITCH_CANCELLED = 0, 1, 2
+POLICY_MAX_WINDOW = 1024
+
+
+class _Policy(ctypes.Structure):
+    """struct moe_policy (include/libmoe.h)."""
+    _fields_ = [("t_high", ctypes.c_double), ("t_low", ctypes.c_double), ("cooldown_s", ctypes.c_double),
+                ("window", ctypes.c_int32), ("mode", ctypes.c_int32), ("n_hist", ctypes.c_int32),
+                ("head", ctypes.c_int32), ("has_event", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("last_event_s", ctypes.c_double), ("hist_sum", ctypes.c_int64),
+                ("hist", ctypes.c_int64 * POLICY_MAX_WINDOW)]
 
 
 class MoeError(RuntimeError):
@@ -61,6 +73,13 @@ def lib():
         "moe_reshard_experts": ([i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp], i32),
         "moe_kv_slots": ([vp, i64, vp, i32, i32, vp, i64, vp], i32),
         "moe_kv_move": ([i32, vp, vp, vp, vp, i32, vp, vp, i64, i32, i32, i32, i32, i32, vp, vp, vp], i32),
+        "moe_policy_init": ([ctypes.POINTER(_Policy), ctypes.c_double, ctypes.c_double, i32, ctypes.c_double,
+                             i32], i32),
+        "moe_policy_step": ([ctypes.POINTER(_Policy), i64, ctypes.c_double, i32, ctypes.POINTER(ctypes.c_int)],
+                            i32),
+        "moe_partition_requests": ([vp, i32, i32, vp, vp, vp], i32),
+        "moe_kv_fits": ([i32, vp, i32, vp, i32, i32, i32, i64, ctypes.POINTER(ctypes.c_int)], i32),
+        "moe_policy_crossover": ([vp, vp, vp, i32, ctypes.POINTER(ctypes.c_double)], i32),
         "moe_timing_enable": ([i32], i32),
         "moe_timing_enable_mask": ([ctypes.c_uint32], i32),
         "moe_timing_reset": ([], i32),
@@ -408,6 +427,75 @@ def kv_move(src_k, src_v, dst_k: torch.Tensor, dst_v: Optional[torch.Tensor],
     _check(lib().moe_kv_move(n, ak, av, sl, fi, ks[0].shape[1], _ptr(dst_k), _ptr(dst_v), dst_k.shape[0],
                              dst_k.shape[1], ks[0].shape[2], src_head0, dst_head0, n_heads, _ptr(src_slot),
                              _ptr(dst_slot), _stream(stream)))
+
+
+# ------------------------------------------------- layout-switch control
+def _host(a, dtype):
+    """A contiguous host numpy array of `dtype` (a copy when needed)."""
+    import numpy as np
+    return np.ascontiguousarray(np.asarray(a), dtype=dtype)
+
+
+def _hptr(a):
+    return ctypes.c_void_p(a.ctypes.data) if a.size else None
+
+
+class SwitchPolicy:
+    """The layout-switch coordinator (host only): feed step() the global
+    in-flight request count once per decode iteration; it returns STAY,
+    SWITCH (mode has flipped) or SWITCH_CANCELLED (the other mode could not
+    hold the live KV cache; retried after the cooldown)."""
+
+    def __init__(self, t_high: float, t_low: float, window: int, cooldown_s: float, mode: int = MODE_TP):
+        self._p = _Policy()
+        _check(lib().moe_policy_init(ctypes.byref(self._p), t_high, t_low, window, cooldown_s, mode))
+
+    @property
+    def mode(self) -> int:
+        return self._p.mode
+
+    def step(self, in_flight: int, now_s: float, target_fits: bool = True) -> int:
+        d = ctypes.c_int(-1)
+        _check(lib().moe_policy_step(ctypes.byref(self._p), int(in_flight), float(now_s), 1 if target_fits else 0,
+                                     ctypes.byref(d)))
+        return d.value
+
+
+def partition_requests(tokens, P: int):
+    """Owner rank of every request for a TP->EP switch, plus each rank's
+    token and request totals (numpy arrays)."""
+    import numpy as np
+    t = _host(tokens, np.int64)
+    owner = np.empty(t.size, np.int32)
+    rt = np.empty(P, np.int64)
+    rr = np.empty(P, np.int32)
+    _check(lib().moe_partition_requests(_hptr(t), t.size, P, _hptr(owner), _hptr(rt), _hptr(rr)))
+    return owner, rt, rr
+
+
+def kv_fits(mode: int, tokens, P: int, n_kv_heads: int, page_size: int, capacity: int, owner=None) -> bool:
+    """Whether every rank's KV pool (`capacity` (page, head) units) holds the
+    live requests in `mode` (EP needs the owner of every request)."""
+    import numpy as np
+    t = _host(tokens, np.int64)
+    o = None if owner is None else _host(owner, np.int32)
+    if o is not None and o.size != t.size:
+        raise ValueError("owner needs one entry per request")
+    f = ctypes.c_int(-1)
+    _check(lib().moe_kv_fits(mode, _hptr(t), t.size, None if o is None else _hptr(o), P, n_kv_heads, page_size,
+                             int(capacity), ctypes.byref(f)))
+    return bool(f.value)
+
+
+def policy_crossover(batch, tp_cost, ep_cost) -> float:
+    """Initial switch threshold from decode costs probed in both modes."""
+    import numpy as np
+    b, tc, ec = _host(batch, np.int64), _host(tp_cost, np.float64), _host(ep_cost, np.float64)
+    if not (b.size == tc.size == ec.size):
+        raise ValueError("one cost per probed batch size in each mode")
+    th = ctypes.c_double(0.0)
+    _check(lib().moe_policy_crossover(_hptr(b), _hptr(tc), _hptr(ec), b.size, ctypes.byref(th)))
+    return th.value
 
 
 # ---------------------------------------------------------------- timing
