@@ -49,13 +49,23 @@ __device__ __forceinline__ float silu_mul(float g, float u)
 
 // Large-tile launches split K only from this many K-slices per tile.
 constexpr int SPLIT_MIN_NK = 128;
-// Time of a small-row K-slice relative to a large-tile one (measured: a
-// 32-row slice is bound by its weight rows, a 256-row one by MFMA), as the
-// fraction SMALL_COST_NUM / SMALL_COST_DEN.
-constexpr int SMALL_COST_NUM = 11, SMALL_COST_DEN = 20;
+// The small-row class comes in two heights, chosen per launch by the
+// schedule: 64-row tiles (decode: experts of a few rows) and 128-row tiles
+// (prefill leftovers of 65-128 rows, which would otherwise take two 64-row
+// tiles that each stream the expert's weights).  Each has a largest expert
+// it takes whole and the time of one of its K-slices relative to a
+// large-tile K-slice (measured: a small-row slice is bound by its weight
+// rows, a 256-row one by MFMA), as the fraction cost_num / 20.
+constexpr int SMALL_COST_DEN = 20;
+struct SmallKind {
+    int rows, max_rows, cost_num;
+};
+constexpr SmallKind SMALL64{64, 96, 11};
+constexpr SmallKind SMALL128{128, 128, 11};
 
-// Block-wide exclusive scan of one value per thread (1024 threads); returns
-// the exclusive prefix and writes the total to *total (thread 1023).
+// Block-wide exclusive scan of one value per thread (blocks of whole waves,
+// at most 1024 threads); returns the exclusive prefix and writes the total
+// to *total (last thread).
 __device__ __forceinline__ int32_t block_exscan(int32_t v, int32_t *wsum, int32_t *total)
 {
     const int e = threadIdx.x, lane = e & 63, wv = e >> 6;
@@ -69,9 +79,45 @@ __device__ __forceinline__ int32_t block_exscan(int32_t v, int32_t *wsum, int32_
     __syncthreads();
     int32_t before = 0;
     for (int i = 0; i < wv; ++i) before += wsum[i];
-    if (e == 1023) *total = before + incl;
+    if (e == (int)blockDim.x - 1) *total = before + incl;
     __syncthreads();
     return before + incl - v;
+}
+
+// The same for three values at once (independent shuffle chains run
+// interleaved); totals to tot[0..2].
+__device__ __forceinline__ int3 block_exscan3(int3 v, int32_t (*wsum)[3], int32_t *tot)
+{
+    const int e = threadIdx.x, lane = e & 63, wv = e >> 6;
+    int3 incl = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int ox = __shfl_up(incl.x, off, 64), oy = __shfl_up(incl.y, off, 64), oz = __shfl_up(incl.z, off, 64);
+        if (lane >= off) {
+            incl.x += ox;
+            incl.y += oy;
+            incl.z += oz;
+        }
+    }
+    if (lane == 63) {
+        wsum[wv][0] = incl.x;
+        wsum[wv][1] = incl.y;
+        wsum[wv][2] = incl.z;
+    }
+    __syncthreads();
+    int3 before = make_int3(0, 0, 0);
+    for (int i = 0; i < wv; ++i) {
+        before.x += wsum[i][0];
+        before.y += wsum[i][1];
+        before.z += wsum[i][2];
+    }
+    if (e == (int)blockDim.x - 1) {
+        tot[0] = before.x + incl.x;
+        tot[1] = before.y + incl.y;
+        tot[2] = before.z + incl.z;
+    }
+    __syncthreads();
+    return make_int3(before.x + incl.x - v.x, before.y + incl.y - v.y, before.z + incl.z - v.z);
 }
 
 // Shape of both GEMMs as the schedule's cost model sees it: output tiles per
@@ -84,10 +130,10 @@ struct SchedShape {
 // workgroup, for tl large and ts small-row tiles of nk K-slices: rounds of
 // large tiles (or their stream-K share, with its partial-sum traffic, when
 // there are fewer tiles than workgroups and K is long), plus
-// the small-row share (SMALL_COST_NUM / SMALL_COST_DEN of a large slice per
+// the small-row share (cost_num / SMALL_COST_DEN of a large slice per
 // small-row slice) unless it fits on the workgroups the large tiles leave
 // idle in their last round.
-__device__ __forceinline__ float gemm_cost(int64_t tl, int64_t ts, int nk, int grid)
+__device__ __forceinline__ float gemm_cost(int64_t tl, int64_t ts, int nk, int grid, int cost_num, bool tall)
 {
     const float t = (float)tl, g = (float)grid;
     const bool split = tl < grid && nk >= SPLIT_MIN_NK;
@@ -102,39 +148,53 @@ __device__ __forceinline__ float gemm_cost(int64_t tl, int64_t ts, int nk, int g
         if (rest) c += (0.6f + 0.4f * (float)rest / g) * (float)nk;
     }
     const int idle = rest ? grid - rest : 0;
-    if (!split && idle && SMALL_COST_NUM * ts <= (int64_t)SMALL_COST_DEN * idle) return c;
-    return c + (float)SMALL_COST_NUM / (float)SMALL_COST_DEN * (float)ts * (float)nk / g;
+    if (!split && idle && cost_num * ts <= (int64_t)SMALL_COST_DEN * idle) return c;
+    // 128-row tiles only on idle workgroups: run over the whole grid they are
+    // cut into many stream-K pieces whose larger partials the last
+    // contributor reads back alone (measured slower than 64-row tiles there)
+    if (tall && ts > 0) return 3.0e38f;
+    return c + (float)cost_num / (float)SMALL_COST_DEN * (float)ts * (float)nk / g;
 }
+
+constexpr int NC_SCHED = 10;  // schedule candidates (one thread each)
 
 // Tile schedule of the grouped FFN.  An expert's rows [a, b) are cut at
 // split[e]: rows [a, split) go to the large-tile class (m-tiles of bm rows),
-// rows [split, b) to the small-row class (m-tiles of bm_small rows).  An
-// expert with at most small_max rows is all small.  A larger one may give
-// its leftover rows after whole large tiles to the small class: a nearly
-// empty large tile costs as much as a full one, while small-row tiles are
-// split evenly over the grid.  Which leftovers move (none, or those of at
-// most 32, 64 or 96 rows) is chosen for the lowest estimated time of both
-// GEMMs (gemm_cost).  small_max = 0 disables the small class.
-//   pre[e] / pre_small[e] = m-tiles of that class of the experts before e,
-//   pre[ne] / pre_small[ne] = totals (ne experts: the routed ones, then the
-//   shared one if the call has shared rows).
+// rows [split, b) to the small-row class.  An expert with at most smax rows
+// (96 or 128) is all small.  A larger one may give its leftover rows after
+// whole large tiles to the small class: a nearly empty large tile costs as
+// much as a full one, while small-row tiles are split evenly over the grid.
+// smax and which leftovers move (none, or those of at most 32, 64, 96 or 128
+// rows) are chosen for the lowest estimated time of both GEMMs (gemm_cost);
+// each GEMM then takes the small tile height (64 or 128 rows) that is
+// cheaper for it.  small = false disables the small class.
+//   pre[e] / pre_gu[e] / pre_dn[e] = m-tiles of the large class / of the
+//   small class of the gate-up and of the down GEMM for the experts before
+//   e, [ne] = totals (ne experts: the routed ones, then the shared one if the
+//   call has shared rows), pre_gu[ne + 1] / pre_dn[ne + 1] = the GEMM's
+//   small tile height.
 // Also clears the split-K tile counters (no memset node is needed, so the
 // chain stays graph-capturable).
 __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restrict__ offsets, int El,
-                                                        int64_t cap, int64_t shared_rows, int bm, int bm_small,
-                                                        int small_max,
+                                                        int64_t cap, int64_t shared_rows, int bm, bool small,
                                                         SchedShape sh, int32_t *__restrict__ pre,
-                                                        int32_t *__restrict__ pre_small,
+                                                        int32_t *__restrict__ pre_gu,
+                                                        int32_t *__restrict__ pre_dn,
                                                         int32_t *__restrict__ split,
                                                         int32_t *__restrict__ counters, int64_t n_counters)
 {
-    constexpr int NC = 4;  // leftover thresholds 0, 32, 64, 96 (up to small_max)
-    __shared__ int32_t wsum[16];
-    __shared__ int32_t part[16][2 * NC];
+    constexpr int NT = NC_SCHED / 2;  // leftover thresholds 0, 32, 64, 96, 128
+    constexpr int NC = NC_SCHED;      // candidates: (smax 96 or 128, threshold)
+    __shared__ int32_t wsum[16][3];
+    __shared__ int32_t vals[1024][3 * NC];  // per expert: its tiles of every candidate
+    __shared__ int32_t tot[3 * NC];
+    __shared__ int32_t ptot[3];
     __shared__ int32_t chosen;
     __shared__ float cost[NC];
-    const int e = threadIdx.x, lane = e & 63, wv = e >> 6;
-    for (int64_t i = e; i < n_counters; i += 1024) counters[i] = 0;
+    __shared__ int32_t tall[NC];  // bit 0: gate-up takes 128-row tiles, bit 1: down does
+    // one thread per expert, whole waves (the launch sizes the block)
+    const int e = threadIdx.x;
+    for (int64_t i = e; i < n_counters; i += blockDim.x) counters[i] = 0;
     // experts: the El routed ones, then the shared one when there are shared
     // rows; rows fit int32 (cap + shared rows < 2^31 is checked on the host)
     const int ne = El + (shared_rows > 0 ? 1 : 0);
@@ -144,70 +204,90 @@ __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restric
         const int32_t b = (int32_t)expert_end(offsets, El, cap, shared_rows, e);
         n = b > a ? b - a : 0;
     }
-    // m-tiles of both classes (x: large, y: small) for a leftover threshold th
-    auto tiles_for = [&](int th) {
+    // for candidate c (smax = c / NT ? 128 : 96, threshold 32 * (c % NT)):
+    // large m-tiles (x) and the rows that go to the small class (y)
+    const int32_t whole = n / bm, rest = n - whole * bm;
+    auto rows_for = [&](int c) {
+        const int smax = c / NT ? SMALL128.max_rows : SMALL64.max_rows;
+        const int th = 32 * (c % NT);
         int2 r = make_int2(0, 0);
-        if (n > 0 && n <= small_max) {
-            r.y = (n + bm_small - 1) / bm_small;
+        if (n > 0 && small && n <= smax) {
+            r.y = n;
         } else if (n > 0) {
-            const int32_t whole = n / bm, rest = n - whole * bm;
-            if (rest > 0 && rest <= th) {
+            if (small && rest > 0 && rest <= th) {
                 r.x = whole;
-                r.y = (rest + bm_small - 1) / bm_small;
+                r.y = rest;
             } else {
-                r.x = (n + bm - 1) / bm;
+                r.x = whole + (rest > 0);
             }
         }
         return r;
     };
-    auto wave_sum = [&](int32_t v) {
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-        return v;
-    };
-    int th = 0;
-    if (small_max > 0) {
-        // class totals of every candidate threshold in one block reduction
+    int cand = 0, kinds = 0;
+    if (small) {
+        // class totals of every candidate: large m-tiles, small m-tiles of 64
+        // and of 128 rows; each expert writes its row, one thread per column
+        // sums it (a few dozen experts typically: cheaper than shuffle trees)
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
-            const int2 r = tiles_for(32 * c);
-            const int32_t sx = wave_sum(r.x), sy = wave_sum(r.y);
-            if (lane == 0) {
-                part[wv][2 * c] = sx;
-                part[wv][2 * c + 1] = sy;
-            }
+            const int2 r = rows_for(c);
+            vals[e][3 * c] = r.x;
+            vals[e][3 * c + 1] = (r.y + 63) / 64;
+            vals[e][3 * c + 2] = (r.y + 127) / 128;
         }
         __syncthreads();
-        // candidate c's estimate on thread c, the cheapest on thread 0 (ties:
-        // fewer moves)
+        if (e < 3 * NC) {
+            int32_t sum = 0;
+            for (int i = 0; i < ne; ++i) sum += vals[i][e];
+            tot[e] = sum;
+        }
+        __syncthreads();
+        // candidate c's estimate on thread c (each GEMM with its cheaper
+        // height; ties: 64 rows), the cheapest candidate on thread 0 (ties:
+        // smax 96, then fewer moves)
         if (e < NC) {
-            int64_t tl = 0, ts = 0;
-            for (int w = 0; w < 16; ++w) {
-                tl += part[w][2 * e];
-                ts += part[w][2 * e + 1];
+            const int64_t tl = tot[3 * e], t64 = tot[3 * e + 1], t128 = tot[3 * e + 2];
+            int bits = 0;
+            float total = 0.f;
+            const int nt[2] = {sh.nt_gu, sh.nt_dn}, nk[2] = {sh.nk_gu, sh.nk_dn};
+            for (int gi = 0; gi < 2; ++gi) {
+                const float c64 = gemm_cost(tl * nt[gi], t64 * nt[gi], nk[gi], sh.grid, SMALL64.cost_num, false);
+                const float c128 = gemm_cost(tl * nt[gi], t128 * nt[gi], nk[gi], sh.grid, SMALL128.cost_num, true);
+                if (c128 < c64) bits |= 1 << gi;
+                total += c128 < c64 ? c128 : c64;
             }
-            cost[e] = 32 * e <= small_max ? gemm_cost(tl * sh.nt_gu, ts * sh.nt_gu, sh.nk_gu, sh.grid) +
-                                                gemm_cost(tl * sh.nt_dn, ts * sh.nt_dn, sh.nk_dn, sh.grid)
-                                          : 3.0e38f;
+            cost[e] = total;
+            tall[e] = bits;
         }
         __syncthreads();
         if (e == 0) {
             int b = 0;
             for (int c = 1; c < NC; ++c)
                 if (cost[c] < cost[b]) b = c;
-            chosen = 32 * b;
+            chosen = b;
         }
         __syncthreads();
-        th = chosen;
+        cand = chosen;
+        kinds = tall[cand];
     }
-    const int2 r = tiles_for(th);
-    const int32_t mt = r.x, mts = r.y;
-    if (split && e < ne) split[e] = a + (mts ? mt * bm : n);
-    const int32_t x = block_exscan(mt, wsum, &pre[ne]);
-    if (e < ne) pre[e] = x;
-    if (pre_small) {
-        const int32_t xs = block_exscan(mts, wsum, &pre_small[ne]);
-        if (e < ne) pre_small[e] = xs;
+    const int2 r = rows_for(cand);
+    if (split && e < ne) split[e] = a + (n - r.y);
+    const int h_gu = kinds & 1 ? SMALL128.rows : SMALL64.rows, h_dn = kinds & 2 ? SMALL128.rows : SMALL64.rows;
+    // prefixes of the large m-tiles and of both GEMMs' small m-tiles
+    const int3 x = block_exscan3(make_int3(r.x, (r.y + h_gu - 1) / h_gu, (r.y + h_dn - 1) / h_dn), wsum, ptot);
+    if (e < ne) pre[e] = x.x;
+    if (e == 0) pre[ne] = ptot[0];
+    if (pre_gu) {
+        if (e < ne) {
+            pre_gu[e] = x.y;
+            pre_dn[e] = x.z;
+        }
+        if (e == 0) {
+            pre_gu[ne] = ptot[1];
+            pre_dn[ne] = ptot[2];
+            pre_gu[ne + 1] = h_gu;
+            pre_dn[ne + 1] = h_dn;
+        }
     }
 }
 
@@ -593,7 +673,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                                            const uint16_t *__restrict__ Wsh, int up_off,
                                            uint16_t *__restrict__ C, uint16_t *__restrict__ Csh,
                                            int32_t *__restrict__ tile_cnt, float *__restrict__ partials,
-                                           int grp_base, int grp_size)
+                                           int v, int grp_size)
 {
     constexpr int A_STAGE = BMt * CPR, B_STAGE = BNt * CPR;  // 16-byte chunks per slot
     constexpr int A_INS = BMt / RPI / GEMM_WAVES, B_INS = BNt / RPI / GEMM_WAVES;
@@ -617,15 +697,10 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
     const int wm = wave / WN, wn = wave % WN;
     const int n_tiles = (N + OUTN - 1) / OUTN;
     const int nk = K / BIG_BK;
-    // the class runs on workgroups [grp_base, grp_base + grp_size) of the
-    // XCD-aware numbering below, renumbered from 0
+    // the class runs on grp_size workgroups; this one is number v of them
+    // (negative: not one of them)
     const WorkSplit ws((int64_t)tile_prefix[ne] * n_tiles, nk, grp_size, TAIL);
-    if (ws.T == 0) return;
-    // XCD-aware numbering: the 8 dies take workgroups round robin, so the
-    // workgroups of one die get consecutive virtual ids and with them a
-    // contiguous run of tiles (shared panels in that die's L2).
-    const int v = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3) - grp_base;
-    if (v < 0 || v >= grp_size) return;
+    if (ws.T == 0 || v < 0 || v >= grp_size) return;
     // This lane's chunk within a DMA instruction: row lane/CPR of the
     // instruction's rows, LDS position lane%CPR, global chunk
     // (lane%CPR) ^ swz(row); swz depends on the instruction only through its
@@ -926,10 +1001,23 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
         store_staged(Cb, r0, r1, n0, nvalid);
     };
 
-    // This workgroup's work items, in order: whole tiles v, v+G, ... below
-    // dp, then its stream-K run.  One call site keeps the kernel's register
-    // allocation to a single copy of the pipeline.
-    const int64_t n_dp = v < ws.dp ? (ws.dp - 1 - v) / ws.G + 1 : 0;
+    // This workgroup's work items, in order: its whole tiles, then its
+    // stream-K run.  Whole tiles: the group is 8 runs of G/8 ids, one per die
+    // (die-major numbering, see gemm_grouped); die d takes the contiguous
+    // tiles [dp*d/8, dp*(d+1)/8), dealt round robin over its workgroups, so
+    // each die walks a run of consecutive tiles (m-tiles innermost: shared B
+    // panels in its L2) and every die gets the same number of tiles (the
+    // workgroups idle in the last round are spread over all dies).  One call
+    // site keeps the kernel's register allocation to a single copy of the
+    // pipeline.
+    int64_t n_dp = 0, t0 = 0;
+    const int P = ws.G / 8;
+    if (ws.dp > 0) {
+        const int d = v / P, u = v % P;
+        const int64_t lo = ws.dp * d / 8, hi = ws.dp * (d + 1) / 8;
+        n_dp = u < hi - lo ? (hi - lo - 1 - u) / P + 1 : 0;
+        t0 = lo + u;
+    }
     const bool has_sk = ws.iters > 0 && v < ws.Gsk;
     int64_t sk_i = has_sk ? ws.begin(v) : 0;
     const int64_t sk_end = has_sk ? ws.begin(v + 1) : 0;
@@ -937,7 +1025,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
         int64_t tile;
         int klo, khi;
         if (w < n_dp) {
-            tile = v + w * ws.G;
+            tile = t0 + w * P;
             klo = 0;
             khi = nk;
         } else if (sk_i < sk_end) {
@@ -954,39 +1042,58 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
 
 constexpr int BIGM = 256, BIGN = 256;  // large tiles: 256 rows x 256 weight rows
 constexpr int BIG_WM = 4;              // ... 4 x 2 waves of 64 x 128
-constexpr int SMALLM = 64;             // small-row tiles: 64 rows x 256 weight rows
-constexpr int SMALL_WM = 2;            // ... 2 x 4 waves of 32 x 64
-constexpr int SMALL_MAX = 96;          // experts with at most this many rows use small-row tiles
+// small-row tiles: 64 or 128 rows x 256 weight rows, 2 x 4 waves of 32 x 64
+// or 64 x 64; the 128-row rings are shallower (A(s+1), B(s+2) in flight)
+constexpr int SMALL_WM = 2;
+constexpr int S128_ASL = 2, S128_BSL = 3;
 constexpr int REDUCE_GRID = 2048;      // workgroups of the split-K reduction
 constexpr int BIG_RING = BIG_RING_CHUNKS;
-// floats per partial slot of each class (one per accumulator register)
-constexpr int SLOT_SMALL = (SMALLM / SMALL_WM / 32) * (BIGN / (GEMM_WAVES / SMALL_WM) / 32) * 16 * GEMM_THREADS;
+// floats per partial slot of each class (one per accumulator register; the
+// small class's slots fit either height)
+constexpr int SLOT_SMALL = (SMALL128.rows / SMALL_WM / 32) * (BIGN / (GEMM_WAVES / SMALL_WM) / 32) * 16 *
+                           GEMM_THREADS;
 constexpr int SLOT_BIG = (BIGM / BIG_WM / 32) * (BIGN / (GEMM_WAVES / BIG_WM) / 32) * 16 * GEMM_THREADS;
 
 // Where the small-row class runs: on the workgroups the large tiles leave
 // idle in their last round when its work fits there (its slices, weighted
-// SMALL_COST_NUM / SMALL_COST_DEN, add up to at most one large tile per idle
-// workgroup), else on all workgroups after their large tiles.
+// cost_num / SMALL_COST_DEN, add up to at most one large tile per idle
+// workgroup), else on all workgroups after their large tiles.  vx is this
+// workgroup's die-major id (G/8 consecutive ids per die).  Returns this
+// workgroup's number in the small class's group (negative: not in it) and
+// the group size.
 struct SmallGroup {
-    int base, size;
+    int v, size;
 };
 
-__device__ __forceinline__ SmallGroup small_group(int64_t tl, int64_t ts, int nk, int G)
+__device__ __forceinline__ SmallGroup small_group(int64_t tl, int64_t ts, int nk, int G, int cost_num, int vx)
 {
     const bool large_dp = !(tl < G && nk >= SPLIT_MIN_NK);
-    if (large_dp && tl > 0 && tl % G != 0) {
-        const int64_t idle = G - tl % G;
-        if (SMALL_COST_NUM * ts <= SMALL_COST_DEN * idle) return SmallGroup{(int)(tl % G), (int)idle};
+    if (large_dp && tl > 0 && tl % G != 0 && cost_num * ts <= (int64_t)SMALL_COST_DEN * (G - tl % G)) {
+        // die d holds c_d = tl*(d+1)/8 - tl*d/8 whole tiles; with R rounds
+        // (the busiest die's), its workgroups u < c_d - (R-1)*P are busy in
+        // the last round and the others idle.  Number the idle ones die by
+        // die (G - tl % G of them in all).
+        const int P = G / 8, d = vx / P, u = vx % P;
+        const int64_t R = ((tl + 7) / 8 + P - 1) / P;
+        int before = 0, mine = -1;
+        for (int dd = 0; dd < 8; ++dd) {
+            const int64_t c = tl * (dd + 1) / 8 - tl * dd / 8;
+            const int64_t b64 = c - (R - 1) * P;
+            const int busy = b64 < 0 ? 0 : (b64 > P ? P : (int)b64);
+            if (dd == d && u >= busy) mine = before + (u - busy);
+            before += P - busy;
+        }
+        return SmallGroup{mine, before};
     }
-    return SmallGroup{0, G};
+    return SmallGroup{vx, G};
 }
 
 // One grouped GEMM launch: the large-tile class (256-row tiles) and the
-// small-row class (32-row tiles, K-split over its workgroups: these stream
-// weights, and spreading them over many CUs is what reaches HBM bandwidth)
-// in the same persistent grid.  The classes cover disjoint rows, so a
-// workgroup goes from its large tiles to its small-row share without
-// waiting for anyone.
+// small-row class (64- or 128-row tiles as the schedule chose, K-split over
+// its workgroups: these stream weights, and spreading them over many CUs is
+// what reaches HBM bandwidth) in the same persistent grid.  The classes
+// cover disjoint rows, so a workgroup goes from its large tiles to its
+// small-row share without waiting for anyone.
 template <bool GATED>
 __global__ __attribute__((amdgpu_flat_work_group_size(GEMM_THREADS, GEMM_THREADS), amdgpu_waves_per_eu(2, 2)))
 void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
@@ -994,16 +1101,26 @@ void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
     __shared__ uint4 ring[BIG_RING];
     constexpr int OUTN = GATED ? BIGN / 2 : BIGN;
     const int64_t n_tiles = (g.N + OUTN - 1) / OUTN;
+    const bool tall = small.tile_prefix[g.ne + 1] == SMALL128.rows;  // uniform
+    // die-major id: the hardware deals workgroups to the 8 dies round robin
+    const int vx = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
     const SmallGroup sg = small_group((int64_t)large.tile_prefix[g.ne] * n_tiles,
-                                      (int64_t)small.tile_prefix[g.ne] * n_tiles, g.K / BIG_BK, gridDim.x);
+                                      (int64_t)small.tile_prefix[g.ne] * n_tiles, g.K / BIG_BK, gridDim.x,
+                                      tall ? SMALL128.cost_num : SMALL64.cost_num, vx);
     gemm_class<BIGM, BIGN, GATED, BIG_WM, false, A_SLOTS, B_SLOTS>(
         ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, large.tile_prefix, g.El, g.ne, g.cap,
         g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh, large.tile_cnt,
-        large.partials, 0, gridDim.x);
-    gemm_class<SMALLM, BIGN, GATED, SMALL_WM, true, SA_SLOTS, SB_SLOTS>(
-        ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, small.tile_prefix, g.El, g.ne, g.cap,
-        g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh, small.tile_cnt,
-        small.partials, sg.base, sg.size);
+        large.partials, vx, gridDim.x);
+    if (tall)
+        gemm_class<SMALL128.rows, BIGN, GATED, SMALL_WM, true, S128_ASL, S128_BSL>(
+            ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, small.tile_prefix, g.El, g.ne, g.cap,
+            g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh,
+            small.tile_cnt, small.partials, sg.v, sg.size);
+    else
+        gemm_class<SMALL64.rows, BIGN, GATED, SMALL_WM, true, SA_SLOTS, SB_SLOTS>(
+            ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, small.tile_prefix, g.El, g.ne, g.cap,
+            g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh,
+            small.tile_cnt, small.partials, sg.v, sg.size);
 }
 
 // Combines the split-K partials of the large-tile class after its GEMM
@@ -1081,7 +1198,8 @@ int device_cus()
 }
 
 // Workspace layout of the grouped FFN (every part 256-byte aligned):
-//   prefix large [El+1] | prefix small [El+1] | class cut [El] |
+//   prefix large [El+1] | prefix small, gate-up and down [El+1] + small tile height each |
+//   class cut [El] |
 //   tile counters: large gate-up, large down, small gate-up, small down |
 //   split-K partial slots: small [2*G][SLOT_SMALL], large [2*G][SLOT_BIG] fp32 |
 //   h [cap, I_s] bf16
@@ -1091,7 +1209,7 @@ struct FfnLayout {
     bool big;
     int64_t t_gu, t_dn, ts_gu, ts_dn;  // tile-count bounds per class and GEMM
     int grid;                          // persistent workgroups of a large-tile launch
-    size_t off_pre_s, off_split, off_cnt, off_part_s, off_part, off_h, total;
+    size_t off_pre_s, off_pre_sd, off_split, off_cnt, off_part_s, off_part, off_h, total;
     FfnLayout(int64_t cap, int El, int H, int Is)
     {
         big = (H % BIG_BK == 0) && (Is % BIG_BK == 0) && H >= 2 * BIG_BK && Is >= 2 * BIG_BK;
@@ -1099,14 +1217,17 @@ struct FfnLayout {
         const int64_t mt = ceil_div(cap, bm) + El;
         t_gu = mt * ceil_div(Is, big ? BIGN / 2 : BN);
         t_dn = mt * ceil_div(H, big ? BIGN : BN);
-        // a small-row expert has at most SMALL_MAX rows: ceil(SMALL_MAX/SMALLM) m-tiles
-        const int64_t mts = big ? (int64_t)El * ceil_div(SMALL_MAX, SMALLM) : 0;
+        // a small-row expert or leftover has at most max_rows rows: at most
+        // two m-tiles of either height
+        static_assert(SMALL64.max_rows <= 2 * SMALL64.rows && SMALL128.max_rows <= 2 * SMALL128.rows, "");
+        const int64_t mts = big ? (int64_t)El * 2 : 0;
         ts_gu = mts * ceil_div(Is, BIGN / 2);
         ts_dn = mts * ceil_div(H, BIGN);
         grid = device_cus();
         const size_t slots = big ? 2 * (size_t)grid : 0;
         off_pre_s = align256((size_t)(El + 1) * sizeof(int32_t));
-        off_split = off_pre_s + align256((size_t)(El + 1) * sizeof(int32_t));
+        off_pre_sd = off_pre_s + align256((size_t)(El + 2) * sizeof(int32_t));
+        off_split = off_pre_sd + align256((size_t)(El + 2) * sizeof(int32_t));
         off_cnt = off_split + align256((size_t)El * sizeof(int32_t));
         off_part_s = off_cnt + align256((size_t)(t_gu + t_dn + ts_gu + ts_dn) * sizeof(int32_t));
         off_part = off_part_s + align256(slots * SLOT_SMALL * sizeof(float));
@@ -1145,7 +1266,8 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
     const FfnLayout L(rows, ne, H, Is);
     char *base = static_cast<char *>(ws);
     int32_t *pre = reinterpret_cast<int32_t *>(base);
-    int32_t *pre_s = reinterpret_cast<int32_t *>(base + L.off_pre_s);
+    int32_t *pre_s = reinterpret_cast<int32_t *>(base + L.off_pre_s);    // small class, gate-up
+    int32_t *pre_sd = reinterpret_cast<int32_t *>(base + L.off_pre_sd);  // small class, down
     int32_t *split = reinterpret_cast<int32_t *>(base + L.off_split);
     int32_t *cnt = reinterpret_cast<int32_t *>(base + L.off_cnt);
     float *part_s = reinterpret_cast<float *>(base + L.off_part_s);
@@ -1157,10 +1279,11 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
     hipError_t err;
     {
         KernelTimer timer(MOE_K_SCHEDULE, s);
-        schedule_kernel<<<dim3(1), dim3(1024), 0, s>>>(
-            offsets, El, cap, sc, big ? BIGM : BM, SMALLM, big ? SMALL_MAX : 0,
+        const unsigned threads = (unsigned)(ceil_div(ne > NC_SCHED ? ne : NC_SCHED, 64) * 64);
+        schedule_kernel<<<dim3(1), dim3(threads), 0, s>>>(
+            offsets, El, cap, sc, big ? BIGM : BM, big,
             SchedShape{(int)ceil_div(Is, BIGN / 2), H / BIG_BK, (int)ceil_div(H, BIGN), Is / BIG_BK, L.grid}, pre,
-            big ? pre_s : nullptr, big ? split : nullptr, cnt,
+            big ? pre_s : nullptr, big ? pre_sd : nullptr, big ? split : nullptr, cnt,
             big ? L.t_gu + L.t_dn + L.ts_gu + L.ts_dn : 0);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
@@ -1185,7 +1308,7 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
             const GemmArgs g{h, nullptr, 1, rows, offsets, split, El, ne, cap, sc, shared_begin,
                              H, Is,      w2, (int64_t)H * Is, sw2, 0, y, shared_y};
             gemm_grouped<false><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
-                g, TileClass{pre_s, cs_dn, part_s}, TileClass{pre, c_dn, part});
+                g, TileClass{pre_sd, cs_dn, part_s}, TileClass{pre, c_dn, part});
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         if (Is / BIG_BK >= SPLIT_MIN_NK) {

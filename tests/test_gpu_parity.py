@@ -240,6 +240,35 @@ def test_grouped_ffn_shared(oracle, El, E, H, Is, T, k, e0, sb, sc):
         assert_close_rel(got_s, ref_s, what=f"shared sb={sb} sc={sc}")
 
 
+@pytest.mark.parametrize("counts,H,Is", [([592] * 16, 512, 1024),
+                                         ([1091], 512, 2048),
+                                         ([100, 128, 97, 120, 1, 0, 640, 383] * 2, 256, 512)])
+def test_grouped_ffn_tall_leftovers(oracle, counts, H, Is):
+    """Experts whose rows leave 65-128 after whole 256-row tiles, or have
+    97-128 rows in all: the schedule may take 128-row tiles for them (16
+    experts of 512 + 80 rows fill exactly one round of large tiles, so the
+    80-row leftovers run on every workgroup and one 128-row tile each is
+    cheaper than two 64-row ones).  The result matches the oracle and is
+    bitwise reproducible."""
+    E = len(counts)
+    g = np.random.default_rng(sum(counts))
+    ids = g.permutation(np.repeat(np.arange(E, dtype=np.int32), counts))[:, None]
+    T = ids.shape[0]
+    _, offs, _, _ = oracle.permute(ids, 0, E)
+    np.testing.assert_array_equal(np.diff(offs), counts)
+    x_perm = mi.random_bf16((T, H), seed=T, tag=52)
+    w13 = mi.random_bf16((E, 2 * Is, H), seed=T, tag=53, std=0.05)
+    w2 = mi.random_bf16((E, H, Is), seed=T, tag=54, std=0.05)
+    runs = []
+    for _ in range(2):
+        y = moe.grouped_ffn(dev_bf16(x_perm), torch.from_numpy(offs).cuda(), dev_bf16(w13), dev_bf16(w2))
+        torch.cuda.synchronize()
+        runs.append(bf16_f64(host_bf16(y)[:T]))
+    ref = oracle.grouped_ffn(x_perm, offs, w13, w2)
+    assert_close_rel(runs[0], ref, what=f"tall leftovers E={E} H={H} Is={Is}")
+    np.testing.assert_array_equal(runs[0], runs[1])
+
+
 def test_grouped_ffn_skewed_and_empty_experts(oracle):
     got, ref = ffn_case(oracle, 8, 256, 128, 700, 2, seed=3, hot=5)
     assert_close_rel(got, ref, what="skewed")
