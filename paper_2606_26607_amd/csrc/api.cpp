@@ -95,7 +95,8 @@ extern "C" moe_status moe_route(const float *logits, int64_t T, int E, int k, in
 extern "C" size_t moe_permute_workspace_size(int64_t T, int k, int n_local_experts)
 {
     if (T < 0 || k < 1 || n_local_experts < 1) return 0;
-    return align256((size_t)(permute_chunks(T, k) + 1) * (size_t)n_local_experts * sizeof(int32_t));
+    return align256((size_t)(permute_chunks(T, k, n_local_experts) + 1) * (size_t)n_local_experts *
+                    sizeof(int32_t));
 }
 
 extern "C" moe_status moe_permute(const int32_t *topk_ids, int64_t T, int k, int E, int expert_begin,

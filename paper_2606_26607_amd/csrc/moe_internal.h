@@ -52,7 +52,7 @@ struct KernelTimer {
 hipError_t launch_route(const float *logits, int64_t T, int E, int k, int32_t *ids, float *w,
                         hipStream_t s);
 
-int64_t permute_chunks(int64_t T, int k);
+int64_t permute_chunks(int64_t T, int k, int El);
 hipError_t launch_permute(const int32_t *ids, int64_t T, int k, int e0, int El, int32_t *counts,
                           int32_t *offsets, int32_t *row_to_pair, int32_t *pair_to_row,
                           const uint16_t *x, int H, uint16_t *x_perm, int64_t cap, int32_t *ws,

@@ -1,6 +1,8 @@
 // Permutation: stable counting sort of (token, slot) pairs by local expert.
 //
-// The T*k pairs are cut into chunks of 1024, one wavefront per chunk:
+// The T*k pairs are cut into chunks of 256 (or 1024 when pairs x experts
+// is large, which keeps the per-chunk histograms small), one wavefront per
+// chunk:
 //   1. count:   per-chunk histogram over local experts (LDS),
 //   2. scan:    per expert, exclusive prefix over chunks; per-expert totals
 //               and their exclusive prefix over experts give `offsets`, and
@@ -17,8 +19,9 @@
 namespace moe {
 namespace {
 
-constexpr int CHUNK = 1024;
-constexpr int ROUNDS = CHUNK / 64;
+// Chunk size: short chunks give more wavefronts (the scatter walks its
+// chunk 64 pairs at a time, in order), long ones fewer histogram rows.
+int chunk_pairs(int64_t npairs, int El) { return npairs * El <= ((int64_t)1 << 24) ? 256 : 1024; }
 
 __device__ __forceinline__ int local_index(int32_t id, int e0, int El)
 {
@@ -26,9 +29,11 @@ __device__ __forceinline__ int local_index(int32_t id, int e0, int El)
     return (d >= 0 && d < El) ? d : El;  // El marks a pair owned elsewhere
 }
 
+template <int ROUNDS>
 __global__ __launch_bounds__(64) void count_kernel(const int32_t *__restrict__ ids, int64_t npairs,
                                                    int e0, int El, int32_t *__restrict__ chunk_cnt)
 {
+    constexpr int CHUNK = ROUNDS * 64;
     extern __shared__ int32_t hist[];
     const int lane = threadIdx.x;
     const int64_t c = blockIdx.x;
@@ -114,12 +119,14 @@ __global__ __launch_bounds__(1024) void scan_kernel(int32_t *__restrict__ chunk_
     }
 }
 
+template <int ROUNDS>
 __global__ __launch_bounds__(64) void scatter_kernel(const int32_t *__restrict__ ids, int64_t npairs,
                                                      int e0, int El, int nbits,
                                                      const int32_t *__restrict__ chunk_base,
                                                      int32_t *__restrict__ row_to_pair,
                                                      int32_t *__restrict__ pair_to_row)
 {
+    constexpr int CHUNK = ROUNDS * 64;
     extern __shared__ int32_t next_row[];
     const int lane = threadIdx.x;
     const int64_t c = blockIdx.x;
@@ -175,7 +182,7 @@ __global__ __launch_bounds__(256) void gather_kernel(const uint16_t *__restrict_
 
 }  // namespace
 
-int64_t permute_chunks(int64_t T, int k) { return ceil_div(T * k, CHUNK); }
+int64_t permute_chunks(int64_t T, int k, int El) { return ceil_div(T * k, chunk_pairs(T * k, El)); }
 
 hipError_t launch_permute(const int32_t *ids, int64_t T, int k, int e0, int El, int32_t *counts,
                           int32_t *offsets, int32_t *row_to_pair, int32_t *pair_to_row,
@@ -183,15 +190,20 @@ hipError_t launch_permute(const int32_t *ids, int64_t T, int k, int e0, int El, 
                           hipStream_t s)
 {
     const int64_t npairs = T * k;
-    const int64_t nchunks = permute_chunks(T, k);
+    const int64_t nchunks = permute_chunks(T, k, El);
+    const bool short_chunks = chunk_pairs(npairs, El) == 256;
     int nbits = 0;
     while ((1 << nbits) < El + 2) ++nbits;  // distinguishes 0..El+1
     hipError_t err;
     {
         KernelTimer timer(MOE_K_PERMUTE, s);
         if (nchunks > 0) {
-            count_kernel<<<dim3((unsigned)nchunks), dim3(64), El * sizeof(int32_t), s>>>(
-                ids, npairs, e0, El, ws);
+            if (short_chunks)
+                count_kernel<4><<<dim3((unsigned)nchunks), dim3(64), El * sizeof(int32_t), s>>>(
+                    ids, npairs, e0, El, ws);
+            else
+                count_kernel<16><<<dim3((unsigned)nchunks), dim3(64), El * sizeof(int32_t), s>>>(
+                    ids, npairs, e0, El, ws);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         int L = 1;
@@ -199,8 +211,12 @@ hipError_t launch_permute(const int32_t *ids, int64_t T, int k, int e0, int El, 
         scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(ws, nchunks, El, L, counts, offsets);
         if ((err = hipGetLastError()) != hipSuccess) return err;
         if (nchunks > 0) {
-            scatter_kernel<<<dim3((unsigned)nchunks), dim3(64), El * sizeof(int32_t), s>>>(
-                ids, npairs, e0, El, nbits, ws, row_to_pair, pair_to_row);
+            if (short_chunks)
+                scatter_kernel<4><<<dim3((unsigned)nchunks), dim3(64), El * sizeof(int32_t), s>>>(
+                    ids, npairs, e0, El, nbits, ws, row_to_pair, pair_to_row);
+            else
+                scatter_kernel<16><<<dim3((unsigned)nchunks), dim3(64), El * sizeof(int32_t), s>>>(
+                    ids, npairs, e0, El, nbits, ws, row_to_pair, pair_to_row);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
     }
