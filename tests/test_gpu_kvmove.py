@@ -159,3 +159,39 @@ def test_all_sources_in_one_launch():
         t0 += counts[q]
     np.testing.assert_array_equal(host(Dk), rk)
     np.testing.assert_array_equal(host(Dv), rv)
+
+
+def test_sixteen_sources_and_degenerate_tables():
+    """The maximum of 16 source pools in one launch (some supplying no
+    tokens), a slot expansion with capacity 0 (writes nothing), and a page
+    table narrower than a request (its tokens past the last listed page get
+    slot -1 and are not moved)."""
+    rng = np.random.default_rng(21)
+    S, Hs, D = 96, 2, 64
+    counts = [int(c) for c in rng.integers(0, 9, 16)]
+    counts[3] = counts[11] = 0
+    n = sum(counts)
+    pools_k = [rng.integers(0, 65536, (S, Hs, D), dtype=np.uint16) for _ in range(16)]
+    src = np.concatenate([rng.integers(0, S, c) for c in counts]).astype(np.int32)
+    dst = rng.permutation(4 * S)[:n].astype(np.int32)
+    dk = rng.integers(0, 65536, (4 * S, 1, D), dtype=np.uint16)
+    Dk = dev(dk)
+    moe.kv_move([dev(t) for t in pools_k], None, Dk, None, torch.from_numpy(src).cuda(),
+                torch.from_numpy(dst).cuda(), 1, 0, 1, src_tokens=counts)
+    torch.cuda.synchronize()
+    ref, t0 = dk, 0
+    for q in range(16):
+        ref = kvmove.kv_move(pools_k[q], ref, src[t0:t0 + counts[q]], dst[t0:t0 + counts[q]], 1, 0, 1)
+        t0 += counts[q]
+    np.testing.assert_array_equal(host(Dk), ref)
+    # capacity 0: nothing written
+    out = torch.full((4,), -7, dtype=torch.int32, device="cuda")
+    tab = torch.zeros((1, 2), dtype=torch.int32, device="cuda")
+    moe.kv_slots(tab, torch.tensor([0, 5], dtype=torch.int32, device="cuda"), 4, out=out, capacity=0)
+    torch.cuda.synchronize()
+    assert torch.all(out == -7)
+    # a 2-page table for a 13-token request with 4-token pages: tokens 8..12 have no page
+    tab = torch.tensor([[3, 1]], dtype=torch.int32, device="cuda")
+    got = gpu_slots(tab.cpu().numpy(), [13], 4)
+    np.testing.assert_array_equal(got[:8], kvmove.token_slots([[3, 1]], [8], 4))
+    assert np.all(got[8:13] == -1)
