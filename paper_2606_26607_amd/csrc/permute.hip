@@ -74,9 +74,18 @@ __global__ __launch_bounds__(1024) void scan_kernel(int32_t *__restrict__ chunk_
     const int64_t per = (nchunks + L - 1) / L;
     const int64_t c0 = (int64_t)j * per;
     const int64_t c1 = c0 + per < nchunks ? c0 + per : nchunks;
+    // the lane's run of chunk counts, loaded UNR at a time (independent
+    // loads, one memory round trip per batch)
+    constexpr int UNR = 8;
     int32_t run = 0;
     if (active)
-        for (int64_t c = c0; c < c1; ++c) run += chunk_cnt[c * El + e];
+        for (int64_t c = c0; c < c1; c += UNR) {
+            int32_t v[UNR];
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) v[u] = c + u < c1 ? chunk_cnt[(c + u) * El + e] : 0;
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) run += v[u];
+        }
     // exclusive scan of the runs over the L lanes of the expert's group
     int32_t incl = run;
     for (int off = 1; off < L; off <<= 1) {
@@ -111,11 +120,76 @@ __global__ __launch_bounds__(1024) void scan_kernel(int32_t *__restrict__ chunk_
     __syncthreads();
     if (active) {
         int32_t row = tot[e] + seg_before;
-        for (int64_t c = c0; c < c1; ++c) {
-            const int32_t v = chunk_cnt[c * El + e];
-            chunk_cnt[c * El + e] = row;
-            row += v;
+        for (int64_t c = c0; c < c1; c += UNR) {
+            int32_t v[UNR];
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) v[u] = c + u < c1 ? chunk_cnt[(c + u) * El + e] : 0;
+#pragma unroll
+            for (int u = 0; u < UNR; ++u)
+                if (c + u < c1) {
+                    chunk_cnt[(c + u) * El + e] = row;
+                    row += v[u];
+                }
         }
+    }
+}
+
+// The scan for at most 64 local experts: lane = expert, each of the 16
+// wavefronts owns a contiguous range of chunks and walks its rows (El
+// consecutive counts: one coalesced load per row, 8 rows in flight).  Wave
+// totals per expert give each wave's starting row; the exclusive scan over
+// experts fits one wavefront, so every wave computes it itself.
+__global__ __launch_bounds__(1024) void scan_narrow_kernel(int32_t *__restrict__ chunk_cnt, int64_t nchunks,
+                                                           int El, int32_t *__restrict__ counts,
+                                                           int32_t *__restrict__ offsets)
+{
+    constexpr int UNR = 8;
+    __shared__ int32_t wtot[16][64];
+    const int t = threadIdx.x, lane = t & 63, wv = t >> 6, nw = blockDim.x >> 6;
+    const bool act = lane < El;
+    const int64_t per = (nchunks + nw - 1) / nw;
+    const int64_t c0 = wv * per < nchunks ? wv * per : nchunks;
+    const int64_t c1 = c0 + per < nchunks ? c0 + per : nchunks;
+    int32_t run = 0;
+    for (int64_t c = c0; c < c1; c += UNR) {
+        int32_t v[UNR];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) v[u] = act && c + u < c1 ? chunk_cnt[(c + u) * El + lane] : 0;
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) run += v[u];
+    }
+    wtot[wv][lane] = run;
+    __syncthreads();
+    int32_t before_w = 0, total = 0;
+    for (int w = 0; w < nw; ++w) {
+        const int32_t x = wtot[w][lane];
+        before_w += w < wv ? x : 0;
+        total += x;
+    }
+    // exclusive scan of the expert totals over the lanes (experts)
+    int32_t incl = total;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int32_t o = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += o;
+    }
+    const int32_t eexcl = incl - total;
+    if (wv == 0 && act) {
+        counts[lane] = total;
+        offsets[lane] = eexcl;
+        if (lane == El - 1) offsets[El] = incl;  // total over all experts
+    }
+    int32_t row = eexcl + before_w;
+    for (int64_t c = c0; c < c1; c += UNR) {
+        int32_t v[UNR];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) v[u] = act && c + u < c1 ? chunk_cnt[(c + u) * El + lane] : 0;
+#pragma unroll
+        for (int u = 0; u < UNR; ++u)
+            if (act && c + u < c1) {
+                chunk_cnt[(c + u) * El + lane] = row;
+                row += v[u];
+            }
     }
 }
 
@@ -206,9 +280,13 @@ hipError_t launch_permute(const int32_t *ids, int64_t T, int k, int e0, int El, 
                     ids, npairs, e0, El, ws);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
-        int L = 1;
-        while (L < 64 && 2 * L * El <= 1024) L *= 2;
-        scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(ws, nchunks, El, L, counts, offsets);
+        if (El <= 64) {
+            scan_narrow_kernel<<<dim3(1), dim3(1024), 0, s>>>(ws, nchunks, El, counts, offsets);
+        } else {
+            int L = 1;
+            while (L < 64 && 2 * L * El <= 1024) L *= 2;
+            scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(ws, nchunks, El, L, counts, offsets);
+        }
         if ((err = hipGetLastError()) != hipSuccess) return err;
         if (nchunks > 0) {
             if (short_chunks)
