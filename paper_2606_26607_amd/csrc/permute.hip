@@ -193,6 +193,98 @@ __global__ __launch_bounds__(1024) void scan_narrow_kernel(int32_t *__restrict__
     }
 }
 
+// The whole permutation in one workgroup, for at most SMALL_PAIRS pairs and
+// 64 local experts: each of the 16 wavefronts owns a contiguous run of pairs
+// (kept in registers), counts it per expert with the same ballot ranking as
+// the scatter, the per-(wave, expert) bases are scanned in LDS, and the
+// wavefronts then place their pairs in order.  Same stable result as the
+// three-kernel path.
+constexpr int SMALL_PAIRS = 16 * 1024;
+__global__ __launch_bounds__(1024) void permute_small_kernel(const int32_t *__restrict__ ids, int64_t npairs,
+                                                             int e0, int El, int nbits,
+                                                             int32_t *__restrict__ counts,
+                                                             int32_t *__restrict__ offsets,
+                                                             int32_t *__restrict__ row_to_pair,
+                                                             int32_t *__restrict__ pair_to_row)
+{
+    constexpr int MAXR = SMALL_PAIRS / 1024;  // rounds of 64 pairs per wave, at most
+    __shared__ int32_t base[16][64];
+    const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+    const int64_t per = ((npairs + 15) / 16 + 63) / 64 * 64;  // pairs per wave, whole rounds
+    const int64_t p0 = wv * per;
+    const int rounds = (int)((per + 63) / 64);
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    int32_t le[MAXR];
+#pragma unroll
+    for (int r = 0; r < MAXR; ++r) {
+        const int64_t p = p0 + r * 64 + lane;
+        le[r] = r < rounds && p < npairs ? local_index(ids[p], e0, El) : El + 1;
+    }
+    if (lane < El) base[wv][lane] = 0;
+    __syncthreads();
+    // per-(wave, expert) counts: the first lane of each group of equal
+    // experts in a round adds the group's size
+    auto peers_of = [&](int x) {
+        uint64_t m = ~0ull;
+        for (int b = 0; b < nbits; ++b) {
+            const bool bit = (x >> b) & 1;
+            const uint64_t bal = __ballot(bit);
+            m &= bit ? bal : ~bal;
+        }
+        return m;
+    };
+#pragma unroll
+    for (int r = 0; r < MAXR; ++r) {
+        if (r >= rounds) break;
+        const uint64_t peers = peers_of(le[r]);
+        if (le[r] < El && __popcll(peers & below) == 0) base[wv][le[r]] += __popcll(peers);
+    }
+    __syncthreads();
+    // expert totals, their exclusive scan (one wavefront), and each wave's
+    // first row per expert
+    if (wv == 0) {
+        int32_t total = 0;
+        if (lane < El)
+            for (int w = 0; w < 16; ++w) total += base[w][lane];
+        int32_t incl = total;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int32_t o = __shfl_up(incl, off, 64);
+            if (lane >= off) incl += o;
+        }
+        if (lane < El) {
+            counts[lane] = total;
+            offsets[lane] = incl - total;
+            if (lane == El - 1) offsets[El] = incl;
+            int32_t row = incl - total;
+            for (int w = 0; w < 16; ++w) {
+                const int32_t c = base[w][lane];
+                base[w][lane] = row;
+                row += c;
+            }
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < MAXR; ++r) {
+        if (r >= rounds) break;
+        const int64_t p = p0 + r * 64 + lane;
+        const uint64_t peers = peers_of(le[r]);
+        const int rank = __popcll(peers & below);
+        if (le[r] < El) {
+            const int32_t row = base[wv][le[r]] + rank;
+            row_to_pair[row] = (int32_t)p;
+            pair_to_row[p] = row;
+        } else if (le[r] == El) {
+            pair_to_row[p] = -1;
+        }
+        // a wave's own LDS row: its leaders bump it after every lane read it
+        __builtin_amdgcn_wave_barrier();
+        if (le[r] < El && rank == 0) base[wv][le[r]] += __popcll(peers);
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
 template <int ROUNDS>
 __global__ __launch_bounds__(64) void scatter_kernel(const int32_t *__restrict__ ids, int64_t npairs,
                                                      int e0, int El, int nbits,
@@ -269,7 +361,12 @@ hipError_t launch_permute(const int32_t *ids, int64_t T, int k, int e0, int El, 
     int nbits = 0;
     while ((1 << nbits) < El + 2) ++nbits;  // distinguishes 0..El+1
     hipError_t err;
-    {
+    if (npairs > 0 && npairs <= SMALL_PAIRS && El <= 64) {
+        KernelTimer timer(MOE_K_PERMUTE, s);
+        permute_small_kernel<<<dim3(1), dim3(1024), 0, s>>>(ids, npairs, e0, El, nbits, counts, offsets,
+                                                             row_to_pair, pair_to_row);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+    } else {
         KernelTimer timer(MOE_K_PERMUTE, s);
         if (nchunks > 0) {
             if (short_chunks)

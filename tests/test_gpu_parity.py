@@ -108,11 +108,14 @@ def test_permute_configs(oracle, name):
 
 @pytest.mark.parametrize("T,E,k,P", [(1, 8, 2, 1), (1, 8, 2, 8), (1023, 8, 2, 2), (1025, 64, 8, 8),
                                      (5000, 128, 8, 8), (3000, 1024, 16, 4), (2048, 16, 1, 1),
-                                     (70000, 8, 2, 8), (8192, 256, 8, 1), (20000, 512, 8, 2)])
+                                     (70000, 8, 2, 8), (8192, 256, 8, 1), (20000, 512, 8, 2),
+                                     (2048, 64, 8, 1), (4096, 128, 4, 2), (4097, 128, 4, 2)])
 def test_permute_every_rank(oracle, T, E, k, P):
-    """Every rank's slice of the same routing, against the oracle.  Pairs x
+    """Every rank's slice of the same routing, against the oracle.  Up to
+    16384 pairs and 64 local experts run in one workgroup (the last three
+    cases: 16384 pairs with 64 experts, then 16388); above that pairs x
     local experts up to 2^24 take 256-pair chunks, larger ones 1024-pair
-    chunks (the last two cases sit on either side of that line)."""
+    chunks (the two cases before them sit on either side of that line)."""
     ids = mi.random_topk_ids(T, E, k, seed=T + E + k)
     total = 0
     for r in range(P):
