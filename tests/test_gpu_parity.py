@@ -397,3 +397,45 @@ def test_layer_is_deterministic():
     torch.cuda.synchronize()
     np.testing.assert_array_equal(out1, out2)
     np.testing.assert_array_equal(y1, host_bf16(layer.y))
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_grouped_ffn_random_row_mixes(oracle, seed):
+    """Seeded random shapes and per-expert row counts (empty experts, a few
+    rows, leftovers of every size after whole 256-row tiles, several whole
+    tiles), large-tile and general shapes alike: the schedule's choices
+    (tail threshold, small tile height, die ranges, idle-slot placement)
+    all give the oracle's result, bitwise reproducibly."""
+    g = np.random.default_rng(900 + seed)
+    El = int(g.integers(1, 41))
+    H = int(g.choice([128, 256, 384, 512, 136]))
+    Is = int(g.choice([128, 192, 256, 512, 72]))
+    kinds = g.integers(0, 5, El)
+    counts = []
+    for kd in kinds:
+        if kd == 0:
+            counts.append(0)
+        elif kd == 1:
+            counts.append(int(g.integers(1, 33)))
+        elif kd == 2:
+            counts.append(int(g.integers(33, 257)))
+        elif kd == 3:
+            counts.append(256 * int(g.integers(1, 4)) + int(g.integers(0, 256)))
+        else:
+            counts.append(256 * int(g.integers(1, 3)))
+    if sum(counts) == 0:
+        counts[0] = 5
+    ids = g.permutation(np.repeat(np.arange(El, dtype=np.int32), counts))[:, None]
+    T = ids.shape[0]
+    _, offs, _, _ = oracle.permute(ids, 0, El)
+    x_perm = mi.random_bf16((T, H), seed=seed, tag=55)
+    w13 = mi.random_bf16((El, 2 * Is, H), seed=seed, tag=56, std=0.05)
+    w2 = mi.random_bf16((El, H, Is), seed=seed, tag=57, std=0.05)
+    runs = []
+    for _ in range(2):
+        y = moe.grouped_ffn(dev_bf16(x_perm), torch.from_numpy(offs).cuda(), dev_bf16(w13), dev_bf16(w2))
+        torch.cuda.synchronize()
+        runs.append(bf16_f64(host_bf16(y)[:T]))
+    ref = oracle.grouped_ffn(x_perm, offs, w13, w2)
+    assert_close_rel(runs[0], ref, what=f"random mix seed={seed} El={El} H={H} Is={Is} rows={counts}")
+    np.testing.assert_array_equal(runs[0], runs[1])
