@@ -339,8 +339,12 @@ def sample_tokens(cfg, ids, n=24, seed=0):
 
 
 @pytest.mark.parametrize("name", list(mi.CONFIGS))
-def test_layer_configs(oracle, name):
+@pytest.mark.parametrize("seed", SEEDS)
+def test_layer_configs(oracle, name, seed):
+    """The whole chain on every workload and three input seeds (the
+    config's own and the next two)."""
     cfg = mi.CONFIGS[name]
+    cfg = cfg.with_(seed=cfg.seed + seed)
     inp = mi.make_inputs(cfg)
     layer, out = layer_on_gpu(inp)
     rid, rw = oracle.route(inp.logits, cfg.k)
@@ -354,7 +358,7 @@ def test_layer_configs(oracle, name):
         sample_tokens(cfg, rid)
     ref = oracle.layer_tokens(inp.x, rid, rw, cfg.e0, cfg.E_l, inp.w13, inp.w2, toks, inp.sw13,
                               inp.sw2, cfg.shared_begin, cfg.shared_count)
-    assert_close_rel(bf16_f64(out[toks]), ref, what=name)
+    assert_close_rel(bf16_f64(out[toks]), ref, what=f"{name} seed+{seed}")
     # tokens with no local pair and no shared term are exactly zero
     local = ((rid >= cfg.e0) & (rid < cfg.e0 + cfg.E_l)).any(1)
     if cfg.shared:
