@@ -384,8 +384,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t *__restrict__ 
 // ---------------------------------------------------------------------------
 // Large-tile kernel (K a multiple of 64, at least 128): BMxBN tiles (BN counts
 // weight rows; a gated tile holds BN/2 gate rows and the BN/2 matching up
-// rows), 4 waves in a 2x2 grid, each wave (BM/2)x(BN/2) of 32x32x16 MFMA
-// blocks, accumulators in AGPRs.
+// rows), 8 waves (two per SIMD) in a WM x (8/WM) grid, each wave owning
+// (BM/WM)x(BN*WM/8) of 32x32x16 MFMA blocks, accumulators in AGPRs.
 //
 // Operands move L2 -> LDS with buffer loads that write LDS directly (no VGPR
 // staging) in BK=64 slices (128-byte row segments: whole L2 lines).  A
@@ -591,8 +591,9 @@ __device__ __forceinline__ TileCoord tile_coord(int64_t tile, const int32_t *__r
 // coalesced 16-byte vector per lane.
 
 // Work split of one launch over G persistent workgroups.  Tiles [0, dp) are
-// handed out whole, round robin: workgroups on one die then walk K in near
-// lockstep over shared panels, which is what keeps the die's L2 effective.
+// handed out whole, each die a contiguous run dealt round robin over its
+// workgroups: workgroups on one die then walk K in near lockstep over shared
+// panels, which is what keeps the die's L2 effective.
 // The K-slices of tiles [dp, T) are cut into G contiguous runs
 // ("stream-K"), so every workgroup gets the same number of slices; partial
 // sums are combined by the last contributor of each tile (small-row tiles,
@@ -657,7 +658,7 @@ struct TileClass {
     float *partials;
 };
 
-// One tile class (BMt x BNt tiles, WM x (4/WM) waves) of a grouped GEMM,
+// One tile class (BMt x BNt tiles, WM x (8/WM) waves) of a grouped GEMM,
 // processed by every workgroup of the persistent grid; `ring` is the
 // workgroup's LDS (at least the class's ring size).  Pointers are restrict
 // parameters so that the inlined body keeps the no-alias facts of kernel
