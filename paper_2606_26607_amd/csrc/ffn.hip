@@ -54,14 +54,28 @@ constexpr int SPLIT_MIN_NK = 128;
 // (prefill leftovers of 65-128 rows, which would otherwise take two 64-row
 // tiles that each stream the expert's weights).  Each has a largest expert
 // it takes whole and the time of one of its K-slices relative to a
-// large-tile K-slice (measured: a small-row slice is bound by its weight
-// rows, a 256-row one by MFMA), as the fraction cost_num / 20.
+// large-tile K-slice, in twentieths: cost_num for a slice of a stream-K
+// piece, its share of the piece's partial-sum traffic included, and
+// whole_num for a slice of a tile run whole (measured on the prefill
+// workloads: a small-row slice is bound by its weight rows, a 256-row one by
+// MFMA).  Every tile also pays a prologue (the first operand slices arrive
+// from memory) and an epilogue (the output leaves through LDS): about
+// LARGE_OVH large slices for a large tile, SMALL_WHOLE_OVH twentieths of one
+// for a small-row tile run whole.
 constexpr int SMALL_COST_DEN = 20;
 struct SmallKind {
-    int rows, max_rows, cost_num;
+    int rows, max_rows, cost_num, whole_num;
 };
-constexpr SmallKind SMALL64{64, 96, 11};
-constexpr SmallKind SMALL128{128, 128, 11};
+constexpr SmallKind SMALL64{64, 96, 11, 7};
+constexpr SmallKind SMALL128{128, 128, 11, 13};
+constexpr int LARGE_OVH = 5, SMALL_WHOLE_OVH = 50;
+
+// Whole small-row tiles of nk K-slices that fit in the time of one large tile
+// (nk < 2^25: operands are addressed with 32-bit byte offsets).
+__device__ __forceinline__ int whole_fit(int nk, int whole_num)
+{
+    return SMALL_COST_DEN * (nk + LARGE_OVH) / (whole_num * nk + SMALL_WHOLE_OVH);
+}
 
 // Block-wide exclusive scan of one value per thread (blocks of whole waves,
 // at most 1024 threads); returns the exclusive prefix and writes the total
@@ -129,26 +143,30 @@ struct SchedShape {
 // Estimated time of one GEMM, in units of one large-tile K-slice on one
 // workgroup, for tl large and ts small-row tiles of nk K-slices: rounds of
 // large tiles (or their stream-K share, with its partial-sum traffic, when
-// there are fewer tiles than workgroups and K is long), plus
-// the small-row share (cost_num / SMALL_COST_DEN of a large slice per
-// small-row slice) unless it fits on the workgroups the large tiles leave
-// idle in their last round.
-__device__ __forceinline__ float gemm_cost(int64_t tl, int64_t ts, int nk, int grid, int cost_num, bool tall)
+// there are fewer tiles than workgroups and K is long), plus the
+// small-row share (cost_num / SMALL_COST_DEN of a large slice per small-row
+// slice) unless it fits on the workgroups the large tiles leave idle in their
+// last round, whole or in stream-K pieces.
+__device__ __forceinline__ float gemm_cost(int64_t tl, int64_t ts, int nk, int grid, int cost_num, int wfit,
+                                           bool tall)
 {
     const float t = (float)tl, g = (float)grid;
     const bool split = tl < grid && nk >= SPLIT_MIN_NK;
-    const int rest = (int)(tl % grid);
+    const int64_t rounds = tl / grid;
+    const int rest = (int)(tl - rounds * grid);
     float c = 0.f;
     if (tl > 0 && split) {
         c = 1.25f * t * (float)nk / g;
     } else if (tl > 0) {
         // a last round with a fraction f of the workgroups busy takes about
         // 0.6 + 0.4 f of a full one (less contention for L2 and HBM)
-        c = (float)((tl - rest) / grid) * (float)nk;
+        c = (float)rounds * (float)nk;
         if (rest) c += (0.6f + 0.4f * (float)rest / g) * (float)nk;
     }
-    const int idle = rest ? grid - rest : 0;
-    if (!split && idle && cost_num * ts <= (int64_t)SMALL_COST_DEN * idle) return c;
+    const int idle = (rest && !split) ? grid - rest : 0;
+    // stream-K pieces or whole small-row tiles on the idle workgroups
+    if (idle && cost_num * ts <= (int64_t)SMALL_COST_DEN * idle) return c;
+    if (idle && ts <= (int64_t)idle * wfit) return c;
     // 128-row tiles only on idle workgroups: run over the whole grid they are
     // cut into many stream-K pieces whose larger partials the last
     // contributor reads back alone (measured slower than 64-row tiles there)
@@ -251,8 +269,10 @@ __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restric
             float total = 0.f;
             const int nt[2] = {sh.nt_gu, sh.nt_dn}, nk[2] = {sh.nk_gu, sh.nk_dn};
             for (int gi = 0; gi < 2; ++gi) {
-                const float c64 = gemm_cost(tl * nt[gi], t64 * nt[gi], nk[gi], sh.grid, SMALL64.cost_num, false);
-                const float c128 = gemm_cost(tl * nt[gi], t128 * nt[gi], nk[gi], sh.grid, SMALL128.cost_num, true);
+                const float c64 = gemm_cost(tl * nt[gi], t64 * nt[gi], nk[gi], sh.grid, SMALL64.cost_num,
+                                            whole_fit(nk[gi], SMALL64.whole_num), false);
+                const float c128 = gemm_cost(tl * nt[gi], t128 * nt[gi], nk[gi], sh.grid, SMALL128.cost_num,
+                                             whole_fit(nk[gi], SMALL128.whole_num), true);
                 if (c128 < c64) bits |= 1 << gi;
                 total += c128 < c64 ? c128 : c64;
             }
@@ -591,26 +611,29 @@ __device__ __forceinline__ TileCoord tile_coord(int64_t tile, const int32_t *__r
 // coalesced 16-byte vector per lane.
 
 // Work split of one launch over G persistent workgroups.  Tiles [0, dp) are
-// handed out whole, each die a contiguous run dealt round robin over its
-// workgroups: workgroups on one die then walk K in near lockstep over shared
-// panels, which is what keeps the die's L2 effective.
+// handed out whole: large tiles each die a contiguous run dealt round robin
+// over its workgroups (workgroups on one die then walk K in near lockstep
+// over shared panels, which is what keeps the die's L2 effective), small-row
+// tiles round robin over the class's group.
 // The K-slices of tiles [dp, T) are cut into G contiguous runs
 // ("stream-K"), so every workgroup gets the same number of slices; partial
 // sums are combined by the last contributor of each tile (small-row tiles,
 // whose partials are small) or by a separate reduction kernel (large tiles:
 // one workgroup reading several 256 KB partials would be bound by what one
-// CU can pull from memory).  Stream-K takes all of the weight-streaming
-// small-row tiles, and large tiles only in a launch of fewer tiles than
-// workgroups with a long K (e.g. one expert's down projection).
+// CU can pull from memory).  Stream-K takes the weight-streaming small-row
+// tiles unless they run whole, and large tiles only in a launch of fewer
+// tiles than workgroups with a long K (e.g. one expert's down projection).
+enum SplitMode { SPLIT_AUTO, SPLIT_ALWAYS, SPLIT_NEVER };
 struct WorkSplit {
     int64_t T, dp, iters;  // tiles, whole tiles, K-slices in the stream-K part
     int nk, G, Gsk;        // slices per tile, workgroups, workgroups in the stream-K part
-    __device__ WorkSplit(int64_t total, int nk_, int g, bool split_always) : T(total), nk(nk_), G(g)
+    __device__ WorkSplit(int64_t total, int nk_, int g, SplitMode mode) : T(total), nk(nk_), G(g)
     {
         // splitting pays only when a tile has many slices and there are too
         // few tiles to fill the grid: each split piece moves its fp32 partial
         // sums through memory, and split pieces lose the lockstep walk over K
-        dp = (split_always || (T < G && nk >= SPLIT_MIN_NK)) ? 0 : T;
+        const bool split = mode == SPLIT_ALWAYS || (mode == SPLIT_AUTO && T < G && nk >= SPLIT_MIN_NK);
+        dp = split ? 0 : T;
         iters = (T - dp) * nk;
         // every stream-K workgroup gets at least one slice, so the workgroups
         // that meet a tile are exactly a consecutive range
@@ -674,7 +697,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                                            const uint16_t *__restrict__ Wsh, int up_off,
                                            uint16_t *__restrict__ C, uint16_t *__restrict__ Csh,
                                            int32_t *__restrict__ tile_cnt, float *__restrict__ partials,
-                                           int v, int grp_size)
+                                           int v, int grp_size, bool deal)
 {
     constexpr int A_STAGE = BMt * CPR, B_STAGE = BNt * CPR;  // 16-byte chunks per slot
     constexpr int A_INS = BMt / RPI / GEMM_WAVES, B_INS = BNt / RPI / GEMM_WAVES;
@@ -699,8 +722,10 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
     const int n_tiles = (N + OUTN - 1) / OUTN;
     const int nk = K / BIG_BK;
     // the class runs on grp_size workgroups; this one is number v of them
-    // (negative: not one of them)
-    const WorkSplit ws((int64_t)tile_prefix[ne] * n_tiles, nk, grp_size, TAIL);
+    // (negative: not one of them).  deal (small-row class only): whole tiles
+    // dealt round robin over the group instead of stream-K
+    const WorkSplit ws((int64_t)tile_prefix[ne] * n_tiles, nk, grp_size,
+                       TAIL ? (deal ? SPLIT_NEVER : SPLIT_ALWAYS) : SPLIT_AUTO);
     if (ws.T == 0 || v < 0 || v >= grp_size) return;
     // This lane's chunk within a DMA instruction: row lane/CPR of the
     // instruction's rows, LDS position lane%CPR, global chunk
@@ -1012,8 +1037,12 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
     // site keeps the kernel's register allocation to a single copy of the
     // pipeline.
     int64_t n_dp = 0, t0 = 0;
-    const int P = ws.G / 8;
-    if (ws.dp > 0) {
+    int P = ws.G / 8;
+    if (ws.dp > 0 && TAIL) {
+        P = grp_size;
+        n_dp = v < ws.dp ? (ws.dp - 1 - v) / P + 1 : 0;
+        t0 = v;
+    } else if (ws.dp > 0) {
         const int d = v / P, u = v % P;
         const int64_t lo = ws.dp * d / 8, hi = ws.dp * (d + 1) / 8;
         n_dp = u < hi - lo ? (hi - lo - 1 - u) / P + 1 : 0;
@@ -1056,20 +1085,27 @@ constexpr int SLOT_SMALL = (SMALL128.rows / SMALL_WM / 32) * (BIGN / (GEMM_WAVES
 constexpr int SLOT_BIG = (BIGM / BIG_WM / 32) * (BIGN / (GEMM_WAVES / BIG_WM) / 32) * 16 * GEMM_THREADS;
 
 // Where the small-row class runs: on the workgroups the large tiles leave
-// idle in their last round when its work fits there (its slices, weighted
-// cost_num / SMALL_COST_DEN, add up to at most one large tile per idle
-// workgroup), else on all workgroups after their large tiles.  vx is this
-// workgroup's die-major id (G/8 consecutive ids per die).  Returns this
-// workgroup's number in the small class's group (negative: not in it) and
-// the group size.
+// idle in their last round when its work fits there, else on all workgroups
+// after their large tiles.  On the idle ones it runs stream-K when its
+// slices, at cost_num / SMALL_COST_DEN of a large slice each, add up to at
+// most one large tile per idle workgroup; failing that, its tiles are dealt
+// whole, round robin, when as many fit there as take the time of one large
+// tile each (whole tiles pay no partial sums, which is what makes them fit
+// where the pieces do not).  vx is this workgroup's die-major id (G/8 consecutive ids per
+// die).  Returns this workgroup's number in the small class's group
+// (negative: not in it), the group size and whether whole tiles are dealt.
 struct SmallGroup {
     int v, size;
+    bool deal;
 };
 
-__device__ __forceinline__ SmallGroup small_group(int64_t tl, int64_t ts, int nk, int G, int cost_num, int vx)
+__device__ __forceinline__ SmallGroup small_group(int64_t tl, int64_t ts, int nk, int G, SmallKind kind, int vx)
 {
     const bool large_dp = !(tl < G && nk >= SPLIT_MIN_NK);
-    if (large_dp && tl > 0 && tl % G != 0 && cost_num * ts <= (int64_t)SMALL_COST_DEN * (G - tl % G)) {
+    const int idle = tl % G ? G - (int)(tl % G) : 0;
+    const bool pieces = kind.cost_num * ts <= (int64_t)SMALL_COST_DEN * idle;
+    const bool whole = !pieces && ts <= (int64_t)idle * whole_fit(nk, kind.whole_num);
+    if (large_dp && idle && (pieces || whole)) {
         // die d holds c_d = tl*(d+1)/8 - tl*d/8 whole tiles; with R rounds
         // (the busiest die's), its workgroups u < c_d - (R-1)*P are busy in
         // the last round and the others idle.  Number the idle ones die by
@@ -1084,9 +1120,9 @@ __device__ __forceinline__ SmallGroup small_group(int64_t tl, int64_t ts, int nk
             if (dd == d && u >= busy) mine = before + (u - busy);
             before += P - busy;
         }
-        return SmallGroup{mine, before};
+        return SmallGroup{mine, before, whole};
     }
-    return SmallGroup{vx, G};
+    return SmallGroup{vx, G, false};
 }
 
 // One grouped GEMM launch: the large-tile class (256-row tiles) and the
@@ -1101,27 +1137,29 @@ void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
 {
     __shared__ uint4 ring[BIG_RING];
     constexpr int OUTN = GATED ? BIGN / 2 : BIGN;
-    const int64_t n_tiles = (g.N + OUTN - 1) / OUTN;
-    const bool tall = small.tile_prefix[g.ne + 1] == SMALL128.rows;  // uniform
     // die-major id: the hardware deals workgroups to the 8 dies round robin
     const int vx = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
-    const SmallGroup sg = small_group((int64_t)large.tile_prefix[g.ne] * n_tiles,
-                                      (int64_t)small.tile_prefix[g.ne] * n_tiles, g.K / BIG_BK, gridDim.x,
-                                      tall ? SMALL128.cost_num : SMALL64.cost_num, vx);
     gemm_class<BIGM, BIGN, GATED, BIG_WM, false, A_SLOTS, B_SLOTS>(
         ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, large.tile_prefix, g.El, g.ne, g.cap,
         g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh, large.tile_cnt,
-        large.partials, vx, gridDim.x);
+        large.partials, vx, gridDim.x, false);
+    // the small class's group, worked out only now (nothing of it stays
+    // live through the large tiles)
+    const int64_t n_tiles = (g.N + OUTN - 1) / OUTN;
+    const bool tall = small.tile_prefix[g.ne + 1] == SMALL128.rows;  // uniform
+    const SmallGroup sg = small_group((int64_t)large.tile_prefix[g.ne] * n_tiles,
+                                      (int64_t)small.tile_prefix[g.ne] * n_tiles, g.K / BIG_BK, gridDim.x,
+                                      tall ? SMALL128 : SMALL64, vx);
     if (tall)
         gemm_class<SMALL128.rows, BIGN, GATED, SMALL_WM, true, S128_ASL, S128_BSL>(
             ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, small.tile_prefix, g.El, g.ne, g.cap,
             g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh,
-            small.tile_cnt, small.partials, sg.v, sg.size);
+            small.tile_cnt, small.partials, sg.v, sg.size, sg.deal);
     else
         gemm_class<SMALL64.rows, BIGN, GATED, SMALL_WM, true, SA_SLOTS, SB_SLOTS>(
             ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, small.tile_prefix, g.El, g.ne, g.cap,
             g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh,
-            small.tile_cnt, small.partials, sg.v, sg.size);
+            small.tile_cnt, small.partials, sg.v, sg.size, sg.deal);
 }
 
 // Combines the split-K partials of the large-tile class after its GEMM
@@ -1144,7 +1182,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void splitk_reduce(const int32_t *__r
     constexpr int JJ = GATED ? NB / 2 : NB;  // output blocks per wave row
     const int n_tiles = (N + OUTN - 1) / OUTN;
     const int nk = K / BIG_BK;
-    const WorkSplit ws((int64_t)tile_prefix[ne] * n_tiles, nk, G, false);
+    const WorkSplit ws((int64_t)tile_prefix[ne] * n_tiles, nk, G, SPLIT_AUTO);
     const int64_t items = (ws.T - ws.dp) * MB * JJ;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
