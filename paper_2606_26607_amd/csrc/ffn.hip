@@ -72,7 +72,7 @@ constexpr int LARGE_OVH = 5, SMALL_WHOLE_OVH = 50;
 
 // Whole small-row tiles of nk K-slices that fit in the time of one large tile
 // (nk < 2^25: operands are addressed with 32-bit byte offsets).
-__device__ __forceinline__ int whole_fit(int nk, int whole_num)
+__host__ __device__ __forceinline__ int whole_fit(int nk, int whole_num)
 {
     return SMALL_COST_DEN * (nk + LARGE_OVH) / (whole_num * nk + SMALL_WHOLE_OVH);
 }
@@ -98,61 +98,116 @@ __device__ __forceinline__ int32_t block_exscan(int32_t v, int32_t *wsum, int32_
     return before + incl - v;
 }
 
-// The same for three values at once (independent shuffle chains run
-// interleaved); totals to tot[0..2].
-__device__ __forceinline__ int3 block_exscan3(int3 v, int32_t (*wsum)[3], int32_t *tot)
+// The same for N values at once (independent shuffle chains run
+// interleaved), in place; totals to tot[0..N-1].
+template <int N>
+__device__ __forceinline__ void block_exscan_n(int32_t (&v)[N], int32_t (*wsum)[N], int32_t *tot)
 {
     const int e = threadIdx.x, lane = e & 63, wv = e >> 6;
-    int3 incl = v;
+    int32_t incl[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) incl[i] = v[i];
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
-        const int ox = __shfl_up(incl.x, off, 64), oy = __shfl_up(incl.y, off, 64), oz = __shfl_up(incl.z, off, 64);
+        int32_t o[N];
+#pragma unroll
+        for (int i = 0; i < N; ++i) o[i] = __shfl_up(incl[i], off, 64);
         if (lane >= off) {
-            incl.x += ox;
-            incl.y += oy;
-            incl.z += oz;
+#pragma unroll
+            for (int i = 0; i < N; ++i) incl[i] += o[i];
         }
     }
     if (lane == 63) {
-        wsum[wv][0] = incl.x;
-        wsum[wv][1] = incl.y;
-        wsum[wv][2] = incl.z;
+#pragma unroll
+        for (int i = 0; i < N; ++i) wsum[wv][i] = incl[i];
     }
     __syncthreads();
-    int3 before = make_int3(0, 0, 0);
-    for (int i = 0; i < wv; ++i) {
-        before.x += wsum[i][0];
-        before.y += wsum[i][1];
-        before.z += wsum[i][2];
+    int32_t before[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) before[i] = 0;
+    for (int w = 0; w < wv; ++w) {
+#pragma unroll
+        for (int i = 0; i < N; ++i) before[i] += wsum[w][i];
     }
     if (e == (int)blockDim.x - 1) {
-        tot[0] = before.x + incl.x;
-        tot[1] = before.y + incl.y;
-        tot[2] = before.z + incl.z;
+#pragma unroll
+        for (int i = 0; i < N; ++i) tot[i] = before[i] + incl[i];
     }
     __syncthreads();
-    return make_int3(before.x + incl.x - v.x, before.y + incl.y - v.y, before.z + incl.z - v.z);
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = before[i] + incl[i] - v[i];
 }
 
 // Shape of both GEMMs as the schedule's cost model sees it: output tiles per
 // m-tile (n_tiles) and K-slices per tile (nk).
 struct SchedShape {
     int nt_gu, nk_gu, nt_dn, nk_dn, grid;
+    int wfit[2][2];      // [GEMM][64- or 128-row tiles]: whole_fit of the GEMM's nk
+    float whole[2][2];   // ... and whole_time
 };
+
+// Where a GEMM's ts small-row tiles run next to its tl large tiles on a grid
+// of G persistent workgroups:
+//   SM_PIECES_IDLE: stream-K over the workgroups the large tiles leave idle
+//     in their last round, when its slices (cost_num / SMALL_COST_DEN of a
+//     large slice each) add up to at most one large tile per idle workgroup;
+//   SM_WHOLE_IDLE: else whole tiles dealt round robin over the idle
+//     workgroups, when as many fit there as take one large tile's time each
+//     (whole tiles pay no partial sums);
+//   SM_WHOLE_ALL: else, with at most one tile per workgroup, whole tiles
+//     dealt over all workgroups (the idle ones first) after their large
+//     tiles, when one whole tile takes less than a stream-K share plus the
+//     fixed cost of a stream-K piece (prologue and partial sums);
+//   SM_PIECES_ALL: else stream-K over all workgroups after their large tiles.
+// extra = what the small-row work adds to the large tiles' rounds, in units
+// of one large-tile K-slice.
+enum SmallMode { SM_PIECES_IDLE, SM_WHOLE_IDLE, SM_WHOLE_ALL, SM_PIECES_ALL };
+
+// x / g for x >= 0, in 32 bits whenever x fits (it always does in practice;
+// a 64-bit division is a long instruction sequence on the GPU)
+__device__ __forceinline__ int64_t div_g(int64_t x, int g)
+{
+    return x <= 0x7fffffff ? (int64_t)((uint32_t)x / (uint32_t)g) : x / g;
+}
+constexpr float PIECE_OVH = 8.0f;  // fixed cost of a stream-K piece, in large slices
+struct SmallPlan {
+    SmallMode mode;
+    int idle;
+    float extra;
+};
+
+// Time of one whole small-row tile of nk K-slices, in large slices.
+__host__ __device__ __forceinline__ float whole_time(int nk, int whole_num)
+{
+    return (float)(whole_num * nk + SMALL_WHOLE_OVH) / (float)SMALL_COST_DEN;
+}
+
+// The per-GEMM constants of the plan: wfit = whole_fit(nk, kind.whole_num),
+// whole = whole_time(nk, kind.whole_num) (worked out once, on the host for
+// the schedule).
+__device__ __forceinline__ SmallPlan small_plan(int64_t tl, int64_t ts, int nk, int G, int cost_num, int wfit,
+                                                float whole)
+{
+    const bool large_dp = !(tl < G && nk >= SPLIT_MIN_NK);
+    const int rest = (int)(tl - div_g(tl, G) * G);
+    const int idle = (large_dp && rest) ? G - rest : 0;
+    if (ts == 0) return SmallPlan{SM_PIECES_ALL, idle, 0.f};
+    if (idle && (int64_t)cost_num * ts <= (int64_t)SMALL_COST_DEN * idle) return SmallPlan{SM_PIECES_IDLE, idle, 0.f};
+    if (idle && ts <= (int64_t)idle * wfit) return SmallPlan{SM_WHOLE_IDLE, idle, 0.f};
+    const float pieces = (float)cost_num / (float)SMALL_COST_DEN * (float)ts * (float)nk / (float)G;
+    if (ts <= G && whole < pieces + PIECE_OVH) return SmallPlan{SM_WHOLE_ALL, idle, ts > idle ? whole : 0.f};
+    return SmallPlan{SM_PIECES_ALL, idle, pieces};
+}
 
 // Estimated time of one GEMM, in units of one large-tile K-slice on one
 // workgroup, for tl large and ts small-row tiles of nk K-slices: rounds of
 // large tiles (or their stream-K share, with its partial-sum traffic, when
-// there are fewer tiles than workgroups and K is long), plus the
-// small-row share (cost_num / SMALL_COST_DEN of a large slice per small-row
-// slice) unless it fits on the workgroups the large tiles leave idle in their
-// last round, whole or in stream-K pieces.
-__device__ __forceinline__ float gemm_cost(int64_t tl, int64_t ts, int nk, int grid, int cost_num, int wfit,
-                                           bool tall)
+// there are fewer tiles than workgroups and K is long) ...
+__device__ __forceinline__ float large_cost(int64_t tl, int nk, int grid)
 {
     const float t = (float)tl, g = (float)grid;
     const bool split = tl < grid && nk >= SPLIT_MIN_NK;
-    const int64_t rounds = tl / grid;
+    const int64_t rounds = div_g(tl, grid);
     const int rest = (int)(tl - rounds * grid);
     float c = 0.f;
     if (tl > 0 && split) {
@@ -163,55 +218,63 @@ __device__ __forceinline__ float gemm_cost(int64_t tl, int64_t ts, int nk, int g
         c = (float)rounds * (float)nk;
         if (rest) c += (0.6f + 0.4f * (float)rest / g) * (float)nk;
     }
-    const int idle = (rest && !split) ? grid - rest : 0;
-    // stream-K pieces or whole small-row tiles on the idle workgroups
-    if (idle && cost_num * ts <= (int64_t)SMALL_COST_DEN * idle) return c;
-    if (idle && ts <= (int64_t)idle * wfit) return c;
-    // 128-row tiles only on idle workgroups: run over the whole grid they are
-    // cut into many stream-K pieces whose larger partials the last
-    // contributor reads back alone (measured slower than 64-row tiles there)
-    if (tall && ts > 0) return 3.0e38f;
-    return c + (float)cost_num / (float)SMALL_COST_DEN * (float)ts * (float)nk / g;
+    return c;
 }
 
-constexpr int NC_SCHED = 10;  // schedule candidates (one thread each)
+// ... plus what its small-row work adds (small_plan); c = large_cost(tl, ...).
+__device__ __forceinline__ float gemm_cost(float c, int64_t tl, int64_t ts, int nk, int grid, int cost_num,
+                                           int wfit, float whole, bool tall)
+{
+    const SmallPlan p = small_plan(tl, ts, nk, grid, cost_num, wfit, whole);
+    // 128-row tiles not in stream-K pieces over the whole grid: there the
+    // last contributor of each tile reads back larger partials alone
+    // (measured slower than 64-row tiles)
+    if (tall && ts > 0 && p.mode == SM_PIECES_ALL) return 3.0e38f;
+    return c + p.extra;
+}
 
-// Tile schedule of the grouped FFN.  An expert's rows [a, b) are cut at
-// split[e]: rows [a, split) go to the large-tile class (m-tiles of bm rows),
-// rows [split, b) to the small-row class.  An expert with at most smax rows
-// (96 or 128) is all small.  A larger one may give its leftover rows after
-// whole large tiles to the small class: a nearly empty large tile costs as
-// much as a full one, while small-row tiles are split evenly over the grid.
-// smax and which leftovers move (none, or those of at most 32, 64, 96 or 128
-// rows) are chosen for the lowest estimated time of both GEMMs (gemm_cost);
-// each GEMM then takes the small tile height (64 or 128 rows) that is
-// cheaper for it.  small = false disables the small class.
-//   pre[e] / pre_gu[e] / pre_dn[e] = m-tiles of the large class / of the
-//   small class of the gate-up and of the down GEMM for the experts before
-//   e, [ne] = totals (ne experts: the routed ones, then the shared one if the
-//   call has shared rows), pre_gu[ne + 1] / pre_dn[ne + 1] = the GEMM's
-//   small tile height.
+constexpr int NC_SCHED = 10;  // base candidates: smax 96 or 128 x leftover threshold 0 .. 128
+constexpr int ND_SCHED = 8;   // ... each also with up to 7 more m-tiles of the largest expert moved
+
+// Tile schedule of the grouped FFN, chosen for each GEMM on its own.  An
+// expert's rows [a, b) are cut at split[e]: rows [a, split) go to the
+// large-tile class (m-tiles of bm rows), rows [split, b) to the small-row
+// class.  An expert with at most smax rows (96 or 128) is all small.  A
+// larger one may give its leftover rows after whole large tiles to the small
+// class (none, or those of at most 32, 64, 96 or 128 rows): a nearly empty
+// large tile costs as much as a full one, while small-row work fits where the
+// large tiles leave workgroups idle.  The largest expert may also give its
+// last D = 1 .. 7 large m-tiles, only where that saves a round of large
+// tiles (a sparse last round costs about as much as a full one): the fewest
+// such D is a candidate beside D = 0.  Each GEMM takes the candidate (smax,
+// threshold, D) and small tile height (64 or 128 rows) of the lowest
+// estimated time (gemm_cost); small = false disables the small class.
+//   pre_l[g][e] / pre_s[g][e] = m-tiles of the large / small class of GEMM g
+//   (0 gate-up, 1 down) for the experts before e, [ne] = totals (ne experts:
+//   the routed ones, then the shared one if the call has shared rows),
+//   pre_s[g][ne + 1] = the GEMM's small tile height; split[g][e] its cut.
 // Also clears the split-K tile counters (no memset node is needed, so the
 // chain stays graph-capturable).
+struct SchedOut {
+    int32_t *pre_l[2], *pre_s[2], *split[2];
+};
+
 __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restrict__ offsets, int El,
                                                         int64_t cap, int64_t shared_rows, int bm, bool small,
-                                                        SchedShape sh, int32_t *__restrict__ pre,
-                                                        int32_t *__restrict__ pre_gu,
-                                                        int32_t *__restrict__ pre_dn,
-                                                        int32_t *__restrict__ split,
+                                                        SchedShape sh, SchedOut out,
                                                         int32_t *__restrict__ counters, int64_t n_counters)
 {
     constexpr int NT = NC_SCHED / 2;  // leftover thresholds 0, 32, 64, 96, 128
-    constexpr int NC = NC_SCHED;      // candidates: (smax 96 or 128, threshold)
-    __shared__ int32_t wsum[16][3];
-    __shared__ int32_t vals[1024][3 * NC];  // per expert: its tiles of every candidate
+    constexpr int NC = NC_SCHED;
+    __shared__ int32_t wsum[16][4];
+    __shared__ int32_t vals[1024][3 * NC + 1];  // per expert: its tiles of every base candidate, its rows
     __shared__ int32_t tot[3 * NC];
-    __shared__ int32_t ptot[3];
-    __shared__ int32_t chosen;
-    __shared__ float cost[NC];
-    __shared__ int32_t tall[NC];  // bit 0: gate-up takes 128-row tiles, bit 1: down does
-    // one thread per expert, whole waves (the launch sizes the block)
-    const int e = threadIdx.x;
+    __shared__ int32_t ptot[4];
+    __shared__ int32_t big[2];  // the largest expert and its rows
+    __shared__ unsigned long long kmin[2];
+    // one thread per expert, at least two waves, whole waves (the launch
+    // sizes the block)
+    const int e = threadIdx.x, lane = e & 63, wv = e >> 6;
     for (int64_t i = e; i < n_counters; i += blockDim.x) counters[i] = 0;
     // experts: the El routed ones, then the shared one when there are shared
     // rows; rows fit int32 (cap + shared rows < 2^31 is checked on the host)
@@ -222,16 +285,16 @@ __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restric
         const int32_t b = (int32_t)expert_end(offsets, El, cap, shared_rows, e);
         n = b > a ? b - a : 0;
     }
-    // for candidate c (smax = c / NT ? 128 : 96, threshold 32 * (c % NT)):
+    // for base candidate c (smax = c / NT ? 128 : 96, threshold 32 * (c % NT)):
     // large m-tiles (x) and the rows that go to the small class (y)
-    const int32_t whole = n / bm, rest = n - whole * bm;
-    auto rows_for = [&](int c) {
+    auto rows_for = [&](int32_t rows, int c) {
+        const int32_t whole = rows / bm, rest = rows - whole * bm;
         const int smax = c / NT ? SMALL128.max_rows : SMALL64.max_rows;
         const int th = 32 * (c % NT);
         int2 r = make_int2(0, 0);
-        if (n > 0 && small && n <= smax) {
-            r.y = n;
-        } else if (n > 0) {
+        if (rows > 0 && small && rows <= smax) {
+            r.y = rows;
+        } else if (rows > 0) {
             if (small && rest > 0 && rest <= th) {
                 r.x = whole;
                 r.y = rest;
@@ -241,72 +304,128 @@ __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restric
         }
         return r;
     };
-    int cand = 0, kinds = 0;
+    // ... and with D more m-tiles of the largest expert moved
+    auto rows_moved = [&](int32_t rows, int2 r, int D) {
+        if (D > 0 && r.x > 0) {
+            r.x = r.x > D ? r.x - D : 0;
+            r.y = rows - r.x * bm;
+        }
+        return r;
+    };
+    int cand[2] = {0, 0}, kinds = 0, L = -1;
     if (small) {
-        // class totals of every candidate: large m-tiles, small m-tiles of 64
-        // and of 128 rows; each expert writes its row, one thread per column
-        // sums it (a few dozen experts typically: cheaper than shuffle trees)
+        // class totals of every base candidate: large m-tiles, small m-tiles
+        // of 64 and of 128 rows; each expert writes its row, one thread per
+        // column sums it (a few dozen experts typically: cheaper than
+        // shuffle trees)
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
-            const int2 r = rows_for(c);
+            const int2 r = rows_for(n, c);
             vals[e][3 * c] = r.x;
             vals[e][3 * c + 1] = (r.y + 63) / 64;
             vals[e][3 * c + 2] = (r.y + 127) / 128;
         }
+        vals[e][3 * NC] = n;
         __syncthreads();
         if (e < 3 * NC) {
             int32_t sum = 0;
             for (int i = 0; i < ne; ++i) sum += vals[i][e];
             tot[e] = sum;
-        }
-        __syncthreads();
-        // candidate c's estimate on thread c (each GEMM with its cheaper
-        // height; ties: 64 rows), the cheapest candidate on thread 0 (ties:
-        // smax 96, then fewer moves)
-        if (e < NC) {
-            const int64_t tl = tot[3 * e], t64 = tot[3 * e + 1], t128 = tot[3 * e + 2];
-            int bits = 0;
-            float total = 0.f;
-            const int nt[2] = {sh.nt_gu, sh.nt_dn}, nk[2] = {sh.nk_gu, sh.nk_dn};
-            for (int gi = 0; gi < 2; ++gi) {
-                const float c64 = gemm_cost(tl * nt[gi], t64 * nt[gi], nk[gi], sh.grid, SMALL64.cost_num,
-                                            whole_fit(nk[gi], SMALL64.whole_num), false);
-                const float c128 = gemm_cost(tl * nt[gi], t128 * nt[gi], nk[gi], sh.grid, SMALL128.cost_num,
-                                             whole_fit(nk[gi], SMALL128.whole_num), true);
-                if (c128 < c64) bits |= 1 << gi;
-                total += c128 < c64 ? c128 : c64;
+        } else if (e == 3 * NC) {
+            // the largest expert (ties: the lowest index), none when no
+            // expert has rows
+            int32_t m = 0, at = -1;
+            for (int i = 0; i < ne; ++i) {
+                const int32_t r = vals[i][3 * NC];
+                if (r > m) {
+                    m = r;
+                    at = i;
+                }
             }
-            cost[e] = total;
-            tall[e] = bits;
+            big[0] = at;
+            big[1] = m;
         }
         __syncthreads();
-        if (e == 0) {
-            int b = 0;
-            for (int c = 1; c < NC; ++c)
-                if (cost[c] < cost[b]) b = c;
-            chosen = b;
+        L = big[0];
+        // Candidates of GEMM gi on lanes 0 .. 19 of wave gi: base
+        // candidate c = t / 2 (t = lane) with D = 0 (even t) or with the
+        // fewest moves D that save a round of large tiles (odd t; none where
+        // that takes more than ND_SCHED - 1 moves or more m-tiles than the
+        // largest expert has).  Each takes the cheaper small tile height
+        // (ties: 64 rows).  Its key is the cost's bits (non-negative floats
+        // order as integers), then the candidate as c * ND_SCHED + D (ties:
+        // the lowest: smax 96, then fewer moves), with the height in the
+        // lowest bit.
+        unsigned long long key = ~0ull;
+        const int gi = wv, t = lane;
+        if (wv < 2 && t < 2 * NC) {
+            const int c = t / 2;
+            const int nt = gi ? sh.nt_dn : sh.nt_gu, nk = gi ? sh.nk_dn : sh.nk_gu, g = sh.grid;
+            const int wf64 = sh.wfit[gi][0], wf128 = sh.wfit[gi][1];
+            const float wh64 = sh.whole[gi][0], wh128 = sh.whole[gi][1];
+            const int64_t tl0 = tot[3 * c];
+            int64_t tl = tl0, t64 = tot[3 * c + 1], t128 = tot[3 * c + 2];
+            int D = 0;
+            bool valid = true;
+            if (t & 1) {
+                const int64_t r0 = div_g(tl0 * nt + g - 1, g);  // rounds of large tiles
+                const int xl = L >= 0 ? vals[L][3 * c] : 0;
+                const int64_t dmin = r0 >= 1 ? tl0 - div_g((r0 - 1) * g, nt) : 0;
+                valid = dmin >= 1 && dmin < ND_SCHED && dmin <= xl;
+                if (valid) {
+                    D = (int)dmin;
+                    const int2 r = rows_moved(big[1], make_int2(xl, 0), D);
+                    tl += r.x - xl;
+                    t64 += (r.y + 63) / 64 - vals[L][3 * c + 1];
+                    t128 += (r.y + 127) / 128 - vals[L][3 * c + 2];
+                }
+            }
+            if (valid) {
+                const float cl = large_cost(tl * nt, nk, g);
+                const float c64 = gemm_cost(cl, tl * nt, t64 * nt, nk, g, SMALL64.cost_num, wf64, wh64, false);
+                const float c128 = gemm_cost(cl, tl * nt, t128 * nt, nk, g, SMALL128.cost_num, wf128, wh128, true);
+                const float cmin = c128 < c64 ? c128 : c64;
+                key = ((unsigned long long)__float_as_uint(cmin) << 32) |
+                      ((unsigned)(c * ND_SCHED + D) << 1) | (c128 < c64);
+            }
+        }
+        // the cheapest candidate of each GEMM: a minimum over lanes 0 .. 31 of
+        // its wave
+        if (wv < 2) {
+#pragma unroll
+            for (int off = 1; off < 32; off <<= 1) {
+                const unsigned long long o = __shfl_xor(key, off, 64);
+                key = o < key ? o : key;
+            }
+            if (t == 0) kmin[gi] = key;
         }
         __syncthreads();
-        cand = chosen;
-        kinds = tall[cand];
+        for (int i = 0; i < 2; ++i) {
+            cand[i] = (int)((kmin[i] & 0xffffffffu) >> 1);
+            kinds |= (int)(kmin[i] & 1) << i;
+        }
     }
-    const int2 r = rows_for(cand);
-    if (split && e < ne) split[e] = a + (n - r.y);
-    const int h_gu = kinds & 1 ? SMALL128.rows : SMALL64.rows, h_dn = kinds & 2 ? SMALL128.rows : SMALL64.rows;
-    // prefixes of the large m-tiles and of both GEMMs' small m-tiles
-    const int3 x = block_exscan3(make_int3(r.x, (r.y + h_gu - 1) / h_gu, (r.y + h_dn - 1) / h_dn), wsum, ptot);
-    if (e < ne) pre[e] = x.x;
-    if (e == 0) pre[ne] = ptot[0];
-    if (pre_gu) {
-        if (e < ne) {
-            pre_gu[e] = x.y;
-            pre_dn[e] = x.z;
-        }
-        if (e == 0) {
-            pre_gu[ne] = ptot[1];
-            pre_dn[ne] = ptot[2];
-            pre_gu[ne + 1] = h_gu;
-            pre_dn[ne + 1] = h_dn;
+    int32_t v[4];
+    int h[2];
+    for (int gi = 0; gi < 2; ++gi) {
+        int2 r = rows_for(n, cand[gi] / ND_SCHED);
+        if (e == L) r = rows_moved(n, r, cand[gi] % ND_SCHED);
+        if (small && e < ne) out.split[gi][e] = a + (n - r.y);
+        h[gi] = kinds & (1 << gi) ? SMALL128.rows : SMALL64.rows;
+        v[2 * gi] = r.x;
+        v[2 * gi + 1] = (r.y + h[gi] - 1) / h[gi];
+    }
+    // prefixes of both GEMMs' large and small m-tiles
+    block_exscan_n<4>(v, wsum, ptot);
+    for (int gi = 0; gi < 2; ++gi) {
+        if (e < ne) out.pre_l[gi][e] = v[2 * gi];
+        if (e == 0) out.pre_l[gi][ne] = ptot[2 * gi];
+        if (small) {
+            if (e < ne) out.pre_s[gi][e] = v[2 * gi + 1];
+            if (e == 0) {
+                out.pre_s[gi][ne] = ptot[2 * gi + 1];
+                out.pre_s[gi][ne + 1] = h[gi];
+            }
         }
     }
 }
@@ -1033,18 +1152,16 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
     // tiles [dp*d/8, dp*(d+1)/8), dealt round robin over its workgroups, so
     // each die walks a run of consecutive tiles (m-tiles innermost: shared B
     // panels in its L2) and every die gets the same number of tiles (the
-    // workgroups idle in the last round are spread over all dies).  One call
-    // site keeps the kernel's register allocation to a single copy of the
+    // workgroups idle in the last round are spread over all dies); small-row
+    // tiles dealt whole form one run over the whole group.  One call site
+    // keeps the kernel's register allocation to a single copy of the
     // pipeline.
+    constexpr int NDIE = TAIL ? 1 : 8;
     int64_t n_dp = 0, t0 = 0;
-    int P = ws.G / 8;
-    if (ws.dp > 0 && TAIL) {
-        P = grp_size;
-        n_dp = v < ws.dp ? (ws.dp - 1 - v) / P + 1 : 0;
-        t0 = v;
-    } else if (ws.dp > 0) {
+    const int P = grp_size / NDIE;
+    if (ws.dp > 0) {
         const int d = v / P, u = v % P;
-        const int64_t lo = ws.dp * d / 8, hi = ws.dp * (d + 1) / 8;
+        const int64_t lo = ws.dp * d / NDIE, hi = ws.dp * (d + 1) / NDIE;
         n_dp = u < hi - lo ? (hi - lo - 1 - u) / P + 1 : 0;
         t0 = lo + u;
     }
@@ -1084,16 +1201,18 @@ constexpr int SLOT_SMALL = (SMALL128.rows / SMALL_WM / 32) * (BIGN / (GEMM_WAVES
                            GEMM_THREADS;
 constexpr int SLOT_BIG = (BIGM / BIG_WM / 32) * (BIGN / (GEMM_WAVES / BIG_WM) / 32) * 16 * GEMM_THREADS;
 
-// Where the small-row class runs: on the workgroups the large tiles leave
-// idle in their last round when its work fits there, else on all workgroups
-// after their large tiles.  On the idle ones it runs stream-K when its
-// slices, at cost_num / SMALL_COST_DEN of a large slice each, add up to at
-// most one large tile per idle workgroup; failing that, its tiles are dealt
-// whole, round robin, when as many fit there as take the time of one large
-// tile each (whole tiles pay no partial sums, which is what makes them fit
-// where the pieces do not).  vx is this workgroup's die-major id (G/8 consecutive ids per
-// die).  Returns this workgroup's number in the small class's group
-// (negative: not in it), the group size and whether whole tiles are dealt.
+// The small-row class's group of workgroups under small_plan: the idle ones
+// (SM_PIECES_IDLE, SM_WHOLE_IDLE), or all of them (SM_WHOLE_ALL with the
+// idle ones numbered first, SM_PIECES_ALL in die-major order).  The
+// workgroups the large tiles leave idle in their last round are found from
+// the large tiles' die-balanced deal.  Stream-K members are numbered die by
+// die (consecutive slices of a tile then share a die's L2); members that are
+// dealt whole tiles are numbered across the dies in turn, so that fewer tiles
+// than members still spread over all dies (on a few dies they would pull
+// every weight panel through those dies' links).  vx is this workgroup's
+// die-major id (G/8 consecutive ids per die).  Returns this workgroup's
+// number in the group (negative: not in it), the group size and whether
+// whole tiles are dealt round robin (else stream-K).
 struct SmallGroup {
     int v, size;
     bool deal;
@@ -1101,28 +1220,35 @@ struct SmallGroup {
 
 __device__ __forceinline__ SmallGroup small_group(int64_t tl, int64_t ts, int nk, int G, SmallKind kind, int vx)
 {
-    const bool large_dp = !(tl < G && nk >= SPLIT_MIN_NK);
-    const int idle = tl % G ? G - (int)(tl % G) : 0;
-    const bool pieces = kind.cost_num * ts <= (int64_t)SMALL_COST_DEN * idle;
-    const bool whole = !pieces && ts <= (int64_t)idle * whole_fit(nk, kind.whole_num);
-    if (large_dp && idle && (pieces || whole)) {
-        // die d holds c_d = tl*(d+1)/8 - tl*d/8 whole tiles; with R rounds
-        // (the busiest die's), its workgroups u < c_d - (R-1)*P are busy in
-        // the last round and the others idle.  Number the idle ones die by
-        // die (G - tl % G of them in all).
-        const int P = G / 8, d = vx / P, u = vx % P;
-        const int64_t R = ((tl + 7) / 8 + P - 1) / P;
-        int before = 0, mine = -1;
-        for (int dd = 0; dd < 8; ++dd) {
-            const int64_t c = tl * (dd + 1) / 8 - tl * dd / 8;
-            const int64_t b64 = c - (R - 1) * P;
-            const int busy = b64 < 0 ? 0 : (b64 > P ? P : (int)b64);
-            if (dd == d && u >= busy) mine = before + (u - busy);
-            before += P - busy;
-        }
-        return SmallGroup{mine, before, whole};
+    const SmallPlan p = small_plan(tl, ts, nk, G, kind.cost_num, whole_fit(nk, kind.whole_num),
+                                   whole_time(nk, kind.whole_num));
+    const bool deal = p.mode == SM_WHOLE_IDLE || p.mode == SM_WHOLE_ALL;
+    if (p.mode == SM_PIECES_ALL) return SmallGroup{vx, G, false};
+    // die d holds c_d = tl*(d+1)/8 - tl*d/8 whole tiles; with R rounds (the
+    // busiest die's), its workgroups u < c_d - (R-1)*P are busy in the last
+    // round and the others idle (G - tl % G of them in all; none, and all
+    // counted busy, when the last round is full or there are no large tiles)
+    const int P = G / 8, d = vx / P, u = vx % P;
+    const int64_t R = ((tl + 7) / 8 + P - 1) / P;
+    int busy[8];
+    int n_idle = 0;
+    for (int dd = 0; dd < 8; ++dd) {
+        const int64_t c = tl * (dd + 1) / 8 - tl * dd / 8;
+        const int64_t b64 = p.idle ? c - (R - 1) * P : P;
+        busy[dd] = b64 < 0 ? 0 : (b64 > P ? P : (int)b64);
+        n_idle += P - busy[dd];
     }
-    return SmallGroup{vx, G, false};
+    const bool idle = u >= busy[d];
+    const int j = idle ? u - busy[d] : u;  // index among the die's idle (busy) workgroups
+    int v = 0;
+    for (int dd = 0; dd < 8; ++dd) {
+        const int cnt = idle ? P - busy[dd] : busy[dd];
+        if (deal) v += (cnt < j ? cnt : j) + (dd < d && cnt > j);  // (j, die) order
+        else if (dd < d) v += cnt;                                 // (die, j) order
+    }
+    v += deal ? 0 : j;
+    if (!idle) v = p.mode == SM_WHOLE_ALL ? n_idle + v : -1;
+    return SmallGroup{v, p.mode == SM_WHOLE_ALL ? G : n_idle, deal};
 }
 
 // One grouped GEMM launch: the large-tile class (256-row tiles) and the
@@ -1143,8 +1269,9 @@ void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
         ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, large.tile_prefix, g.El, g.ne, g.cap,
         g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh, large.tile_cnt,
         large.partials, vx, gridDim.x, false);
-    // the small class's group, worked out only now (nothing of it stays
-    // live through the large tiles)
+    // the small class's group, worked out only now (a compiler barrier keeps
+    // its loads here, so nothing of it stays live through the large tiles)
+    asm volatile("" ::: "memory");
     const int64_t n_tiles = (g.N + OUTN - 1) / OUTN;
     const bool tall = small.tile_prefix[g.ne + 1] == SMALL128.rows;  // uniform
     const SmallGroup sg = small_group((int64_t)large.tile_prefix[g.ne] * n_tiles,
@@ -1236,9 +1363,24 @@ int device_cus()
     return (cus + 7) / 8 * 8;  // whole rounds over the 8 dies
 }
 
+// Shape of both GEMMs for the schedule, with the per-GEMM constants of its
+// small-row plans.
+SchedShape sched_shape(int H, int Is, int grid)
+{
+    SchedShape sh{(int)ceil_div(Is, BIGN / 2), H / BIG_BK, (int)ceil_div(H, BIGN), Is / BIG_BK, grid, {}, {}};
+    const int nk[2] = {sh.nk_gu, sh.nk_dn};
+    const SmallKind kinds[2] = {SMALL64, SMALL128};
+    for (int gi = 0; gi < 2; ++gi)
+        for (int k = 0; k < 2; ++k) {
+            sh.wfit[gi][k] = whole_fit(nk[gi], kinds[k].whole_num);
+            sh.whole[gi][k] = whole_time(nk[gi], kinds[k].whole_num);
+        }
+    return sh;
+}
+
 // Workspace layout of the grouped FFN (every part 256-byte aligned):
-//   prefix large [El+1] | prefix small, gate-up and down [El+1] + small tile height each |
-//   class cut [El] |
+//   prefix large, gate-up and down [El+1] each | prefix small, gate-up and
+//   down [El+1] + small tile height each | class cut, gate-up and down [El] each |
 //   tile counters: large gate-up, large down, small gate-up, small down |
 //   split-K partial slots: small [2*G][SLOT_SMALL], large [2*G][SLOT_BIG] fp32 |
 //   h [cap, I_s] bf16
@@ -1248,7 +1390,7 @@ struct FfnLayout {
     bool big;
     int64_t t_gu, t_dn, ts_gu, ts_dn;  // tile-count bounds per class and GEMM
     int grid;                          // persistent workgroups of a large-tile launch
-    size_t off_pre_s, off_pre_sd, off_split, off_cnt, off_part_s, off_part, off_h, total;
+    size_t off_pre_ld, off_pre_s, off_pre_sd, off_split, off_split_d, off_cnt, off_part_s, off_part, off_h, total;
     FfnLayout(int64_t cap, int El, int H, int Is)
     {
         big = (H % BIG_BK == 0) && (Is % BIG_BK == 0) && H >= 2 * BIG_BK && Is >= 2 * BIG_BK;
@@ -1257,17 +1399,20 @@ struct FfnLayout {
         t_gu = mt * ceil_div(Is, big ? BIGN / 2 : BN);
         t_dn = mt * ceil_div(H, big ? BIGN : BN);
         // a small-row expert or leftover has at most max_rows rows: at most
-        // two m-tiles of either height
+        // two m-tiles of either height; the largest expert may add up to
+        // ND_SCHED - 1 large m-tiles (4 small m-tiles each at most)
         static_assert(SMALL64.max_rows <= 2 * SMALL64.rows && SMALL128.max_rows <= 2 * SMALL128.rows, "");
-        const int64_t mts = big ? (int64_t)El * 2 : 0;
+        const int64_t mts = big ? (int64_t)El * 2 + (ND_SCHED - 1) * (BIGM / SMALL64.rows) : 0;
         ts_gu = mts * ceil_div(Is, BIGN / 2);
         ts_dn = mts * ceil_div(H, BIGN);
         grid = device_cus();
         const size_t slots = big ? 2 * (size_t)grid : 0;
-        off_pre_s = align256((size_t)(El + 1) * sizeof(int32_t));
+        off_pre_ld = align256((size_t)(El + 1) * sizeof(int32_t));
+        off_pre_s = off_pre_ld + align256((size_t)(El + 1) * sizeof(int32_t));
         off_pre_sd = off_pre_s + align256((size_t)(El + 2) * sizeof(int32_t));
         off_split = off_pre_sd + align256((size_t)(El + 2) * sizeof(int32_t));
-        off_cnt = off_split + align256((size_t)El * sizeof(int32_t));
+        off_split_d = off_split + align256((size_t)El * sizeof(int32_t));
+        off_cnt = off_split_d + align256((size_t)El * sizeof(int32_t));
         off_part_s = off_cnt + align256((size_t)(t_gu + t_dn + ts_gu + ts_dn) * sizeof(int32_t));
         off_part = off_part_s + align256(slots * SLOT_SMALL * sizeof(float));
         off_h = off_part + align256(slots * SLOT_BIG * sizeof(float));
@@ -1304,10 +1449,12 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
     if (rows == 0) return hipSuccess;
     const FfnLayout L(rows, ne, H, Is);
     char *base = static_cast<char *>(ws);
-    int32_t *pre = reinterpret_cast<int32_t *>(base);
+    int32_t *pre = reinterpret_cast<int32_t *>(base);                     // large class, gate-up
+    int32_t *pre_ld = reinterpret_cast<int32_t *>(base + L.off_pre_ld);  // large class, down
     int32_t *pre_s = reinterpret_cast<int32_t *>(base + L.off_pre_s);    // small class, gate-up
     int32_t *pre_sd = reinterpret_cast<int32_t *>(base + L.off_pre_sd);  // small class, down
-    int32_t *split = reinterpret_cast<int32_t *>(base + L.off_split);
+    int32_t *split = reinterpret_cast<int32_t *>(base + L.off_split);    // class cut, gate-up
+    int32_t *split_d = reinterpret_cast<int32_t *>(base + L.off_split_d);
     int32_t *cnt = reinterpret_cast<int32_t *>(base + L.off_cnt);
     float *part_s = reinterpret_cast<float *>(base + L.off_part_s);
     float *part = reinterpret_cast<float *>(base + L.off_part);
@@ -1318,12 +1465,12 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
     hipError_t err;
     {
         KernelTimer timer(MOE_K_SCHEDULE, s);
-        const unsigned threads = (unsigned)(ceil_div(ne > NC_SCHED ? ne : NC_SCHED, 64) * 64);
+        const unsigned threads = (unsigned)(ceil_div(ne > 128 ? ne : 128, 64) * 64);
+        const SchedOut so{{pre, pre_ld}, {pre_s, pre_sd}, {split, split_d}};
         schedule_kernel<<<dim3(1), dim3(threads), 0, s>>>(
             offsets, El, cap, sc, big ? BIGM : BM, big,
-            SchedShape{(int)ceil_div(Is, BIGN / 2), H / BIG_BK, (int)ceil_div(H, BIGN), Is / BIG_BK, L.grid}, pre,
-            big ? pre_s : nullptr, big ? pre_sd : nullptr, big ? split : nullptr, cnt,
-            big ? L.t_gu + L.t_dn + L.ts_gu + L.ts_dn : 0);
+            sched_shape(H, Is, L.grid), so,
+            cnt, big ? L.t_gu + L.t_dn + L.ts_gu + L.ts_dn : 0);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     if (big) {
@@ -1344,16 +1491,16 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
         }
         {
             KernelTimer timer(MOE_K_DOWN, s);
-            const GemmArgs g{h, nullptr, 1, rows, offsets, split, El, ne, cap, sc, shared_begin,
+            const GemmArgs g{h, nullptr, 1, rows, offsets, split_d, El, ne, cap, sc, shared_begin,
                              H, Is,      w2, (int64_t)H * Is, sw2, 0, y, shared_y};
             gemm_grouped<false><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
-                g, TileClass{pre_sd, cs_dn, part_s}, TileClass{pre, c_dn, part});
+                g, TileClass{pre_sd, cs_dn, part_s}, TileClass{pre_ld, c_dn, part});
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         if (Is / BIG_BK >= SPLIT_MIN_NK) {
             KernelTimer timer(MOE_K_SPLITK_REDUCE, s);
             splitk_reduce<false><<<dim3(REDUCE_GRID), dim3(GEMM_THREADS), 0, s>>>(
-                offsets, split, pre, El, ne, cap, sc, H, Is, L.grid, part, y, shared_y);
+                offsets, split_d, pre_ld, El, ne, cap, sc, H, Is, L.grid, part, y, shared_y);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         return hipSuccess;

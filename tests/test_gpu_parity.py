@@ -443,3 +443,37 @@ def test_grouped_ffn_random_row_mixes(oracle, seed):
     ref = oracle.grouped_ffn(x_perm, offs, w13, w2)
     assert_close_rel(runs[0], ref, what=f"random mix seed={seed} El={El} H={H} Is={Is} rows={counts}")
     np.testing.assert_array_equal(runs[0], runs[1])
+
+
+@pytest.mark.parametrize("counts,H,Is", [([33 * 256 + 100, 500, 60, 7], 2048, 768),
+                                         ([16 * 256 + 17, 16 * 256 + 5, 90], 2048, 1024)])
+def test_grouped_ffn_moved_tiles(oracle, counts, H, Is):
+    """A layer whose down projection has a few more 256-row tiles than one
+    round of workgroups: the schedule moves the last m-tiles of the largest
+    expert to small-row tiles run whole on all workgroups (and keeps the
+    gate-up GEMM's own cut).  Rows sampled across every expert, the moved
+    rows included, match the oracle (each output row depends only on its own
+    input row and its expert's weights), and the result is bitwise
+    reproducible."""
+    E = len(counts)
+    g = np.random.default_rng(sum(counts))
+    ids = g.permutation(np.repeat(np.arange(E, dtype=np.int32), counts))[:, None]
+    T = ids.shape[0]
+    _, offs, _, _ = oracle.permute(ids, 0, E)
+    x_perm = mi.random_bf16((T, H), seed=T, tag=58)
+    w13 = mi.random_bf16((E, 2 * Is, H), seed=T, tag=59, std=0.05)
+    w2 = mi.random_bf16((E, H, Is), seed=T, tag=60, std=0.05)
+    runs = []
+    for _ in range(2):
+        y = moe.grouped_ffn(dev_bf16(x_perm), torch.from_numpy(offs).cuda(), dev_bf16(w13), dev_bf16(w2))
+        torch.cuda.synchronize()
+        runs.append(host_bf16(y)[:T])
+    np.testing.assert_array_equal(runs[0], runs[1])
+    got = bf16_f64(runs[0])
+    for e in range(E):
+        a, b = int(offs[e]), int(offs[e + 1])
+        # the last 8 m-tiles (where moved rows lie) every 5th row, the rest every 41st
+        tail = max(a, b - 8 * 256)
+        rows = np.unique(np.concatenate([np.arange(a, tail, 41), np.arange(tail, b, 5), [b - 1]]))
+        ref = oracle.grouped_ffn(x_perm[rows], np.array([0, len(rows)], np.int32), w13[e:e + 1], w2[e:e + 1])
+        assert_close_rel(got[rows], ref, what=f"moved tiles expert {e} of {counts}")
