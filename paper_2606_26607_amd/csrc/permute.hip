@@ -15,7 +15,8 @@
 //               unique stable order, identical on every run.
 //   4. gather:  optional copy of x rows into permuted order (16-byte moves).
 // Small inputs (decode: at most 16384 pairs over at most 64 local experts)
-// run steps 1-3 in one workgroup instead, saving two launches.
+// run steps 1-3 in one workgroup instead, saving two launches; larger ones
+// with at most 64 local experts run steps 2 and 3 in one launch.
 #include "moe_internal.h"
 
 namespace moe {
@@ -332,6 +333,121 @@ __global__ __launch_bounds__(64) void scatter_kernel(const int32_t *__restrict__
     }
 }
 
+// Steps 2 and 3 in one launch (at most 64 local experts): a block of four
+// wavefronts scatters four chunks, one each, after rebuilding from the chunk
+// histograms what the scan would have handed it: each expert's total (hence
+// its first row) and the pairs of that expert in the chunks before its own.
+// Every block reads the whole histogram table (a few KB, from L2), which is
+// cheaper than a separate single-workgroup scan launch between count and
+// scatter.  Block 0 also writes counts and offsets.
+template <int ROUNDS>
+__global__ __launch_bounds__(256) void scan_scatter_kernel(const int32_t *__restrict__ ids, int64_t npairs,
+                                                          int e0, int El, int nbits,
+                                                          const int32_t *__restrict__ chunk_cnt, int64_t nchunks,
+                                                          int32_t *__restrict__ counts,
+                                                          int32_t *__restrict__ offsets,
+                                                          int32_t *__restrict__ row_to_pair,
+                                                          int32_t *__restrict__ pair_to_row)
+{
+    constexpr int CHUNK = ROUNDS * 64, UNR = 4;
+    __shared__ int32_t part_tot[256], part_bef[256];
+    __shared__ int32_t next_row[4][64];
+    const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+    const int64_t c_first = (int64_t)blockIdx.x * 4;
+    // 1. column sums of the histogram table: thread t sums expert t % El over
+    //    chunks t / El, t / El + S, ... (S = 256 / El groups), all chunks and
+    //    those before this block's first
+    const int S = 256 / El;
+    int32_t tot = 0, bef = 0;
+    if (t < S * El) {
+        const int e = t % El;
+        for (int64_t c = t / El; c < nchunks; c += (int64_t)S * UNR) {
+            int32_t v[UNR];
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) {
+                const int64_t cu = c + (int64_t)u * S;
+                v[u] = cu < nchunks ? chunk_cnt[cu * El + e] : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) {
+                tot += v[u];
+                bef += c + (int64_t)u * S < c_first ? v[u] : 0;
+            }
+        }
+    }
+    part_tot[t] = tot;
+    part_bef[t] = bef;
+    __syncthreads();
+    // 2. per expert (one lane each): its total, the exclusive scan of the
+    //    totals over the experts (its first row), and this block's first row
+    if (wv == 0) {
+        int32_t total = 0, before = 0;
+        if (lane < El)
+            for (int g = 0; g < S; ++g) {
+                total += part_tot[g * El + lane];
+                before += part_bef[g * El + lane];
+            }
+        int32_t incl = total;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int32_t o = __shfl_up(incl, off, 64);
+            if (lane >= off) incl += o;
+        }
+        const int32_t eexcl = incl - total;
+        if (lane < El) {
+            if (blockIdx.x == 0) {
+                counts[lane] = total;
+                offsets[lane] = eexcl;
+                if (lane == El - 1) offsets[El] = incl;  // total over all experts
+            }
+            next_row[0][lane] = eexcl + before;
+        }
+    }
+    __syncthreads();
+    // 3. wave w scatters chunk c_first + w: its first row per expert is the
+    //    block's plus the pairs of the block's chunks before it
+    int32_t row = lane < El ? next_row[0][lane] : 0;
+    __syncthreads();  // every wave has the block's rows before wave 0 reuses its LDS row
+    const int64_t c = c_first + wv;
+    if (c >= nchunks) return;
+    if (lane < El) {
+        for (int64_t cc = c_first; cc < c; ++cc) row += chunk_cnt[cc * El + lane];
+        next_row[wv][lane] = row;
+    }
+    __builtin_amdgcn_wave_barrier();
+    const int64_t base = c * CHUNK;
+    int32_t v[ROUNDS];
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r) {
+        const int64_t p = base + r * 64 + lane;
+        v[r] = p < npairs ? ids[p] : -1;
+    }
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    for (int r = 0; r < ROUNDS; ++r) {
+        const int64_t p = base + r * 64 + lane;
+        const bool valid = p < npairs;
+        const int le = valid ? local_index(v[r], e0, El) : El + 1;
+        uint64_t peers = ~0ull;
+        for (int b = 0; b < nbits; ++b) {
+            const bool bit = (le >> b) & 1;
+            const uint64_t bal = __ballot(bit);
+            peers &= bit ? bal : ~bal;
+        }
+        const int rank = __popcll(peers & below);
+        if (le < El) {
+            const int32_t row = next_row[wv][le] + rank;
+            row_to_pair[row] = (int32_t)p;
+            pair_to_row[p] = row;
+        } else if (valid) {
+            pair_to_row[p] = -1;
+        }
+        // the wave's own LDS row: its leaders bump it after every lane read it
+        __builtin_amdgcn_wave_barrier();
+        if (le < El && rank == 0) next_row[wv][le] += __popcll(peers);
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
 __global__ __launch_bounds__(256) void gather_kernel(const uint16_t *__restrict__ x, int H, int k,
                                                      const int32_t *__restrict__ row_to_pair,
                                                      const int32_t *__restrict__ offsets, int El,
@@ -379,22 +495,34 @@ hipError_t launch_permute(const int32_t *ids, int64_t T, int k, int e0, int El, 
                     ids, npairs, e0, El, ws);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
-        if (El <= 64) {
-            scan_narrow_kernel<<<dim3(1), dim3(1024), 0, s>>>(ws, nchunks, El, counts, offsets);
-        } else {
-            int L = 1;
-            while (L < 64 && 2 * L * El <= 1024) L *= 2;
-            scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(ws, nchunks, El, L, counts, offsets);
-        }
-        if ((err = hipGetLastError()) != hipSuccess) return err;
-        if (nchunks > 0) {
+        if (El <= 64 && nchunks > 0) {
+            // scan and scatter in one launch
+            const unsigned blocks = (unsigned)ceil_div(nchunks, 4);
             if (short_chunks)
-                scatter_kernel<4><<<dim3((unsigned)nchunks), dim3(64), El * sizeof(int32_t), s>>>(
-                    ids, npairs, e0, El, nbits, ws, row_to_pair, pair_to_row);
+                scan_scatter_kernel<4><<<dim3(blocks), dim3(256), 0, s>>>(ids, npairs, e0, El, nbits, ws, nchunks,
+                                                                          counts, offsets, row_to_pair, pair_to_row);
             else
-                scatter_kernel<16><<<dim3((unsigned)nchunks), dim3(64), El * sizeof(int32_t), s>>>(
-                    ids, npairs, e0, El, nbits, ws, row_to_pair, pair_to_row);
+                scan_scatter_kernel<16><<<dim3(blocks), dim3(256), 0, s>>>(ids, npairs, e0, El, nbits, ws, nchunks,
+                                                                           counts, offsets, row_to_pair, pair_to_row);
             if ((err = hipGetLastError()) != hipSuccess) return err;
+        } else {
+            if (El <= 64) {
+                scan_narrow_kernel<<<dim3(1), dim3(1024), 0, s>>>(ws, nchunks, El, counts, offsets);
+            } else {
+                int L = 1;
+                while (L < 64 && 2 * L * El <= 1024) L *= 2;
+                scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(ws, nchunks, El, L, counts, offsets);
+            }
+            if ((err = hipGetLastError()) != hipSuccess) return err;
+            if (nchunks > 0) {
+                if (short_chunks)
+                    scatter_kernel<4><<<dim3((unsigned)nchunks), dim3(64), El * sizeof(int32_t), s>>>(
+                        ids, npairs, e0, El, nbits, ws, row_to_pair, pair_to_row);
+                else
+                    scatter_kernel<16><<<dim3((unsigned)nchunks), dim3(64), El * sizeof(int32_t), s>>>(
+                        ids, npairs, e0, El, nbits, ws, row_to_pair, pair_to_row);
+                if ((err = hipGetLastError()) != hipSuccess) return err;
+            }
         }
     }
     if (x_perm != nullptr && cap > 0) {

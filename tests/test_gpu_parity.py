@@ -109,13 +109,16 @@ def test_permute_configs(oracle, name):
 @pytest.mark.parametrize("T,E,k,P", [(1, 8, 2, 1), (1, 8, 2, 8), (1023, 8, 2, 2), (1025, 64, 8, 8),
                                      (5000, 128, 8, 8), (3000, 1024, 16, 4), (2048, 16, 1, 1),
                                      (70000, 8, 2, 8), (8192, 256, 8, 1), (20000, 512, 8, 2),
-                                     (2048, 64, 8, 1), (4096, 128, 4, 2), (4097, 128, 4, 2)])
+                                     (2048, 64, 8, 1), (4096, 128, 4, 2), (4097, 128, 4, 2),
+                                     (40000, 512, 8, 8)])
 def test_permute_every_rank(oracle, T, E, k, P):
     """Every rank's slice of the same routing, against the oracle.  Up to
-    16384 pairs and 64 local experts run in one workgroup (the last three
-    cases: 16384 pairs with 64 experts, then 16388); above that pairs x
-    local experts up to 2^24 take 256-pair chunks, larger ones 1024-pair
-    chunks (the two cases before them sit on either side of that line)."""
+    16384 pairs and 64 local experts run in one workgroup (16384 pairs with
+    64 experts, then 16388); above that pairs x local experts up to 2^24
+    take 256-pair chunks, larger ones 1024-pair chunks (20000 x 8 pairs over
+    256 experts and 8192 x 8 over 256 sit on either side of that line, and
+    40000 x 8 pairs over 64 local experts is past it), with the scan and the
+    scatter in one launch for up to 64 local experts."""
     ids = mi.random_topk_ids(T, E, k, seed=T + E + k)
     total = 0
     for r in range(P):
