@@ -14,9 +14,10 @@
 //               among equal lanes.  No global atomics: the result is the
 //               unique stable order, identical on every run.
 //   4. gather:  optional copy of x rows into permuted order (16-byte moves).
-// Small inputs (decode: at most 16384 pairs over at most 64 local experts)
-// run steps 1-3 in one workgroup instead, saving two launches; larger ones
-// with at most 64 local experts run steps 2 and 3 in one launch.
+// Small inputs (decode: at most 16384 pairs over at most 64 local experts,
+// and a bounded amount of ballot work, see SMALL_WORK) run steps 1-3 in one
+// workgroup instead, saving launches; larger ones with at most 64 local
+// experts run steps 2 and 3 in one launch.
 #include "moe_internal.h"
 
 namespace moe {
@@ -201,8 +202,13 @@ __global__ __launch_bounds__(1024) void scan_narrow_kernel(int32_t *__restrict__
 // (kept in registers), counts it per expert with the same ballot ranking as
 // the scatter, the per-(wave, expert) bases are scanned in LDS, and the
 // wavefronts then place their pairs in order.  Same stable result as the
-// three-kernel path.
+// multi-kernel path.  One workgroup's time grows with the pairs and the
+// ballots per pair (bits of the local expert index) while the multi-kernel
+// path costs about two launches, so the workgroup takes at most
+// SMALL_WORK pair-steps (measured: 8192 pairs over 1 local expert and 4096
+// over 32 are faster here, 8192 over 8 in two launches).
 constexpr int SMALL_PAIRS = 16 * 1024;
+constexpr int64_t SMALL_WORK = 32 * 1024;
 __global__ __launch_bounds__(1024) void permute_small_kernel(const int32_t *__restrict__ ids, int64_t npairs,
                                                              int e0, int El, int nbits,
                                                              int32_t *__restrict__ counts,
@@ -479,7 +485,7 @@ hipError_t launch_permute(const int32_t *ids, int64_t T, int k, int e0, int El, 
     int nbits = 0;
     while ((1 << nbits) < El + 2) ++nbits;  // distinguishes 0..El+1
     hipError_t err;
-    if (npairs > 0 && npairs <= SMALL_PAIRS && El <= 64) {
+    if (npairs > 0 && npairs <= SMALL_PAIRS && El <= 64 && npairs * (nbits + 2) <= SMALL_WORK) {
         KernelTimer timer(MOE_K_PERMUTE, s);
         permute_small_kernel<<<dim3(1), dim3(1024), 0, s>>>(ids, npairs, e0, El, nbits, counts, offsets,
                                                              row_to_pair, pair_to_row);

@@ -110,15 +110,16 @@ def test_permute_configs(oracle, name):
                                      (5000, 128, 8, 8), (3000, 1024, 16, 4), (2048, 16, 1, 1),
                                      (70000, 8, 2, 8), (8192, 256, 8, 1), (20000, 512, 8, 2),
                                      (2048, 64, 8, 1), (4096, 128, 4, 2), (4097, 128, 4, 2),
-                                     (40000, 512, 8, 8)])
+                                     (40000, 512, 8, 8), (448, 64, 8, 1), (456, 64, 8, 1)])
 def test_permute_every_rank(oracle, T, E, k, P):
-    """Every rank's slice of the same routing, against the oracle.  Up to
-    16384 pairs and 64 local experts run in one workgroup (16384 pairs with
-    64 experts, then 16388); above that pairs x local experts up to 2^24
-    take 256-pair chunks, larger ones 1024-pair chunks (20000 x 8 pairs over
-    256 experts and 8192 x 8 over 256 sit on either side of that line, and
-    40000 x 8 pairs over 64 local experts is past it), with the scan and the
-    scatter in one launch for up to 64 local experts."""
+    """Every rank's slice of the same routing, against the oracle.  Small
+    inputs run in one workgroup: at most 16384 pairs, 64 local experts and
+    32768 pair-steps of ballot work (pairs x (index bits + 2)), so 3584 pairs
+    over 64 experts do and 3648 do not; above that pairs x local experts up
+    to 2^24 take 256-pair chunks, larger ones 1024-pair chunks (20000 x 8
+    pairs over 256 experts and 8192 x 8 over 256 sit on either side of that
+    line, and 40000 x 8 pairs over 64 local experts is past it), with the
+    scan and the scatter in one launch for up to 64 local experts."""
     ids = mi.random_topk_ids(T, E, k, seed=T + E + k)
     total = 0
     for r in range(P):
