@@ -690,10 +690,14 @@ __device__ __forceinline__ uint16_t bf16_bits(float f)
 }
 
 // Coordinates of tile `tile` of a tile class: expert e, rows [r0, r1) and
-// output columns [n0, n0 + nvalid).  Tiles are numbered expert by expert
-// (ne experts), then by n-tile, with m-tiles innermost; the class's rows of
-// expert e are [begin(e), split[e]) for the large class and
-// [split[e], end(e)) for the tail class.
+// output columns [n0, n0 + nvalid).  Large tiles are numbered expert by
+// expert (ne experts), then by n-tile, with m-tiles innermost, so a die's
+// run of tiles shares weight panels.  Small-row tiles are numbered n-tile by
+// n-tile, every expert's m-tiles within one: an expert with more rows (a
+// shared expert's decode rows) costs more per slice, and numbered this way
+// its tiles fall into many workgroups' stream-K runs instead of filling the
+// runs of a few.  The class's rows of expert e are [begin(e), split[e]) for
+// the large class and [split[e], end(e)) for the tail class.
 struct TileCoord {
     int e;
     int64_t r0, r1;
@@ -706,16 +710,29 @@ __device__ __forceinline__ TileCoord tile_coord(int64_t tile, const int32_t *__r
                                                 int64_t shared_rows, const int32_t *__restrict__ split,
                                                 int64_t cap, int N)
 {
-    int lo = 0, hi = ne - 1;
-    while (lo < hi) {
-        int mid = (lo + hi + 1) >> 1;
-        if ((int64_t)tile_prefix[mid] * n_tiles <= tile) lo = mid; else hi = mid - 1;
+    int lo = 0, hi = ne - 1, nt, mt;
+    if constexpr (TAIL) {
+        // the class has fewer than 2^31 tiles (checked on the host)
+        const uint32_t ms = (uint32_t)tile_prefix[ne];
+        nt = (int)((uint32_t)tile / ms);
+        const int m = (int)((uint32_t)tile - (uint32_t)nt * ms);
+        while (lo < hi) {
+            int mid = (lo + hi + 1) >> 1;
+            if (tile_prefix[mid] <= m) lo = mid; else hi = mid - 1;
+        }
+        mt = m - tile_prefix[lo];
+    } else {
+        while (lo < hi) {
+            int mid = (lo + hi + 1) >> 1;
+            if ((int64_t)tile_prefix[mid] * n_tiles <= tile) lo = mid; else hi = mid - 1;
+        }
+        const int64_t local = tile - (int64_t)tile_prefix[lo] * n_tiles;
+        const int mte = tile_prefix[lo + 1] - tile_prefix[lo];
+        nt = (int)(local / mte);
+        mt = (int)(local % mte);
     }
     TileCoord c;
     c.e = lo;
-    const int64_t local = tile - (int64_t)tile_prefix[lo] * n_tiles;
-    const int mte = tile_prefix[lo + 1] - tile_prefix[lo];
-    const int nt = (int)(local / mte), mt = (int)(local % mte);
     const int64_t rb = TAIL ? split[lo] : expert_begin(offsets, El, cap, lo);
     const int64_t re = TAIL ? expert_end(offsets, El, cap, shared_rows, lo) : split[lo];
     c.r0 = rb + (int64_t)mt * BMt;
@@ -1429,9 +1446,12 @@ size_t ffn_workspace_bytes(int64_t cap, int El, int H, int Is)
 
 bool ffn_large_tiles(int64_t x_rows, int64_t rows, int H, int Is)
 {
-    // K a multiple of 64 with at least two slices, and every operand
-    // addressable with 32-bit buffer offsets
+    // K a multiple of 64 with at least two slices, every operand
+    // addressable with 32-bit buffer offsets, and small-row tile numbers
+    // below 2^31 (at most 2 * 1025 + 28 m-tiles, with a shared expert, of
+    // 2^26 / 128 + 1 n-tiles)
     if (H % BIG_BK || Is % BIG_BK || H < 2 * BIG_BK || Is < 2 * BIG_BK) return false;
+    if (H > (1 << 26) || Is > (1 << 26)) return false;
     const int64_t lim = ((int64_t)1 << 32) - 4 * (int64_t)(H > Is ? H : Is);
     return x_rows * (int64_t)H * 2 < lim && rows * (int64_t)H * 2 < lim && rows * (int64_t)Is * 2 < lim;
 }
