@@ -257,6 +257,7 @@ constexpr int ND_SCHED = 8;   // ... each also with up to 7 more m-tiles of the 
 // chain stays graph-capturable).
 struct SchedOut {
     int32_t *pre_l[2], *pre_s[2], *split[2];
+    int4 *mt[2];  // per small m-tile: expert, first row, end row
 };
 
 __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restrict__ offsets, int El,
@@ -406,14 +407,16 @@ __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restric
         }
     }
     int32_t v[4];
-    int h[2];
+    int h[2], ms[2];
+    int32_t cut[2];
     for (int gi = 0; gi < 2; ++gi) {
         int2 r = rows_for(n, cand[gi] / ND_SCHED);
         if (e == L) r = rows_moved(n, r, cand[gi] % ND_SCHED);
-        if (small && e < ne) out.split[gi][e] = a + (n - r.y);
+        cut[gi] = a + (n - r.y);
+        if (small && e < ne) out.split[gi][e] = cut[gi];
         h[gi] = kinds & (1 << gi) ? SMALL128.rows : SMALL64.rows;
         v[2 * gi] = r.x;
-        v[2 * gi + 1] = (r.y + h[gi] - 1) / h[gi];
+        v[2 * gi + 1] = ms[gi] = (r.y + h[gi] - 1) / h[gi];
     }
     // prefixes of both GEMMs' large and small m-tiles
     block_exscan_n<4>(v, wsum, ptot);
@@ -421,7 +424,14 @@ __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restric
         if (e < ne) out.pre_l[gi][e] = v[2 * gi];
         if (e == 0) out.pre_l[gi][ne] = ptot[2 * gi];
         if (small) {
-            if (e < ne) out.pre_s[gi][e] = v[2 * gi + 1];
+            if (e < ne) {
+                out.pre_s[gi][e] = v[2 * gi + 1];
+                // this expert's small m-tiles: rows [cut, end) in runs of h
+                for (int j = 0; j < ms[gi]; ++j) {
+                    const int32_t r0 = cut[gi] + j * h[gi], r1 = r0 + h[gi] < a + n ? r0 + h[gi] : a + n;
+                    out.mt[gi][v[2 * gi + 1] + j] = make_int4(e, r0, r1, 0);
+                }
+            }
             if (e == 0) {
                 out.pre_s[gi][ne] = ptot[2 * gi + 1];
                 out.pre_s[gi][ne + 1] = h[gi];
@@ -705,41 +715,43 @@ struct TileCoord {
 };
 
 template <int BMt, int OUTN, bool TAIL>
-__device__ __forceinline__ TileCoord tile_coord(int64_t tile, const int32_t *__restrict__ tile_prefix, int ne,
+__device__ __forceinline__ TileCoord tile_coord(int64_t tile, const int32_t *__restrict__ tile_prefix,
+                                                const int4 *__restrict__ mtile, int ne,
                                                 int n_tiles, const int32_t *__restrict__ offsets, int El,
                                                 int64_t shared_rows, const int32_t *__restrict__ split,
                                                 int64_t cap, int N)
 {
-    int lo = 0, hi = ne - 1, nt, mt;
+    TileCoord c;
     if constexpr (TAIL) {
-        // the class has fewer than 2^31 tiles (checked on the host)
+        // the class has fewer than 2^31 tiles (checked on the host); its
+        // m-tiles are listed by the schedule, so one load finds the expert
         const uint32_t ms = (uint32_t)tile_prefix[ne];
-        nt = (int)((uint32_t)tile / ms);
-        const int m = (int)((uint32_t)tile - (uint32_t)nt * ms);
-        while (lo < hi) {
-            int mid = (lo + hi + 1) >> 1;
-            if (tile_prefix[mid] <= m) lo = mid; else hi = mid - 1;
-        }
-        mt = m - tile_prefix[lo];
+        const int nt = (int)((uint32_t)tile / ms);
+        const int4 m = mtile[(uint32_t)tile - (uint32_t)nt * ms];
+        c.e = m.x;
+        c.r0 = m.y;
+        c.r1 = m.z;
+        c.n0 = nt * OUTN;
+        c.nvalid = N - c.n0 < OUTN ? N - c.n0 : OUTN;
+        return c;
     } else {
+        int lo = 0, hi = ne - 1;
         while (lo < hi) {
             int mid = (lo + hi + 1) >> 1;
             if ((int64_t)tile_prefix[mid] * n_tiles <= tile) lo = mid; else hi = mid - 1;
         }
         const int64_t local = tile - (int64_t)tile_prefix[lo] * n_tiles;
         const int mte = tile_prefix[lo + 1] - tile_prefix[lo];
-        nt = (int)(local / mte);
-        mt = (int)(local % mte);
+        const int nt = (int)(local / mte), mt = (int)(local % mte);
+        c.e = lo;
+        const int64_t rb = expert_begin(offsets, El, cap, lo);
+        const int64_t re = split[lo];
+        c.r0 = rb + (int64_t)mt * BMt;
+        c.r1 = re < c.r0 + BMt ? re : c.r0 + BMt;
+        c.n0 = nt * OUTN;
+        c.nvalid = N - c.n0 < OUTN ? N - c.n0 : OUTN;
+        return c;
     }
-    TileCoord c;
-    c.e = lo;
-    const int64_t rb = TAIL ? split[lo] : expert_begin(offsets, El, cap, lo);
-    const int64_t re = TAIL ? expert_end(offsets, El, cap, shared_rows, lo) : split[lo];
-    c.r0 = rb + (int64_t)mt * BMt;
-    c.r1 = re < c.r0 + BMt ? re : c.r0 + BMt;
-    c.n0 = nt * OUTN;
-    c.nvalid = N - c.n0 < OUTN ? N - c.n0 : OUTN;
-    return c;
 }
 
 // A partial accumulator slot holds one fp32 value per accumulator register
@@ -813,6 +825,7 @@ struct GemmArgs {
 // [split[e], offsets[e+1]).
 struct TileClass {
     const int32_t *tile_prefix;
+    const int4 *mtile;  // small class: the schedule's list of its m-tiles
     int32_t *tile_cnt;
     float *partials;
 };
@@ -827,7 +840,8 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                                            const int32_t *__restrict__ row_index, int kdiv, int64_t a_rows,
                                            const int32_t *__restrict__ offsets,
                                            const int32_t *__restrict__ split,
-                                           const int32_t *__restrict__ tile_prefix, int El, int ne,
+                                           const int32_t *__restrict__ tile_prefix,
+                                           const int4 *__restrict__ mtile, int El, int ne,
                                            int64_t cap, int64_t shared_rows, int64_t shared_begin,
                                            int N, int K, const uint16_t *__restrict__ W, int64_t w_stride,
                                            const uint16_t *__restrict__ Wsh, int up_off,
@@ -906,7 +920,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
 
     // One piece of work: K-slices [klo, khi) of tile `tile`.
     auto do_work = [&](int64_t tile, int klo, int khi) {
-        const TileCoord tc = tile_coord<BMt, OUTN, TAIL>(tile, tile_prefix, ne, n_tiles, offsets, El, shared_rows,
+        const TileCoord tc = tile_coord<BMt, OUTN, TAIL>(tile, tile_prefix, mtile, ne, n_tiles, offsets, El, shared_rows,
                                                          split, cap, N);
         const int e = tc.e;
         const int64_t r0 = tc.r0, r1 = tc.r1;
@@ -1283,7 +1297,7 @@ void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
     // die-major id: the hardware deals workgroups to the 8 dies round robin
     const int vx = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
     gemm_class<BIGM, BIGN, GATED, BIG_WM, false, A_SLOTS, B_SLOTS>(
-        ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, large.tile_prefix, g.El, g.ne, g.cap,
+        ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, large.tile_prefix, nullptr, g.El, g.ne, g.cap,
         g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh, large.tile_cnt,
         large.partials, vx, gridDim.x, false);
     // the small class's group, worked out only now (a compiler barrier keeps
@@ -1296,12 +1310,12 @@ void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
                                       tall ? SMALL128 : SMALL64, vx);
     if (tall)
         gemm_class<SMALL128.rows, BIGN, GATED, SMALL_WM, true, S128_ASL, S128_BSL>(
-            ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, small.tile_prefix, g.El, g.ne, g.cap,
+            ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, small.tile_prefix, small.mtile, g.El, g.ne, g.cap,
             g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh,
             small.tile_cnt, small.partials, sg.v, sg.size, sg.deal);
     else
         gemm_class<SMALL64.rows, BIGN, GATED, SMALL_WM, true, SA_SLOTS, SB_SLOTS>(
-            ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, small.tile_prefix, g.El, g.ne, g.cap,
+            ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, small.tile_prefix, small.mtile, g.El, g.ne, g.cap,
             g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh,
             small.tile_cnt, small.partials, sg.v, sg.size, sg.deal);
 }
@@ -1333,7 +1347,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void splitk_reduce(const int32_t *__r
     for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
         const int64_t tile = ws.dp + it / (MB * JJ);
         const int i = (int)((it / JJ) % MB), j = (int)(it % JJ);
-        const TileCoord tc = tile_coord<BIGM, OUTN, false>(tile, tile_prefix, ne, n_tiles, offsets, El, shared_rows,
+        const TileCoord tc = tile_coord<BIGM, OUTN, false>(tile, tile_prefix, nullptr, ne, n_tiles, offsets, El, shared_rows,
                                                            split, cap, N);
         uint16_t *Cb = tc.e < El ? C + tc.r0 * N : Csh + (tc.r0 - cap) * N;
         const int64_t tb = (tile - ws.dp) * nk;
@@ -1398,6 +1412,7 @@ SchedShape sched_shape(int H, int Is, int grid)
 // Workspace layout of the grouped FFN (every part 256-byte aligned):
 //   prefix large, gate-up and down [El+1] each | prefix small, gate-up and
 //   down [El+1] + small tile height each | class cut, gate-up and down [El] each |
+//   small m-tiles (expert, first row, end row), gate-up and down [mts] each |
 //   tile counters: large gate-up, large down, small gate-up, small down |
 //   split-K partial slots: small [2*G][SLOT_SMALL], large [2*G][SLOT_BIG] fp32 |
 //   h [cap, I_s] bf16
@@ -1407,7 +1422,8 @@ struct FfnLayout {
     bool big;
     int64_t t_gu, t_dn, ts_gu, ts_dn;  // tile-count bounds per class and GEMM
     int grid;                          // persistent workgroups of a large-tile launch
-    size_t off_pre_ld, off_pre_s, off_pre_sd, off_split, off_split_d, off_cnt, off_part_s, off_part, off_h, total;
+    size_t off_pre_ld, off_pre_s, off_pre_sd, off_split, off_split_d, off_mt, off_mt_d, off_cnt, off_part_s, off_part,
+        off_h, total;
     FfnLayout(int64_t cap, int El, int H, int Is)
     {
         big = (H % BIG_BK == 0) && (Is % BIG_BK == 0) && H >= 2 * BIG_BK && Is >= 2 * BIG_BK;
@@ -1429,7 +1445,9 @@ struct FfnLayout {
         off_pre_sd = off_pre_s + align256((size_t)(El + 2) * sizeof(int32_t));
         off_split = off_pre_sd + align256((size_t)(El + 2) * sizeof(int32_t));
         off_split_d = off_split + align256((size_t)El * sizeof(int32_t));
-        off_cnt = off_split_d + align256((size_t)El * sizeof(int32_t));
+        off_mt = off_split_d + align256((size_t)El * sizeof(int32_t));
+        off_mt_d = off_mt + align256((size_t)mts * sizeof(int4));
+        off_cnt = off_mt_d + align256((size_t)mts * sizeof(int4));
         off_part_s = off_cnt + align256((size_t)(t_gu + t_dn + ts_gu + ts_dn) * sizeof(int32_t));
         off_part = off_part_s + align256(slots * SLOT_SMALL * sizeof(float));
         off_h = off_part + align256(slots * SLOT_BIG * sizeof(float));
@@ -1475,6 +1493,8 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
     int32_t *pre_sd = reinterpret_cast<int32_t *>(base + L.off_pre_sd);  // small class, down
     int32_t *split = reinterpret_cast<int32_t *>(base + L.off_split);    // class cut, gate-up
     int32_t *split_d = reinterpret_cast<int32_t *>(base + L.off_split_d);
+    int4 *mt_g = reinterpret_cast<int4 *>(base + L.off_mt);  // small m-tiles, gate-up
+    int4 *mt_d = reinterpret_cast<int4 *>(base + L.off_mt_d);
     int32_t *cnt = reinterpret_cast<int32_t *>(base + L.off_cnt);
     float *part_s = reinterpret_cast<float *>(base + L.off_part_s);
     float *part = reinterpret_cast<float *>(base + L.off_part);
@@ -1486,7 +1506,7 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
     {
         KernelTimer timer(MOE_K_SCHEDULE, s);
         const unsigned threads = (unsigned)(ceil_div(ne > 128 ? ne : 128, 64) * 64);
-        const SchedOut so{{pre, pre_ld}, {pre_s, pre_sd}, {split, split_d}};
+        const SchedOut so{{pre, pre_ld}, {pre_s, pre_sd}, {split, split_d}, {mt_g, mt_d}};
         schedule_kernel<<<dim3(1), dim3(threads), 0, s>>>(
             offsets, El, cap, sc, big ? BIGM : BM, big,
             sched_shape(H, Is, L.grid), so,
@@ -1500,7 +1520,7 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
             const GemmArgs g{x,   row_index, kdiv, x_rows, offsets, split, El, ne, cap, sc, shared_begin,
                              Is,  H,         w13,  (int64_t)2 * Is * H, sw13, Is, h, h_sh};
             gemm_grouped<true><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
-                g, TileClass{pre_s, cs_gu, part_s}, TileClass{pre, c_gu, part});
+                g, TileClass{pre_s, mt_g, cs_gu, part_s}, TileClass{pre, nullptr, c_gu, part});
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         if (H / BIG_BK >= SPLIT_MIN_NK) {  // the large tiles may have been split over K
@@ -1514,7 +1534,7 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
             const GemmArgs g{h, nullptr, 1, rows, offsets, split_d, El, ne, cap, sc, shared_begin,
                              H, Is,      w2, (int64_t)H * Is, sw2, 0, y, shared_y};
             gemm_grouped<false><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
-                g, TileClass{pre_sd, cs_dn, part_s}, TileClass{pre_ld, c_dn, part});
+                g, TileClass{pre_sd, mt_d, cs_dn, part_s}, TileClass{pre_ld, nullptr, c_dn, part});
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         if (Is / BIG_BK >= SPLIT_MIN_NK) {
