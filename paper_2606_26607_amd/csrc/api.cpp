@@ -219,7 +219,7 @@ extern "C" moe_status moe_grouped_ffn_shared(const uint16_t *x, int64_t x_rows, 
             return fail(MOE_ERR_UNSUPPORTED, "%s: cap_rows + shared_count too large", fn);
         if (!ffn_large_tiles(x_rows, cap_rows + shared_count, H, I_s))
             return fail(MOE_ERR_UNSUPPORTED,
-                        "%s: H=%d and I_s=%d must be multiples of 64, at least 128, with operands under 4 GiB",
+                        "%s: H=%d and I_s=%d must be multiples of 64, from 128 to 2^26, with operands under 4 GiB",
                         fn, H, I_s);
     }
     const int ne = n_local_experts + (shared_count > 0 ? 1 : 0);

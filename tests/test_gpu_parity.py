@@ -481,3 +481,32 @@ def test_grouped_ffn_moved_tiles(oracle, counts, H, Is):
         rows = np.unique(np.concatenate([np.arange(a, tail, 41), np.arange(tail, b, 5), [b - 1]]))
         ref = oracle.grouped_ffn(x_perm[rows], np.array([0, len(rows)], np.int32), w13[e:e + 1], w2[e:e + 1])
         assert_close_rel(got[rows], ref, what=f"moved tiles expert {e} of {counts}")
+
+
+def test_grouped_ffn_max_experts(oracle):
+    """The most local experts the library takes (1024), most of them small
+    (empty, a few rows, 97-128 rows that take two 64-row or one 128-row
+    m-tile), some with whole 256-row tiles and a leftover, one large enough
+    for the schedule to move its last m-tiles: the schedule's per-expert
+    m-tile list is at its widest, and the result matches the oracle,
+    bitwise reproducibly."""
+    g = np.random.default_rng(4242)
+    El, H, Is = 1024, 128, 192
+    kinds = g.integers(0, 4, El)
+    counts = np.where(kinds == 0, 0, np.where(kinds == 1, g.integers(1, 33, El), g.integers(97, 129, El)))
+    counts[g.choice(El, 12, replace=False)] = 256 * g.integers(1, 3, 12) + g.integers(1, 100, 12)
+    counts[7] = 256 * 9 + 40
+    ids = g.permutation(np.repeat(np.arange(El, dtype=np.int32), counts))[:, None]
+    T = ids.shape[0]
+    _, offs, _, _ = oracle.permute(ids, 0, El)
+    x_perm = mi.random_bf16((T, H), seed=11, tag=58)
+    w13 = mi.random_bf16((El, 2 * Is, H), seed=11, tag=59, std=0.05)
+    w2 = mi.random_bf16((El, H, Is), seed=11, tag=60, std=0.05)
+    runs = []
+    for _ in range(2):
+        y = moe.grouped_ffn(dev_bf16(x_perm), torch.from_numpy(offs).cuda(), dev_bf16(w13), dev_bf16(w2))
+        torch.cuda.synchronize()
+        runs.append(bf16_f64(host_bf16(y)[:T]))
+    ref = oracle.grouped_ffn(x_perm, offs, w13, w2)
+    assert_close_rel(runs[0], ref, what=f"max experts El={El} rows={T}")
+    np.testing.assert_array_equal(runs[0], runs[1])
