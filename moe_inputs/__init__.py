@@ -60,6 +60,7 @@ class MoeConfig:
     layout: str = "replicated"   # "replicated" | "tp" | "ep"
     rank: int = 0
     zipf_s: Optional[float] = None   # per-expert Zipf log-bias on the logits
+    zipf_hot: bool = False  # Zipf popularity rank = expert id (rank 0 holds the hottest experts)
     shared: bool = False   # one shared expert, applied to the rank's DP share
     seed: int = 0
 
@@ -110,7 +111,8 @@ class MoeConfig:
 
 
 # The five workloads: one tiny replicated layer, three prefill-sized slices
-# and one decode-sized slice at two batch sizes.  Seeds are 1000 + index.
+# (the Qwen-shaped one also in a skew-stress variant) and one decode-sized
+# slice at two batch sizes.  Seeds are 1000 + index.
 CONFIGS = {
     "c1": MoeConfig("tiny-replicated", T=64, H=256, E=8, k=2, I=512, P=1,
                     layout="replicated", seed=1000),
@@ -120,6 +122,10 @@ CONFIGS = {
                     P=8, layout="ep", seed=1002),
     "c4": MoeConfig("qwen-moe-ep8-slice-zipf", T=8192, H=2048, E=128, k=8,
                     I=768, P=8, layout="ep", zipf_s=1.2, seed=1003),
+    # stress variant of the Qwen-shaped slice: popularity follows the expert
+    # id, so rank 0's 16 experts are the 16 most popular (about 56k pairs)
+    "c4h": MoeConfig("qwen-moe-ep8-slice-zipf-hot", T=8192, H=2048, E=128, k=8,
+                     I=768, P=8, layout="ep", zipf_s=1.2, zipf_hot=True, seed=1003),
     "c5a": MoeConfig("dsv3-ep8-decode-t64", T=64, H=7168, E=256, k=8, I=2048,
                      P=8, layout="ep", shared=True, seed=1004),
     "c5b": MoeConfig("dsv3-ep8-decode-t512", T=512, H=7168, E=256, k=8,
@@ -201,10 +207,14 @@ def make_router(cfg: MoeConfig) -> np.ndarray:
 
 def zipf_bias(cfg: MoeConfig) -> np.ndarray:
     """Log of a Zipf(s) popularity over experts, up to a constant:
-    bias_e = -s * ln(pi(e)) with pi a seeded permutation of 1..E."""
+    bias_e = -s * ln(pi(e)) with pi a seeded permutation of 1..E (the
+    identity with zipf_hot: expert 0 the most popular)."""
     if cfg.zipf_s is None:
         return np.zeros(cfg.E, dtype=np.float32)
-    perm = _rng(cfg.seed, _TAG_ZIPF).permutation(cfg.E) + 1
+    if cfg.zipf_hot:
+        perm = np.arange(cfg.E) + 1
+    else:
+        perm = _rng(cfg.seed, _TAG_ZIPF).permutation(cfg.E) + 1
     return (-cfg.zipf_s * np.log(perm.astype(np.float64))).astype(np.float32)
 
 

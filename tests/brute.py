@@ -67,3 +67,13 @@ def dense_layer(x, logits, k, w13, w2, e0, El):
         a = g / (1.0 + np.exp(-g)) * u
         out += gate[:, le:le + 1] * (a @ bf16(w2[le]).T)
     return out
+
+
+def swiglu_mlp(x, w13, w2):
+    """A dense SwiGLU MLP on every row of x (fp64 matmuls): w13 [2I, H] holds
+    the gate rows, then the up rows; w2 [H, I]."""
+    xf = bf16(x)
+    W = bf16(w13)
+    I = W.shape[0] // 2
+    g, u = xf @ W[:I].T, xf @ W[I:].T
+    return (g / (1.0 + np.exp(-g)) * u) @ bf16(w2).T

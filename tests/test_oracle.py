@@ -170,23 +170,90 @@ def test_shared_expert_partials(oracle):
 
 
 # --------------------------------------------------------- stage functions
-def test_grouped_ffn_stage_rows(oracle):
-    cfg = tiny(E=4, k=2, T=19, H=24, I=16)
+# bf16 rounding (round to nearest even, 8 significant bits: unit roundoff
+# 2^-8) moves a value by at most 2^-8 of its magnitude; a double first
+# rounded to fp32 adds 2^-24, and the fp32 gate weight another 2^-24.
+BF16_REL = 2.0 ** -8 + 2.0 ** -22
+
+
+def to_bf16(y):
+    return mi.f32_to_bf16_bits(np.asarray(y, np.float64).astype(np.float32))
+
+
+COMPOSE_CFGS = [
+    tiny(),
+    tiny(E=16, k=2, T=13, H=24, I=16, seed=3),            # several local experts with no rows
+    tiny(E=8, k=2, P=2, layout="tp", rank=1, I=32),
+    tiny(E=8, k=3, P=4, layout="ep", rank=2),
+    tiny(E=16, k=4, P=4, layout="ep", rank=3, H=48, I=40, T=31),
+    tiny(E=8, k=2, T=16, H=32, I=16, seed=5, shared=True, P=4, layout="ep", rank=1),
+]
+
+
+@pytest.mark.parametrize("cfg", COMPOSE_CFGS, ids=lambda c: f"{c.layout}{c.P}r{c.rank}E{c.E}k{c.k}T{c.T}")
+def test_stages_compose_to_dense_layer(oracle, cfg):
+    """The oracle's stages chained as the library chains its calls (route,
+    permute, row gather, grouped FFN, combine, with the shared expert as a
+    one-expert grouped FFN) give the layer of the dense evaluation: every
+    expert on every token, masked by the top-k selection (the same function
+    whatever the layout, Sec. 1 and Sec. 3).  The stage boundary carries y
+    in bf16 and the gate weights in fp32, so each output element may differ
+    from the dense fp64 value by at most the rounding of its terms:
+    sum_j w_j |y_j| 2^-8 (+ |shared| 2^-8)."""
     inp = mi.make_inputs(cfg)
-    ids, _ = oracle.route(inp.logits, cfg.k)
-    _, offsets, r2p, _ = oracle.permute(ids, 0, cfg.E)
-    x_perm = inp.x[r2p // cfg.k]
-    y = oracle.grouped_ffn(x_perm, offsets, inp.w13, inp.w2)
-    for le in range(cfg.E):
-        rows = slice(offsets[le], offsets[le + 1])
-        xf = brute.bf16(x_perm[rows])
-        W = brute.bf16(inp.w13[le])
-        g, u = xf @ W[:cfg.I].T, xf @ W[cfg.I:].T
-        ref = (g / (1 + np.exp(-g)) * u) @ brute.bf16(inp.w2[le]).T
-        np.testing.assert_allclose(y[rows], ref, rtol=0, atol=1e-13 * max(1e-30, np.abs(ref).max()))
+    ids, w = oracle.route(inp.logits, cfg.k)
+    _, offsets, r2p, p2r = oracle.permute(ids, cfg.e0, cfg.E_l)
+    y = oracle.grouped_ffn(inp.x[r2p // cfg.k], offsets, inp.w13, inp.w2)     # [n, H] fp64
+    sb, sc = cfg.shared_begin, cfg.shared_count
+    sy = None
+    ref = brute.dense_layer(inp.x, inp.logits, cfg.k, inp.w13, inp.w2, cfg.e0, cfg.E_l)
+    bound = np.zeros_like(ref)
+    if sc:
+        sy64 = oracle.grouped_ffn(inp.x[sb:sb + sc], np.array([0, sc], np.int32), inp.sw13, inp.sw2)
+        sy = to_bf16(sy64)
+        dense_sh = brute.swiglu_mlp(inp.x[sb:sb + sc], inp.sw13[0], inp.sw2[0])
+        ref[sb:sb + sc] += dense_sh
+        bound[sb:sb + sc] += np.abs(dense_sh) * BF16_REL
+    out = oracle.combine(to_bf16(y), p2r, w.astype(np.float32), cfg.T, cfg.k, shared_y=sy, sb=sb, sc=sc)
+    # rounding bound of the routed terms, from the dense side's own values
+    wb = brute.route_weights(inp.logits, brute.topk_lexsort(inp.logits, cfg.k))
+    idsb = brute.topk_lexsort(inp.logits, cfg.k)
+    xf = brute.bf16(inp.x)
+    for le in range(cfg.E_l):
+        tok, slot = np.nonzero(idsb == cfg.e0 + le)
+        if tok.size:
+            ye = brute.swiglu_mlp(inp.x[tok], inp.w13[le], inp.w2[le])
+            bound[tok] += wb[tok, slot][:, None] * np.abs(ye) * BF16_REL
+    assert xf.shape == ref.shape
+    scale = np.abs(ref).max()
+    # the bound is loose only by the factor between actual and worst-case
+    # rounding; a wrong row or weight moves an element by about |y|
+    assert scale > 0
+    err = np.abs(out - ref)
+    assert np.all(err <= bound * (1 + 1e-9) + 1e-12 * scale), float((err - bound).max())
 
 
-def test_combine_stage(oracle):
+def test_combine_relabelled_rows(oracle):
+    """The combine reads each pair's row through pair_to_row only: storing
+    the rows of y in another order (and pair_to_row with them) gives the
+    same output bit for bit."""
+    T, k, H, E = 23, 3, 16, 6
+    ids = mi.random_topk_ids(T, E, k, seed=2)
+    _, offsets, r2p, p2r = oracle.permute(ids, 2, 3)
+    n = int(offsets[-1])
+    y = mi.random_bf16((n, H), seed=4)
+    w = mi.random_gate_weights(T, k, seed=4)
+    sigma = np.random.default_rng(1).permutation(n)        # new row of old row r: sigma[r]
+    y2 = np.empty_like(y)
+    y2[sigma] = y
+    p2r2 = np.where(p2r >= 0, sigma[np.maximum(p2r, 0)], -1).astype(np.int32)
+    np.testing.assert_array_equal(oracle.combine(y, p2r, w, T, k), oracle.combine(y2, p2r2, w, T, k))
+
+
+def test_combine_accumulate_and_shared_are_additive(oracle):
+    """accumulate adds the prior output and the shared term adds shared_y on
+    its token rows only, each with weight one; tokens with no local pair,
+    no shared row and no prior are exactly zero."""
     T, k, H, E = 23, 3, 16, 6
     ids = mi.random_topk_ids(T, E, k, seed=2)
     _, offsets, r2p, p2r = oracle.permute(ids, 2, 3)
@@ -195,20 +262,40 @@ def test_combine_stage(oracle):
     w = mi.random_gate_weights(T, k, seed=4)
     shared = mi.random_bf16((5, H), seed=9)
     prior = mi.random_bf16((T, H), seed=10)
-    out = oracle.combine(y, p2r, w, T, k, shared_y=shared, sb=7, sc=5, accumulate=1, prior=prior)
-    ref = brute.bf16(prior).copy()
-    ref[7:12] += brute.bf16(shared)
-    yf = brute.bf16(y)
-    for t in range(T):
-        for j in range(k):
-            r = p2r[t * k + j]
-            if r >= 0:
-                ref[t] += float(w[t, j]) * yf[r]
-    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
-    # untouched tokens give exactly zero without accumulate/shared
-    out0 = oracle.combine(y, p2r, w, T, k)
+    base = oracle.combine(y, p2r, w, T, k)
+    full = oracle.combine(y, p2r, w, T, k, shared_y=shared, sb=7, sc=5, accumulate=1, prior=prior)
+    extra = brute.bf16(prior).copy()
+    extra[7:12] += brute.bf16(shared)
+    np.testing.assert_allclose(full - base, extra, rtol=0, atol=1e-12)
     untouched = np.all(p2r.reshape(T, k) < 0, axis=1)
-    assert np.all(out0[untouched] == 0.0)
+    assert untouched.any() and np.all(base[untouched] == 0.0)
+    # a token whose every slot is local is the sum of its slots' weighted rows:
+    # scaling all weights by 2 doubles the routed part exactly
+    np.testing.assert_array_equal(oracle.combine(y, p2r, 2 * w, T, k), 2 * base)
+
+
+def test_grouped_ffn_experts_are_independent(oracle):
+    """Each expert's rows depend only on that expert's weights: the grouped
+    call over all experts equals one single-expert call per expert, and
+    changing one expert's weights changes only its rows."""
+    cfg = tiny(E=4, k=2, T=19, H=24, I=16)
+    inp = mi.make_inputs(cfg)
+    ids, _ = oracle.route(inp.logits, cfg.k)
+    _, offsets, r2p, _ = oracle.permute(ids, 0, cfg.E)
+    x_perm = inp.x[r2p // cfg.k]
+    y = oracle.grouped_ffn(x_perm, offsets, inp.w13, inp.w2)
+    for le in range(cfg.E):
+        a, b = int(offsets[le]), int(offsets[le + 1])
+        one = oracle.grouped_ffn(x_perm[a:b], np.array([0, b - a], np.int32), inp.w13[le:le + 1],
+                                 inp.w2[le:le + 1])
+        np.testing.assert_array_equal(y[a:b], one)
+    w13b = inp.w13.copy()
+    w13b[2] = mi.random_bf16(w13b[2].shape, seed=3, std=0.02)
+    y2 = oracle.grouped_ffn(x_perm, offsets, w13b, inp.w2)
+    other = np.ones(len(y), bool)
+    other[offsets[2]:offsets[3]] = False
+    np.testing.assert_array_equal(y2[other], y[other])
+    assert offsets[3] > offsets[2] and np.any(y2[~other] != y[~other])
 
 
 # ------------------------------------------------------------- workloads
@@ -218,6 +305,7 @@ def test_config_geometry():
     assert (c["c3"].E_l, c["c3"].I_s, c["c3"].e0) == (1, 14336, 0)
     assert (c["c4"].E_l, c["c4"].I_s, c["c4"].cap) == (16, 768, 65536)
     assert (c["c5a"].E_l, c["c5a"].shared_count, c["c5b"].shared_count) == (32, 8, 64)
+    assert (c["c4h"].E_l, c["c4h"].e0, c["c4h"].zipf_hot) == (16, 0, True)
     for cfg in c.values():
         cfg.validate()
 
@@ -232,6 +320,16 @@ def test_generator_slices_concatenate_to_full_weight():
     u = np.concatenate([p[0][Is:] for p in parts])
     np.testing.assert_array_equal(np.concatenate([g, u]), full13)
     np.testing.assert_array_equal(np.concatenate([p[1] for p in parts], axis=1), full2)
+
+
+def test_zipf_hot_bias_follows_expert_id():
+    """The stress variant's popularity rank is the expert id: bias_e =
+    -s ln(e + 1), largest for expert 0; the seeded variant permutes the
+    same values."""
+    hot, seeded = mi.zipf_bias(mi.CONFIGS["c4h"]), mi.zipf_bias(mi.CONFIGS["c4"])
+    np.testing.assert_allclose(hot, -1.2 * np.log(np.arange(1, 129)), rtol=1e-6)
+    assert np.all(np.diff(hot) < 0)
+    np.testing.assert_array_equal(np.sort(seeded), np.sort(hot))
 
 
 def test_bf16_rounding_is_nearest_even():

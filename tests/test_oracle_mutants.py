@@ -29,7 +29,17 @@ MUTANTS = {
     "shared_range_off_by_one": [("if (sc > 0 && t >= sb && t < sb + sc)", "if (sc > 0 && t >= sb && t <= sb + sc)")],
     "layer_skips_weight": [("o[h] += w[t * k + j] * y[h];", "o[h] += y[h];")],
     "permute_total_off_by_one": [("offsets[El] = (int32_t)n;", "offsets[El] = (int32_t)n - 1;")],
+    # the grouped FFN's row -> expert lookup takes the first row of the next
+    # expert as its own last row
+    "ffn_lookup_boundary": [("while (!(offsets[le] <= r && r < offsets[le + 1])) ++le;",
+                             "while (!(offsets[le] <= r && r <= offsets[le + 1])) ++le;")],
+    # the combine reads the row of the token's first slot for every slot
+    "combine_reads_slot0_row": [("int32_t r = pair_to_row[t * k + j];", "int32_t r = pair_to_row[t * k];")],
 }
+
+# mutants that only the composition of the stages against the dense layer
+# can see (the stage functions have no other value pin)
+COMPOSITION_ONLY = ("ffn_lookup_boundary", "combine_reads_slot0_row")
 
 PIN_SUITE = [
     lambda o: [pins.test_route_ids_match_lexsort(o, E, k, kind)
@@ -39,8 +49,10 @@ PIN_SUITE = [
     lambda o: pins.test_layer_matches_dense_masked_evaluation(o, pins.tiny(E=8, k=3, P=4, layout="ep", rank=2)),
     lambda o: pins.test_layer_matches_dense_masked_evaluation(o, pins.tiny(E=8, k=2, P=2, layout="tp", rank=1, I=32)),
     lambda o: pins.test_shared_expert_partials(o),
-    lambda o: pins.test_combine_stage(o),
-    lambda o: pins.test_grouped_ffn_stage_rows(o),
+    lambda o: [pins.test_stages_compose_to_dense_layer(o, c) for c in pins.COMPOSE_CFGS],
+    lambda o: pins.test_combine_relabelled_rows(o),
+    lambda o: pins.test_combine_accumulate_and_shared_are_additive(o),
+    lambda o: pins.test_grouped_ffn_experts_are_independent(o),
 ]
 
 
@@ -49,8 +61,7 @@ def test_unmutated_source_passes_suite(oracle):
         pin(oracle)
 
 
-@pytest.mark.parametrize("name", sorted(MUTANTS))
-def test_pins_reject_mutant(tmp_path, name):
+def build_mutant(tmp_path, name):
     src = open(SRC).read()
     for old, new in MUTANTS[name]:
         assert src.count(old) >= 1, f"mutation anchor missing: {old!r}"
@@ -59,11 +70,27 @@ def test_pins_reject_mutant(tmp_path, name):
     msrc.write_text(src)
     lib = str(tmp_path / "libmutant.so")
     oracle_pkg.build(str(msrc), lib)
-    mut = oracle_pkg.Oracle(lib)
-    caught = 0
-    for pin in PIN_SUITE:
-        try:
-            pin(mut)
-        except (AssertionError, ValueError, IndexError):
-            caught += 1
+    return oracle_pkg.Oracle(lib)
+
+
+def rejects(pin, mut) -> bool:
+    try:
+        pin(mut)
+    except (AssertionError, ValueError, IndexError):
+        return True
+    return False
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_reject_mutant(tmp_path, name):
+    mut = build_mutant(tmp_path, name)
+    caught = sum(rejects(pin, mut) for pin in PIN_SUITE)
     assert caught > 0, f"no pin rejects mutant {name}"
+
+
+@pytest.mark.parametrize("name", COMPOSITION_ONLY)
+def test_composition_pin_alone_rejects(tmp_path, name):
+    """The stage functions' slips are caught by the composition pin itself
+    (not only by some other pin of the suite)."""
+    mut = build_mutant(tmp_path, name)
+    assert rejects(lambda o: [pins.test_stages_compose_to_dense_layer(o, c) for c in pins.COMPOSE_CFGS], mut)
