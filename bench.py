@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 METRIC = "MoE-layer tokens/s per GPU + % bf16 MFMA peak (prefill) / % HBM BW (decode)"
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+REPLAYS = 10                # graph replays of the K steps (step time = median over them)
 
 
 def log(*a):
@@ -86,9 +87,33 @@ def measured_traffic(workload: str, per: str = "dispatch"):
         return None
 
 
-def cpu_baseline(inp, target_s: float):
+def cpu_model() -> str:
+    """The host CPU's model name (lscpu), for the oracle's timing line."""
+    try:
+        import subprocess
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.lower().startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except Exception:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def oracle_flops(cfg, ids, tokens) -> float:
+    """Flops of the layer on `tokens`: 6 H I_s per local pair, 6 H I per
+    shared-expert row."""
+    t = np.asarray(tokens, np.int64)
+    sel = ids[t]
+    pairs = int(((sel >= cfg.e0) & (sel < cfg.e0 + cfg.E_l)).sum())
+    sh = int(((t >= cfg.shared_begin) & (t < cfg.shared_begin + cfg.shared_count)).sum()) if cfg.shared else 0
+    return 6.0 * cfg.H * cfg.I_s * pairs + 6.0 * cfg.H * cfg.I * sh
+
+
+def cpu_baseline(inp, target_s: float, runs: int = 3):
     """The CPU oracle, timed on a bounded sample of the workload's tokens
-    (routing, permutation, expert FFNs and combine for those tokens)."""
+    (routing, permutation, expert FFNs and combine for those tokens): the
+    median of `runs` runs, or one run when one takes more than 10 s."""
     from oracle import Oracle, build
     build()
     orc = Oracle()
@@ -111,10 +136,35 @@ def cpu_baseline(inp, target_s: float):
     per_tok = max(dt / len(probe), 1e-6)
     S = int(min(cfg.T, max(8, target_s / per_tok)))
     sample = np.sort(g.choice(cfg.T, size=S, replace=False)).astype(np.int64)
-    dt = run(sample)
+    times = [run(sample)]
+    while len(times) < runs and times[0] <= 10.0:
+        times.append(run(sample))
+    dt = float(np.median(times))
+    fl = oracle_flops(cfg, ids, sample)
+    how = f"median of {len(times)} runs" if len(times) > 1 else "one run"
     return dict(value=S / (cfg.P * dt), unit="tokens/s", cores=orc.threads(), kind="oracle",
                 sample=f"{S} of {cfg.T} tokens: expert FFNs + combine for those tokens, plus "
-                       f"routing+permutation of all tokens scaled by {S}/{cfg.T}; fp64; {dt:.1f} s", seconds=dt, slice_tokens_per_s=S / dt)
+                       f"routing+permutation of all tokens scaled by {S}/{cfg.T}; fp64; {dt:.2f} s ({how})",
+                seconds=dt, slice_tokens_per_s=S / dt, gflops=fl / dt / 1e9, runs=len(times))
+
+
+def cpu_single_thread_c1(mi):
+    """The tiny replicated layer (all 64 tokens) on one oracle thread:
+    median of 3 runs, in seconds."""
+    from oracle import Oracle
+    orc = Oracle()
+    inp = mi.make_inputs(mi.CONFIGS["c1"])
+    n = orc.threads()
+    orc.set_threads(1)
+    try:
+        ts = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            orc.layer(inp)
+            ts.append(time.perf_counter() - t0)
+    finally:
+        orc.set_threads(n)
+    return float(np.median(ts))
 
 
 # xGMI of one MI355X: 7 links of about 153 GB/s each way to the 7 peers of
@@ -334,6 +384,187 @@ def kvmove_bench(args, torch, moe):
                           "frac_of_copy": gbs / copy_gbs}), flush=True)
 
 
+def measure(cfg, args, torch, mi, moe, headline: bool):
+    """One workload: warmup, a host-launched kernel timing pass (per-kernel
+    HIP events recorded by the library on its own stream), then the step
+    captured in a HIP graph and replayed K times, each replay timed with
+    events; the step time is the median replay.  Returns the measurement,
+    the inputs and the algorithmic work."""
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    inp = mi.make_inputs(cfg)
+    log(f"[bench] inputs for {cfg.name} in {time.time() - t0:.1f}s")
+
+    def up(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+    x = up(inp.x)
+    logits = torch.from_numpy(inp.logits).to(dev)
+    layer = moe.MoeLayer(cfg.T, cfg.E, cfg.k, cfg.e0, up(inp.w13), up(inp.w2),
+                         up(inp.sw13) if cfg.shared else None, up(inp.sw2) if cfg.shared else None,
+                         cfg.shared_begin, cfg.shared_count)
+    for _ in range(args.warmup):
+        layer.forward(x, logits)
+    torch.cuda.synchronize()
+    if headline and args.copy_calib_mib:
+        # a plain copy of known size: its FETCH_SIZE / WRITE_SIZE calibrate the counters
+        src = torch.empty(args.copy_calib_mib << 19, dtype=torch.int16, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    counts = layer.bufs["counts"].cpu().numpy()
+    work = algorithmic_work(cfg, counts)
+
+    step = lambda: layer.forward(x, logits)  # noqa: E731
+
+    # Kernel timing pass: K steps launched from the host, every kernel
+    # bracketed by HIP events on its own stream (the library records them);
+    # the roofline's kernel durations come from here.
+    moe.timing_reset()
+    moe.timing_enable(True)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    eager_ms = (time.perf_counter() - t_start) * 1e3 / args.steps
+    moe.timing_enable(False)
+
+    replay_ms = []
+    single_ms = None
+    if args.eager:
+        ms_per_step = eager_ms
+    else:
+        # Throughput pass: the K steps captured back to back in one HIP graph
+        # (the kernels run without host launch gaps, as a layer does inside a
+        # model's captured forward), replayed REPLAYS times; the step time is
+        # the median over the replays of replay time / K.  Event records are
+        # not captured (ROCm graphs have no timed event nodes), which is why
+        # the kernel durations come from the pass above.
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(args.steps):
+                step()
+        graph.replay()  # untimed: first replay of the graph
+        torch.cuda.synchronize()
+        for _ in range(REPLAYS):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            graph.replay()
+            b.record()
+            torch.cuda.synchronize()
+            replay_ms.append(a.elapsed_time(b) / args.steps)
+        ms_per_step = float(np.median(replay_ms))
+        del graph
+        # Latency view: one step per graph, replayed K times in a row with an
+        # event between consecutive replays (replay i takes from event i to
+        # event i+1; the host queues replays faster than the GPU runs them).
+        # Each replay ends the graph, whose completion writes back the step's
+        # outputs from the caches: reported beside the throughput figure.
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        graph.replay()
+        torch.cuda.synchronize()
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 2)]
+        graph.replay()  # keeps the stream busy while the timed replays are queued
+        marks[0].record()
+        for i in range(args.steps + 1):
+            graph.replay()
+            marks[i + 1].record()
+        torch.cuda.synchronize()
+        # the first timed replay may still have waited for the host: dropped
+        single_ms = float(np.median([marks[i].elapsed_time(marks[i + 1]) for i in range(1, args.steps + 1)]))
+        del graph
+
+    # Cold steps: a 512 MiB buffer is written before each step (outside the
+    # timed span), so the step finds no weights in L2 or the 256 MB MALL.
+    cold_ms = None
+    if headline and args.cold_steps > 0:
+        scratch = torch.empty(256 << 20, dtype=torch.int16, device=dev)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.cold_steps)]
+        for i, (a, b) in enumerate(ev):
+            scratch.fill_(i)
+            a.record()
+            step()
+            b.record()
+        torch.cuda.synchronize()
+        cold_ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+        del scratch
+
+    kern = {}
+    for kind in moe.binding.KERNEL_KINDS:
+        ms, n = moe.timing_read(kind)
+        if n:
+            kern[kind] = dict(avg_us=1e3 * ms / n, launches=n)
+    log(f"[bench] {cfg.name}: step {ms_per_step:.4f} ms (median of {len(replay_ms)} replays of a "
+        f"{args.steps}-step graph; {single_ms or 0:.4f} per one-step graph); kernels: " +
+        ", ".join(f"{k}={v['avg_us']:.1f}us x{v['launches']}" for k, v in kern.items()))
+
+    decode = cfg.name.startswith("dsv3")
+    # dominant kernel: the gate-up GEMM (2/3 of the flops and of the weight
+    # bytes); its launches per step (the routed experts and, where present,
+    # the shared expert) are summed.  Prefill is priced on MFMA, decode
+    # (a few rows per expert, weights streamed once) on HBM.
+    dom = "gate_up"
+    gu = kern.get(dom)
+    roof = None
+    if gu is not None:
+        dur_s = gu["avg_us"] * 1e-6 * gu["launches"] / args.steps   # kernel time per step
+        if decode:
+            achieved = work["gate_up_bytes"] / dur_s / 1e9
+            roof = dict(bound="hbm", achieved=achieved, peak=PEAK_HBM_GBS, unit="GB/s",
+                        frac=achieved / PEAK_HBM_GBS, traffic=measured_traffic(cfg.name, "step"), kernel=dom,
+                        launches_per_step=gu["launches"] // args.steps,
+                        algorithmic_per_step=work["gate_up_bytes"])
+        else:
+            achieved = work["gate_up_flops"] / dur_s / 1e12
+            roof = dict(bound="mfma", achieved=achieved, peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                        frac=achieved / PEAK_BF16_TFLOPS, traffic=measured_traffic(cfg.name), kernel=dom,
+                        algorithmic_per_launch=work["gate_up_flops"],
+                        algorithmic_bytes_per_launch=work["gate_up_bytes"])
+    step_s = ms_per_step * 1e-3
+    res = {
+        "ms_per_step": ms_per_step,
+        "ms_per_step_replays": replay_ms,
+        "ms_per_step_single_step_graph": single_ms,
+        "value": cfg.T / (cfg.P * step_s),
+        "slice_tokens_per_s": cfg.T / step_s,
+        "pairs_per_s": work["n"] / step_s,
+        "chain_tflops": work["flops"] / step_s / 1e12,
+        "chain_frac_mfma": work["flops"] / step_s / 1e12 / PEAK_BF16_TFLOPS,
+        "chain_gbs": work["bytes"] / step_s / 1e9,
+        "chain_frac_hbm": work["bytes"] / step_s / 1e9 / PEAK_HBM_GBS,
+        "kernels_us": {k: round(v["avg_us"], 2) for k, v in kern.items()},
+        "eager_ms_per_step": eager_ms,
+        "cold_ms_per_step": cold_ms,
+        "roofline": roof,
+    }
+    return res, inp, work, layer
+
+
+def config_block(cfg, work, graph: bool):
+    return {"workload": cfg.name, "T": cfg.T, "H": cfg.H, "E": cfg.E, "k": cfg.k,
+            "I": cfg.I, "I_s": cfg.I_s, "P": cfg.P, "layout": cfg.layout, "rank": cfg.rank,
+            "local_experts": cfg.E_l, "local_pairs": work["n"], "active_experts": work["active"],
+            "shared_expert": cfg.shared, "global_batch": cfg.T, "parallelism": "single-gpu-slice",
+            "graph": graph, "seed": cfg.seed}
+
+
+# Workloads measured beside the headline one in the default run, with a
+# shorter oracle sample each: the other prefill slices and both decode
+# batch sizes (the metric's HBM half).
+PER_CONFIG = ("c3", "c4", "c4h", "c5a", "c5b")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -343,9 +574,13 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--eager", action="store_true",
                     help="report the host-launched kernel timing pass as the step time instead of "
-                         "a replay of the K steps from one captured HIP graph")
+                         "graph replays of the step")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--per-config-cpu-seconds", type=float, default=2.0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--per-config", default=None,
+                    help="comma-separated workloads measured beside the headline one "
+                         "(default: the others of the five configs when --config is c2; 'none' skips)")
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="steps timed one by one after writing a 512 MiB buffer (caches flushed); 0 skips")
     ap.add_argument("--no-ceilings", action="store_true",
@@ -384,118 +619,10 @@ def main():
         return
     cfg = mi.CONFIGS[args.config]
     cfg = cfg.with_(seed=cfg.seed + args.seed)
-    t0 = time.time()
-    inp = mi.make_inputs(cfg)
-    log(f"[bench] inputs for {cfg.name} in {time.time() - t0:.1f}s")
     dev = torch.device("cuda:0")
-
-    def up(a):
-        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
-    x = up(inp.x)
-    logits = torch.from_numpy(inp.logits).to(dev)
-    layer = moe.MoeLayer(cfg.T, cfg.E, cfg.k, cfg.e0, up(inp.w13), up(inp.w2),
-                         up(inp.sw13) if cfg.shared else None, up(inp.sw2) if cfg.shared else None,
-                         cfg.shared_begin, cfg.shared_count)
-    for _ in range(args.warmup):
-        layer.forward(x, logits)
-    torch.cuda.synchronize()
-    if args.copy_calib_mib:
-        # a plain copy of known size: its FETCH_SIZE / WRITE_SIZE calibrate the counters
-        src = torch.empty(args.copy_calib_mib << 19, dtype=torch.int16, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-    counts = layer.bufs["counts"].cpu().numpy()
-    work = algorithmic_work(cfg, counts)
-
-    step = lambda: layer.forward(x, logits)  # noqa: E731
-    dom = "gate_up"  # the dominant kernel (see the roofline below)
-
-    # Kernel timing pass: K steps launched from the host, every kernel
-    # bracketed by HIP events on its own stream (the library records them);
-    # the roofline's kernel durations come from here.
-    moe.timing_reset()
-    moe.timing_enable(True)
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    eager_ms = (time.perf_counter() - t_start) * 1e3 / args.steps
-    moe.timing_enable(False)
-
-    if args.eager:
-        ms_per_step = eager_ms
-    else:
-        # Throughput pass: the K steps captured into one HIP graph and
-        # replayed once (the kernels run back to back, without host launch
-        # gaps).  Event records are not captured (ROCm graphs have no timed
-        # event nodes), which is why the kernel durations come from the pass
-        # above.
-        side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            step()
-        torch.cuda.current_stream().wait_stream(side)
-        torch.cuda.synchronize()
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            for _ in range(args.steps):
-                step()
-        graph.replay()  # untimed: first replay of the graph
-        torch.cuda.synchronize()
-        t_start = time.perf_counter()
-        graph.replay()
-        torch.cuda.synchronize()
-        ms_per_step = (time.perf_counter() - t_start) * 1e3 / args.steps
-
-    # Cold steps: a 512 MiB buffer is written before each step (outside the
-    # timed span), so the step finds no weights in L2 or the 256 MB MALL.
-    cold_ms = None
-    if args.cold_steps > 0:
-        scratch = torch.empty(256 << 20, dtype=torch.int16, device=dev)
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(args.cold_steps)]
-        for i, (a, b) in enumerate(ev):
-            scratch.fill_(i)
-            a.record()
-            step()
-            b.record()
-        torch.cuda.synchronize()
-        cold_ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
-        del scratch
-
-    kern = {}
-    for kind in moe.binding.KERNEL_KINDS:
-        ms, n = moe.timing_read(kind)
-        if n:
-            kern[kind] = dict(avg_us=1e3 * ms / n, launches=n)
-    log("[bench] kernels: " + ", ".join(f"{k}={v['avg_us']:.1f}us x{v['launches']}" for k, v in kern.items()))
-
+    res, inp, work, layer = measure(cfg, args, torch, mi, moe, headline=True)
+    roof = res["roofline"]
     decode = cfg.name.startswith("dsv3")
-    # dominant kernel: the gate-up GEMM (2/3 of the flops and of the weight
-    # bytes); its launches per step (the routed experts and, where present,
-    # the shared expert) are summed.  Prefill is priced on MFMA, decode
-    # (a few rows per expert, weights streamed once) on HBM.
-    gu = kern.get(dom)
-    if gu is not None:
-        dur_s = gu["avg_us"] * 1e-6 * gu["launches"] / args.steps   # kernel time per step
-        if decode:
-            achieved = work["gate_up_bytes"] / dur_s / 1e9
-            roof = dict(bound="hbm", achieved=achieved, peak=PEAK_HBM_GBS, unit="GB/s",
-                        frac=achieved / PEAK_HBM_GBS, traffic=measured_traffic(cfg.name, "step"), kernel=dom,
-                        launches_per_step=gu["launches"] // args.steps,
-                        algorithmic_per_step=work["gate_up_bytes"])
-        else:
-            achieved = work["gate_up_flops"] / dur_s / 1e12
-            roof = dict(bound="mfma", achieved=achieved, peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
-                        frac=achieved / PEAK_BF16_TFLOPS, traffic=measured_traffic(cfg.name), kernel=dom,
-                        algorithmic_per_launch=work["gate_up_flops"],
-                        algorithmic_bytes_per_launch=work["gate_up_bytes"])
-    else:
-        roof = None
 
     # Measured ceilings on this GPU (references, not part of the path): the
     # vendor GEMM (torch.matmul, hipBLASLt) on the dense shape of the
@@ -532,42 +659,69 @@ def main():
             if roof["bound"] == "hbm":
                 roof["frac_of_copy"] = roof["achieved"] / ceilings["copy_gbs"]
 
-    step_s = ms_per_step * 1e-3
     result = {
         "metric": METRIC,
-        "value": cfg.T / (cfg.P * step_s),
+        "value": res["value"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": res["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": cfg.name, "T": cfg.T, "H": cfg.H, "E": cfg.E, "k": cfg.k,
-                   "I": cfg.I, "I_s": cfg.I_s, "P": cfg.P, "layout": cfg.layout, "rank": cfg.rank,
-                   "local_experts": cfg.E_l, "local_pairs": work["n"], "active_experts": work["active"],
-                   "shared_expert": cfg.shared, "global_batch": cfg.T, "parallelism": "single-gpu-slice",
-                   "graph": not args.eager, "seed": cfg.seed},
-        "slice_tokens_per_s": cfg.T / step_s,
-        "pairs_per_s": work["n"] / step_s,
-        "chain_tflops": work["flops"] / step_s / 1e12,
-        "chain_frac_mfma": work["flops"] / step_s / 1e12 / PEAK_BF16_TFLOPS,
-        "chain_gbs": work["bytes"] / step_s / 1e9,
-        "chain_frac_hbm": work["bytes"] / step_s / 1e9 / PEAK_HBM_GBS,
-        "kernels_us": {k: round(v["avg_us"], 2) for k, v in kern.items()},
-        "eager_ms_per_step": eager_ms,
-        "cold_ms_per_step": cold_ms,
-        "ceilings": ceilings,
-        "roofline": roof,
-        "cpu_baseline": None,
+        "config": config_block(cfg, work, not args.eager),
+        "timing": f"median over {REPLAYS} replays of one HIP graph of the {args.steps} steps "
+                  f"(replay time / {args.steps})" if not args.eager
+                  else f"mean of {args.steps} host-launched steps",
     }
+    result.update({k: v for k, v in res.items() if k not in ("value", "ms_per_step", "roofline")})
+    result["ceilings"] = ceilings
+    result["roofline"] = roof
+    result["cpu_baseline"] = None
+    cpu_name = cpu_model()
     if not args.no_cpu:
         cb = cpu_baseline(inp, args.cpu_seconds)
-        log(f"[bench] cpu oracle: {cb['sample']} on {cb['cores']} threads ({platform.processor() or 'cpu'})")
+        log(f"[bench] cpu oracle: {cb['sample']} on {cb['cores']} threads ({cpu_name}); "
+            f"{cb['gflops']:.2f} GFLOP/s")
+        c1_s = cpu_single_thread_c1(mi)
+        log(f"[bench] cpu oracle, tiny-replicated (64 tokens) on 1 thread: {c1_s:.3f} s")
         result["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+        result["cpu_baseline"].update(cpu=cpu_name, gflops=cb["gflops"], seconds=cb["seconds"],
+                                      c1_single_thread_s=c1_s)
+    del layer, inp
+
+    # The other workloads, each with its own step time, roofline (MFMA for
+    # prefill, HBM for decode), counter traffic where committed, and a short
+    # oracle sample timed on the same host.
+    names = args.per_config
+    if names is None:
+        names = ",".join(PER_CONFIG) if args.config == "c2" else "none"
+    per = {}
+    if names != "none":
+        for key in names.split(","):
+            c = mi.CONFIGS[key]
+            c = c.with_(seed=c.seed + args.seed)
+            r, cinp, cwork, clayer = measure(c, args, torch, mi, moe, headline=False)
+            entry = {"config": config_block(c, cwork, not args.eager),
+                     "ms_per_step": r["ms_per_step"], "value": r["value"], "unit": "tokens/s",
+                     "ms_per_step_single_step_graph": r["ms_per_step_single_step_graph"],
+                     "kernels_us": r["kernels_us"], "roofline": r["roofline"],
+                     "chain_frac_mfma": r["chain_frac_mfma"], "chain_frac_hbm": r["chain_frac_hbm"],
+                     "chain_tflops": r["chain_tflops"], "chain_gbs": r["chain_gbs"],
+                     "eager_ms_per_step": r["eager_ms_per_step"]}
+            if not args.no_cpu:
+                cb = cpu_baseline(cinp, args.per_config_cpu_seconds)
+                entry["oracle"] = {"seconds": cb["seconds"], "tokens_per_s": cb["value"],
+                                   "gflops": cb["gflops"], "cores": cb["cores"], "sample": cb["sample"]}
+                log(f"[bench] cpu oracle {c.name}: {cb['sample']}; {cb['gflops']:.2f} GFLOP/s")
+            per[c.name] = entry
+            del clayer, cinp
+            torch.cuda.empty_cache()
+    if per:
+        result["per_config"] = per
     print(json.dumps(result), flush=True)
 
 
