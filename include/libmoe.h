@@ -109,6 +109,29 @@ moe_status moe_permute(const int32_t *topk_ids, int64_t T, int k, int E, int exp
                        uint16_t *x_perm, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * The permutation without a caller workspace, for callers that cannot
+ * allocate device memory: code under HIP graph capture that must not call
+ * hipMalloc, tight serving loops, harnesses that forbid allocation.  Same
+ * arguments, outputs and errors as moe_permute, minus the workspace: the
+ * per-chunk histograms live in a static array of MOE_PERMUTE_SCRATCH_BYTES
+ * in the library, one copy per GPU held until the process ends (its address
+ * is looked up on the first call on each device).  It allocates nothing and
+ * calls no allocating routine.  Calls whose moe_permute_workspace_size(T, k,
+ * n_local_experts) exceeds MOE_PERMUTE_SCRATCH_BYTES return
+ * MOE_ERR_UNSUPPORTED and enqueue nothing (for 256-pair chunks, T*k*E_l up to
+ * 2^24, the need is at most 256 KiB; for larger inputs it is about
+ * T*k*E_l/256 bytes).  The scratch of the CURRENT device is used: `stream`
+ * must belong to it.  Every call on one GPU shares that GPU's array, so calls
+ * that overlap on one GPU (other streams, other threads, other graphs
+ * replayed concurrently) race; calls in stream order do not.  Nothing in the
+ * array needs to start at zero (each call writes every entry it reads).
+ */
+#define MOE_PERMUTE_SCRATCH_BYTES (4u << 20)
+moe_status moe_permute_noalloc(const int32_t *topk_ids, int64_t T, int k, int E, int expert_begin,
+                               int n_local_experts, int32_t *counts, int32_t *offsets, int32_t *row_to_pair,
+                               int32_t *pair_to_row, const uint16_t *x, int H, uint16_t *x_perm, void *stream);
+
+/*
  * Grouped SwiGLU expert FFN (Sec. 3.1 weight shapes).  For every local
  * expert e and every row r in [offsets[e], offsets[e+1]), with input row
  *   in_r = x[row_to_pair[r] / k]   when row_to_pair is not NULL (x is the

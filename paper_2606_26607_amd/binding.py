@@ -65,6 +65,7 @@ def lib():
         "moe_route": ([vp, i64, i32, i32, vp, vp, vp], i32),
         "moe_permute_workspace_size": ([i64, i32, i32], sz),
         "moe_permute": ([vp, i64, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, vp, vp, sz, vp], i32),
+        "moe_permute_noalloc": ([vp, i64, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, vp, vp], i32),
         "moe_ffn_workspace_size": ([i64, i32, i32, i32], sz),
         "moe_grouped_ffn": ([vp, i64, vp, i32, vp, i32, i64, i32, i32, vp, vp, vp, vp, sz, vp], i32),
         "moe_grouped_ffn_shared": ([vp, i64, vp, i32, vp, i32, i64, i32, i32, vp, vp, vp, i64, i64, vp, vp, vp,

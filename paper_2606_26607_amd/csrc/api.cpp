@@ -79,7 +79,7 @@ extern "C" const char *moe_status_str(int status)
 
 extern "C" const char *moe_last_error(void) { return g_msg; }
 
-extern "C" int moe_version(void) { return 6; }
+extern "C" int moe_version(void) { return 7; }
 
 extern "C" moe_status moe_route(const float *logits, int64_t T, int E, int k, int32_t *topk_ids,
                                 float *topk_w, void *stream)
@@ -128,6 +128,41 @@ extern "C" moe_status moe_permute(const int32_t *topk_ids, int64_t T, int k, int
                                      pair_to_row, x, H, x_perm, cap, static_cast<int32_t *>(workspace),
                                      (hipStream_t)stream),
                       "moe_permute launch");
+}
+
+extern "C" moe_status moe_permute_noalloc(const int32_t *topk_ids, int64_t T, int k, int E, int expert_begin,
+                                          int n_local_experts, int32_t *counts, int32_t *offsets,
+                                          int32_t *row_to_pair, int32_t *pair_to_row, const uint16_t *x, int H,
+                                          uint16_t *x_perm, void *stream)
+{
+    // the same checks as moe_permute, then the size bound of the static scratch
+    moe_status st = check_topk(T, E, k);
+    if (st != MOE_OK) return st;
+    const int El = n_local_experts;
+    if (El < 1 || expert_begin < 0 || expert_begin + El > E)
+        return fail(MOE_ERR_INVALID_ARG, "local experts [%d, %d+%d) not inside [0, E=%d)",
+                    expert_begin, expert_begin, El, E);
+    if (!counts || !offsets) return fail(MOE_ERR_INVALID_ARG, "moe_permute_noalloc: null counts/offsets");
+    if (T > 0 && (!topk_ids || !row_to_pair || !pair_to_row))
+        return fail(MOE_ERR_INVALID_ARG, "moe_permute_noalloc: null index array");
+    if (x_perm) {
+        if ((st = check_width("H", H)) != MOE_OK) return st;
+        if (T > 0 && !x) return fail(MOE_ERR_INVALID_ARG, "moe_permute_noalloc: x_perm given without x");
+        if (!aligned16(x) || !aligned16(x_perm))
+            return fail(MOE_ERR_INVALID_ARG, "moe_permute_noalloc: x / x_perm not 16-byte aligned");
+    }
+    const size_t need = moe_permute_workspace_size(T, k, El);
+    if (need > MOE_PERMUTE_SCRATCH_BYTES)
+        return fail(MOE_ERR_UNSUPPORTED,
+                    "moe_permute_noalloc: T=%lld, k=%d, %d local experts need %zu bytes of scratch, "
+                    "above the static %u (use moe_permute with a workspace)",
+                    (long long)T, k, El, need, (unsigned)MOE_PERMUTE_SCRATCH_BYTES);
+    int32_t *scratch = nullptr;
+    if ((st = hip_status(permute_scratch(&scratch), "moe_permute_noalloc scratch")) != MOE_OK) return st;
+    const int64_t cap = T * (k < El ? k : El);
+    return hip_status(launch_permute(topk_ids, T, k, expert_begin, El, counts, offsets, row_to_pair, pair_to_row,
+                                     x, H, x_perm, cap, scratch, (hipStream_t)stream),
+                      "moe_permute_noalloc launch");
 }
 
 extern "C" size_t moe_ffn_workspace_size(int64_t cap_rows, int n_local_experts, int H, int I_s)

@@ -53,6 +53,9 @@ hipError_t launch_route(const float *logits, int64_t T, int E, int k, int32_t *i
                         hipStream_t s);
 
 int64_t permute_chunks(int64_t T, int k, int El);
+// Device address of the current device's permutation scratch array
+// (MOE_PERMUTE_SCRATCH_BYTES), looked up once per device.
+hipError_t permute_scratch(int32_t **ptr);
 hipError_t launch_permute(const int32_t *ids, int64_t T, int k, int e0, int El, int32_t *counts,
                           int32_t *offsets, int32_t *row_to_pair, int32_t *pair_to_row,
                           const uint16_t *x, int H, uint16_t *x_perm, int64_t cap, int32_t *ws,

@@ -18,6 +18,8 @@
 // and a bounded amount of ballot work, see SMALL_WORK) run steps 1-3 in one
 // workgroup instead, saving launches; larger ones with at most 64 local
 // experts run steps 2 and 3 in one launch.
+#include <mutex>
+
 #include "moe_internal.h"
 
 namespace moe {
@@ -470,7 +472,37 @@ __global__ __launch_bounds__(256) void gather_kernel(const uint16_t *__restrict_
     }
 }
 
+// Scratch of the allocation-free entry point: the per-chunk histograms that
+// the caller's workspace holds otherwise.  Each GPU holds its own copy for
+// the life of the process; in host code the name is not a device address,
+// so the kernels get it through permute_scratch().
+static __device__ __align__(256) int32_t scratch[MOE_PERMUTE_SCRATCH_BYTES / sizeof(int32_t)];
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mtx;
+int32_t *g_scratch[MAX_DEVICES];
+
 }  // namespace
+
+hipError_t permute_scratch(int32_t **ptr)
+{
+    int dev = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return err;
+    if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mtx);
+    if (g_scratch[dev] == nullptr) {
+        // once per device, with that device current: the address of this
+        // device's copy of the array
+        void *p = nullptr;
+        err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (err != hipSuccess) return err;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        g_scratch[dev] = static_cast<int32_t *>(p);
+    }
+    *ptr = g_scratch[dev];
+    return hipSuccess;
+}
 
 int64_t permute_chunks(int64_t T, int k, int El) { return ceil_div(T * k, chunk_pairs(T * k, El)); }
 

@@ -80,6 +80,26 @@ def test_permute_rejects():
     assert call(k=17, E=32) == UNSUPPORTED
 
 
+def test_permute_noalloc_rejects():
+    """The allocation-free permutation checks what moe_permute checks, and
+    rejects on the host any size whose histograms exceed its static scratch."""
+    L = moe.lib()
+    limit = L.moe_permute_noalloc and 4 << 20
+
+    def call(T, k, E, El, ids=FAKE, counts=FAKE):
+        return L.moe_permute_noalloc(ids, T, k, E, 0, El, counts, FAKE, FAKE, FAKE, None, 0, None, None)
+    assert moe.permute_workspace_size(1 << 20, 16, 1024) > limit
+    assert call(1 << 20, 16, 1024, 1024) == UNSUPPORTED
+    assert b"scratch" in L.moe_last_error()
+    assert call(16, 2, 8, 0) == INVALID
+    assert call(16, 2, 8, 8, counts=None) == INVALID
+    assert call(16, 2, 8, 8, ids=None) == INVALID
+    assert call(16, 17, 32, 8) == UNSUPPORTED
+    # the largest accepted inputs of either chunk size stay within the scratch
+    assert moe.permute_workspace_size(1 << 18, 8, 8) <= limit          # 2^24 pair-experts: 256-pair chunks
+    assert moe.permute_workspace_size(1 << 18, 8, 256) <= limit         # 1024-pair chunks
+
+
 def test_ffn_rejects():
     L = moe.lib()
     big = 1 << 30
