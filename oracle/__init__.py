@@ -21,8 +21,10 @@ _lib = None
 def build(src: str = _SRC, out: str = LIB_PATH, extra=()) -> str:
     """Compile the oracle with gcc (plain -O2: no fast-math, so floating-point
     evaluation order is the source order)."""
-    cmd = ["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11", *extra, src, "-o", out, "-lm"]
+    tmp = f"{out}.{os.getpid()}.tmp"  # concurrent builders (test workers) each rename a whole file
+    cmd = ["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11", *extra, src, "-o", tmp, "-lm"]
     subprocess.run(cmd, check=True)
+    os.replace(tmp, out)
     return out
 
 
