@@ -30,9 +30,14 @@
  *    results are valid once that stream has been synchronised.  No call
  *    reads device data back to the host, so the chain can be captured in a
  *    HIP graph.
- *  - Arguments are validated on the host before any HIP call; a rejected
- *    call returns MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED or
+ *  - Arguments are validated on the host before anything is enqueued; a
+ *    rejected call returns MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED or
  *    MOE_ERR_WORKSPACE, enqueues nothing and leaves every buffer untouched.
+ *    Checks of sizes, pointers and limits make no HIP call.  Two lookups do:
+ *    the grouped-FFN workspace size depends on the current device's compute
+ *    unit count (moe_ffn_workspace_size, and the workspace check of
+ *    moe_grouped_ffn / moe_grouped_ffn_shared, query it), and the first
+ *    moe_permute_noalloc call on a device looks up its scratch address.
  *    A failed kernel launch returns MOE_ERR_HIP.  moe_last_error() gives a
  *    message for the last non-OK status on the calling thread.
  *  - Sizes: 1 <= E <= 1024, 1 <= k <= min(E, 16), T >= 0, T*k < 2^31,
@@ -150,7 +155,8 @@ moe_status moe_permute_noalloc(const int32_t *topk_ids, int64_t T, int k, int E,
  * Experts with no rows read none of their weights.
  * workspace: at least moe_ffn_workspace_size(cap_rows, El, H, I_s) bytes,
  * 256-byte aligned (holds the bf16 intermediate h, the tile schedule and the
- * split-K partials).
+ * split-K partials; its size depends on the current device's compute unit
+ * count, which the query reads with hipGetDevice / hipDeviceGetAttribute).
  */
 size_t moe_ffn_workspace_size(int64_t cap_rows, int n_local_experts, int H, int I_s);
 moe_status moe_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *row_to_pair, int k,

@@ -1,6 +1,7 @@
 // libmoe C ABI: host-side argument validation, then kernel launches.
-// Validation happens before any HIP call, so a rejected call enqueues
-// nothing and touches no buffer.
+// Validation happens before anything is enqueued, so a rejected call
+// touches no buffer; only the grouped-FFN workspace size queries the device
+// (its compute unit count).
 #include <stdarg.h>
 #include <stdio.h>
 

@@ -341,13 +341,19 @@ __global__ __launch_bounds__(64) void scatter_kernel(const int32_t *__restrict__
     }
 }
 
-// Steps 2 and 3 in one launch (at most 64 local experts): a block of four
+// Steps 2 and 3 in one launch (at most 64 local experts and
+// SCAN_SCATTER_MAX_CHUNKS chunks): a block of four
 // wavefronts scatters four chunks, one each, after rebuilding from the chunk
 // histograms what the scan would have handed it: each expert's total (hence
 // its first row) and the pairs of that expert in the chunks before its own.
 // Every block reads the whole histogram table (a few KB, from L2), which is
 // cheaper than a separate single-workgroup scan launch between count and
-// scatter.  Block 0 also writes counts and offsets.
+// scatter.  Block 0 also writes counts and offsets.  The table reads of all
+// blocks together grow with the square of the chunk count, so above
+// SCAN_SCATTER_MAX_CHUNKS chunks (about 1M pairs in 256-pair chunks, 4M in
+// 1024-pair chunks: 4096 chunks x 64 experts x 4 B = 1 MB read by each of
+// 1024 blocks) the separate scan and scatter launches take over.
+constexpr int64_t SCAN_SCATTER_MAX_CHUNKS = 4096;
 template <int ROUNDS>
 __global__ __launch_bounds__(256) void scan_scatter_kernel(const int32_t *__restrict__ ids, int64_t npairs,
                                                           int e0, int El, int nbits,
@@ -533,7 +539,7 @@ hipError_t launch_permute(const int32_t *ids, int64_t T, int k, int e0, int El, 
                     ids, npairs, e0, El, ws);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
-        if (El <= 64 && nchunks > 0) {
+        if (El <= 64 && nchunks > 0 && nchunks <= SCAN_SCATTER_MAX_CHUNKS) {
             // scan and scatter in one launch
             const unsigned blocks = (unsigned)ceil_div(nchunks, 4);
             if (short_chunks)

@@ -1,6 +1,7 @@
 """The C ABI without a GPU: the library loads, exports every symbol that
 include/libmoe.h declares, sizes workspaces, and rejects bad arguments on the
-host before any HIP call (so these run on a machine with no GPU)."""
+host before anything is enqueued (the checks below make no HIP call, so
+they run on a machine with no GPU)."""
 import ctypes
 import os
 import re

@@ -135,6 +135,25 @@ def test_permute_every_rank(oracle, T, E, k, P):
     assert total == T * k
 
 
+@pytest.mark.parametrize("T", [131072, 131104, 524288, 524289])
+def test_permute_chunk_count_threshold(oracle, T):
+    """Either side of the chunk count above which the scan and the scatter
+    run as separate launches (4096 chunks): 131072 x 8 pairs over 8 local
+    experts make 4096 chunks of 256 pairs and 131104 x 8 make 4097;
+    524288 x 8 and 524289 x 8 (pairs x experts above 2^24) make 4096 and
+    4097 chunks of 1024 pairs."""
+    E, k, P = 64, 8, 8
+    ids = mi.random_topk_ids(T, E, k, seed=T)
+    for r in (0, P - 1):
+        e0, El = r * (E // P), E // P
+        got = gpu_permute(ids, E, e0, El)
+        c, o, r2p, p2r = oracle.permute(ids, e0, El)
+        np.testing.assert_array_equal(got["counts"], c)
+        np.testing.assert_array_equal(got["offsets"], o)
+        np.testing.assert_array_equal(got["row_to_pair"], r2p)
+        np.testing.assert_array_equal(got["pair_to_row"], p2r)
+
+
 def test_permute_hot_expert_and_empty_experts(oracle):
     T, E, k = 4099, 16, 4
     ids = mi.random_topk_ids(T, E, k, seed=5, hot=7)
