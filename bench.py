@@ -30,6 +30,7 @@ METRIC = "MoE-layer tokens/s per GPU + % bf16 MFMA peak (prefill) / % HBM BW (de
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 REPLAYS = 10                # graph replays of the K steps (step time = median over them)
+API = ["moe_layer_forward"]  # the library entry the step calls (--four-calls: the four calls)
 
 
 def log(*a):
@@ -403,7 +404,7 @@ def measure(cfg, args, torch, mi, moe, headline: bool):
                          up(inp.sw13) if cfg.shared else None, up(inp.sw2) if cfg.shared else None,
                          cfg.shared_begin, cfg.shared_count)
     for _ in range(args.warmup):
-        layer.forward(x, logits)
+        layer.forward_calls(x, logits) if args.four_calls else layer.forward(x, logits)
     torch.cuda.synchronize()
     if headline and args.copy_calib_mib:
         # a plain copy of known size: its FETCH_SIZE / WRITE_SIZE calibrate the counters
@@ -416,7 +417,8 @@ def measure(cfg, args, torch, mi, moe, headline: bool):
     counts = layer.bufs["counts"].cpu().numpy()
     work = algorithmic_work(cfg, counts)
 
-    step = lambda: layer.forward(x, logits)  # noqa: E731
+    # one moe_layer_forward call (fused first launches), or the four calls
+    step = (lambda: layer.forward_calls(x, logits)) if args.four_calls else (lambda: layer.forward(x, logits))
 
     # Kernel timing pass: K steps launched from the host, every kernel
     # bracketed by HIP events on its own stream (the library records them);
@@ -594,6 +596,9 @@ def main():
     ap.add_argument("--kvmove", action="store_true",
                     help="instead of one workload: time the paged KV head moves of an EP->TP switch "
                          "for a decode batch (one JSON line per case)")
+    ap.add_argument("--four-calls", action="store_true",
+                    help="time the four calls (route, permute, grouped FFN, combine) instead of the one-call "
+                         "layer forward")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -608,6 +613,8 @@ def main():
     import paper_2606_26607_amd as moe
 
     assert torch.cuda.is_available(), "bench needs a GPU"
+    if args.four_calls:
+        API[0] = "moe_route+moe_permute+moe_grouped_ffn+moe_combine"
     if args.crossover:
         crossover(args, torch, mi, moe)
         return

@@ -20,6 +20,7 @@
  *
  * The forward is four calls on one stream:
  *   moe_route -> moe_permute -> moe_grouped_ffn -> moe_combine
+ * or the same in one call, moe_layer_forward, with fewer launches.
  *
  * Conventions for every call:
  *  - Array arguments are DEVICE pointers owned by the caller, row-major and
@@ -210,6 +211,39 @@ moe_status moe_combine(const uint16_t *y, int64_t y_rows, const int32_t *pair_to
                        uint16_t *out, void *stream);
 
 /*
+ * The whole layer forward in one call: exactly
+ *   moe_route(logits) -> moe_permute (no x_perm) -> moe_grouped_ffn_shared
+ *   (or moe_grouped_ffn without a shared expert; the row gather fused) ->
+ *   moe_combine (accumulate = 0, the shared rows added)
+ * with every intermediate written to the caller's buffers, bit for bit what
+ * those four calls write.  Where the shapes allow it (at most 64 local
+ * experts, the large-tile FFN shapes: H and I_s multiples of 64, at least
+ * 128), routing, the permutation and the FFN's tile schedule run in fused
+ * launches: for small inputs (at most 16384 pairs) routing, then the
+ * permutation with the schedule in one workgroup; for larger ones routing
+ * with the permutation's histogram, then its scan and scatter with the
+ * schedule: two launches instead of three or four.  Otherwise it runs the
+ * four calls' launches.
+ *   x [T, H] bf16; logits [T, E] fp32; w13, w2 and shared_w13 [2*I_s, H],
+ *   shared_w2 [H, I_s] as for moe_grouped_ffn(_shared) (the shared expert,
+ *   on token rows [shared_begin, shared_begin + shared_count), has the
+ *   routed experts' width; shared_count = 0 for none);
+ *   outputs: topk_ids, topk_w [T, k]; counts [El]; offsets [El+1];
+ *   row_to_pair [T*min(k,El)]; pair_to_row [T*k]; y [T*min(k,El), H];
+ *   shared_y [shared_count, H]; out [T, H] bf16.
+ * workspace: at least moe_layer_workspace_size(T, k, El, H, I_s,
+ * shared_count) bytes, 256-byte aligned.  Errors as for the four calls.
+ */
+size_t moe_layer_workspace_size(int64_t T, int k, int n_local_experts, int H, int I_s, int64_t shared_count);
+moe_status moe_layer_forward(const uint16_t *x, const float *logits, int64_t T, int E, int k, int expert_begin,
+                             int n_local_experts, int H, int I_s, const uint16_t *w13, const uint16_t *w2,
+                             int64_t shared_begin, int64_t shared_count, const uint16_t *shared_w13,
+                             const uint16_t *shared_w2, int32_t *topk_ids, float *topk_w, int32_t *counts,
+                             int32_t *offsets, int32_t *row_to_pair, int32_t *pair_to_row, uint16_t *y,
+                             uint16_t *shared_y, uint16_t *out, void *workspace, size_t workspace_bytes,
+                             void *stream);
+
+/*
  * Expert-weight resharding between the EP and TP views (Sec. 3.1; the
  * layout switch of Sec. 4.2-4.3), for one destination rank.  With E experts,
  * P ranks, hidden size H and expert intermediate size I:
@@ -362,7 +396,9 @@ typedef enum moe_kernel_kind {
     MOE_K_SPLITK_REDUCE = 7, /* combination of split-K partials of the large tiles (long K only) */
     MOE_K_RESHARD = 8,       /* expert-weight resharding */
     MOE_K_KV_MOVE = 9,       /* paged KV head moves (and their slot expansion) */
-    MOE_K_COUNT = 10
+    MOE_K_LAYER_PREP = 10,   /* moe_layer_forward: the fused launches of permutation and tile schedule
+                                (with routing on larger inputs; on small ones routing is timed as MOE_K_ROUTE) */
+    MOE_K_COUNT = 11
 } moe_kernel_kind;
 
 moe_status moe_timing_enable(int enable);

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libmoe.so")
 MAX_TOPK = 16
 MAX_EXPERTS = 1024
 KERNEL_KINDS = {"route": 0, "permute": 1, "gather": 2, "schedule": 3, "gate_up": 4, "down": 5,
-                "combine": 6, "splitk_reduce": 7, "reshard": 8, "kv_move": 9}
+                "combine": 6, "splitk_reduce": 7, "reshard": 8, "kv_move": 9, "layer_prep": 10}
 EP_TO_TP, TP_TO_EP = 0, 1
 MODE_TP, MODE_EP = 0, 1
 STAY, SWITCH, SWITCH_CANCELLED = 0, 1, 2
@@ -70,6 +70,9 @@ def lib():
         "moe_grouped_ffn": ([vp, i64, vp, i32, vp, i32, i64, i32, i32, vp, vp, vp, vp, sz, vp], i32),
         "moe_grouped_ffn_shared": ([vp, i64, vp, i32, vp, i32, i64, i32, i32, vp, vp, vp, i64, i64, vp, vp, vp,
                                     vp, sz, vp], i32),
+        "moe_layer_workspace_size": ([i64, i32, i32, i32, i32, i64], sz),
+        "moe_layer_forward": ([vp, vp, i64, i32, i32, i32, i32, i32, i32, vp, vp, i64, i64, vp, vp, vp, vp, vp, vp,
+                               vp, vp, vp, vp, vp, vp, sz, vp], i32),
         "moe_combine": ([vp, i64, vp, vp, i64, i32, i32, vp, i64, i64, i32, vp, vp], i32),
         "moe_reshard_experts": ([i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp], i32),
         "moe_kv_slots": ([vp, i64, vp, i32, i32, vp, i64, vp], i32),
@@ -141,6 +144,10 @@ def permute_workspace_size(T: int, k: int, n_local: int) -> int:
 
 def ffn_workspace_size(cap_rows: int, n_local: int, H: int, I_s: int) -> int:
     return int(lib().moe_ffn_workspace_size(cap_rows, n_local, H, I_s))
+
+
+def layer_workspace_size(T: int, k: int, n_local: int, H: int, I_s: int, shared_count: int = 0) -> int:
+    return int(lib().moe_layer_workspace_size(T, k, n_local, H, I_s, shared_count))
 
 
 def permute(topk_ids: torch.Tensor, E: int, expert_begin: int, n_local: int,
@@ -579,7 +586,36 @@ class MoeLayer:
                 self.ws_sh = torch.empty(ffn_workspace_size(self.sc, 1, self.H, sIs), dtype=torch.uint8,
                                          device=dev)
 
+        # the whole-layer call (fused launches) serves every layer whose shared
+        # expert, if any, shares the routed experts' launches
+        self.one_call = self.sc == 0 or self.fused_shared
+        if self.one_call:
+            self.ws_layer = torch.empty(max(layer_workspace_size(T, k, self.El, self.H, self.I_s, self.sc), 256),
+                                        dtype=torch.uint8, device=dev)
+            if self.sc == 0:
+                self.s_y = None
+
     def forward(self, x: torch.Tensor, logits: torch.Tensor, stream=None) -> torch.Tensor:
+        """The layer forward: one moe_layer_forward call where it serves the
+        layer, else the four calls."""
+        if not self.one_call:
+            return self.forward_calls(x, logits, stream)
+        _need(x, torch.bfloat16, "x", 2)
+        _need(logits, torch.float32, "logits", 2)
+        if tuple(x.shape) != (self.T, self.H) or tuple(logits.shape) != (self.T, self.E):
+            raise ValueError("x must be [T, H] and logits [T, E]")
+        b = self.bufs
+        _check(lib().moe_layer_forward(
+            _ptr(x), _ptr(logits), self.T, self.E, self.k, self.e0, self.El, self.H, self.I_s, _ptr(self.w13),
+            _ptr(self.w2), self.sb, self.sc, _ptr(self.sw13_2d) if self.sc else None,
+            _ptr(self.sw2_2d) if self.sc else None, _ptr(self.topk_ids), _ptr(self.topk_w), _ptr(b["counts"]),
+            _ptr(b["offsets"]), _ptr(b["row_to_pair"]), _ptr(b["pair_to_row"]), _ptr(self.y), _ptr(self.s_y),
+            _ptr(self.out), _ptr(self.ws_layer), self.ws_layer.numel(), _stream(stream)))
+        return self.out
+
+    def forward_calls(self, x: torch.Tensor, logits: torch.Tensor, stream=None) -> torch.Tensor:
+        """The same forward as the four calls route, permute, grouped FFN and
+        combine, each with its own launches."""
         route(logits, self.k, self.topk_ids, self.topk_w, stream=stream)
         # the permutation's row gather is fused into the gate-up GEMM
         permute(self.topk_ids, self.E, self.e0, self.El, out=self.bufs, workspace=self.ws_perm,

@@ -80,7 +80,7 @@ extern "C" const char *moe_status_str(int status)
 
 extern "C" const char *moe_last_error(void) { return g_msg; }
 
-extern "C" int moe_version(void) { return 7; }
+extern "C" int moe_version(void) { return 8; }
 
 extern "C" moe_status moe_route(const float *logits, int64_t T, int E, int k, int32_t *topk_ids,
                                 float *topk_w, void *stream)
@@ -265,6 +265,64 @@ extern "C" moe_status moe_grouped_ffn_shared(const uint16_t *x, int64_t x_rows, 
                                          w13, w2, y, shared_begin, shared_count, shared_w13, shared_w2, shared_y,
                                          workspace, (hipStream_t)stream),
                       "moe_grouped_ffn_shared launch");
+}
+
+extern "C" size_t moe_layer_workspace_size(int64_t T, int k, int n_local_experts, int H, int I_s,
+                                           int64_t shared_count)
+{
+    if (T < 0 || k < 1 || n_local_experts < 1 || H <= 0 || I_s <= 0 || shared_count < 0) return 0;
+    const int64_t cap = T * (k < n_local_experts ? k : n_local_experts);
+    const size_t perm = align256(moe_permute_workspace_size(T, k, n_local_experts));
+    return perm + moe_ffn_workspace_size(cap + shared_count, n_local_experts + (shared_count > 0 ? 1 : 0), H, I_s);
+}
+
+extern "C" moe_status moe_layer_forward(const uint16_t *x, const float *logits, int64_t T, int E, int k,
+                                        int expert_begin, int n_local_experts, int H, int I_s, const uint16_t *w13,
+                                        const uint16_t *w2, int64_t shared_begin, int64_t shared_count,
+                                        const uint16_t *shared_w13, const uint16_t *shared_w2, int32_t *topk_ids,
+                                        float *topk_w, int32_t *counts, int32_t *offsets, int32_t *row_to_pair,
+                                        int32_t *pair_to_row, uint16_t *y, uint16_t *shared_y, uint16_t *out,
+                                        void *workspace, size_t workspace_bytes, void *stream)
+{
+    static const char fn[] = "moe_layer_forward";
+    // what moe_route, moe_permute, moe_grouped_ffn_shared and moe_combine check
+    moe_status st = check_topk(T, E, k);
+    if (st != MOE_OK) return st;
+    const int El = n_local_experts;
+    if (El < 1 || expert_begin < 0 || expert_begin + El > E)
+        return fail(MOE_ERR_INVALID_ARG, "%s: local experts [%d, %d+%d) not inside [0, E=%d)", fn, expert_begin,
+                    expert_begin, El, E);
+    const int64_t cap = T * (k < El ? k : El);
+    if ((st = check_ffn(fn, x, T, row_to_pair, k, offsets, El, cap, H, I_s, w13, w2, y)) != MOE_OK) return st;
+    if (!counts) return fail(MOE_ERR_INVALID_ARG, "%s: null counts", fn);
+    if (T > 0 && (!logits || !topk_ids || !topk_w || !row_to_pair || !pair_to_row || !out))
+        return fail(MOE_ERR_INVALID_ARG, "%s: null pointer", fn);
+    if (!aligned16(out)) return fail(MOE_ERR_INVALID_ARG, "%s: out must be 16-byte aligned", fn);
+    if (shared_begin < 0 || shared_count < 0 || shared_begin + shared_count > T)
+        return fail(MOE_ERR_INVALID_ARG, "%s: shared rows [%lld, +%lld) outside the %lld tokens", fn,
+                    (long long)shared_begin, (long long)shared_count, (long long)T);
+    if (shared_count > 0) {
+        if (!shared_w13 || !shared_w2 || !shared_y) return fail(MOE_ERR_INVALID_ARG, "%s: null pointer", fn);
+        if (!aligned16(shared_w13) || !aligned16(shared_w2) || !aligned16(shared_y))
+            return fail(MOE_ERR_INVALID_ARG, "%s: tensors must be 16-byte aligned", fn);
+        if (El + 1 > MOE_MAX_EXPERTS)
+            return fail(MOE_ERR_UNSUPPORTED, "%s: n_local_experts + 1 exceeds %d", fn, MOE_MAX_EXPERTS);
+        if (cap + shared_count >= ((int64_t)1 << 31))
+            return fail(MOE_ERR_UNSUPPORTED, "%s: cap_rows + shared_count too large", fn);
+        if (!ffn_large_tiles(T, cap + shared_count, H, I_s))
+            return fail(MOE_ERR_UNSUPPORTED,
+                        "%s: H=%d and I_s=%d must be multiples of 64, from 128 to 2^26, with operands under 4 GiB",
+                        fn, H, I_s);
+    }
+    const size_t need = moe_layer_workspace_size(T, k, El, H, I_s, shared_count);
+    if ((st = check_workspace(fn, workspace, workspace_bytes, need)) != MOE_OK) return st;
+    char *ws = static_cast<char *>(workspace);
+    void *ws_ffn = ws + align256(moe_permute_workspace_size(T, k, El));
+    return hip_status(launch_layer(x, logits, T, E, k, expert_begin, El, H, I_s, w13, w2, shared_begin, shared_count,
+                                   shared_w13, shared_w2, topk_ids, topk_w, counts, offsets, row_to_pair,
+                                   pair_to_row, y, shared_y, out, reinterpret_cast<int32_t *>(ws), ws_ffn,
+                                   (hipStream_t)stream),
+                      "moe_layer_forward launch");
 }
 
 extern "C" moe_status moe_reshard_experts(int direction, int P, int rank, int E, int H, int I,

@@ -13,6 +13,8 @@
 #include <type_traits>
 
 #include "moe_internal.h"
+#include "permute_dev.h"
+#include "route_dev.h"
 
 namespace moe {
 namespace {
@@ -260,15 +262,19 @@ struct SchedOut {
     int4 *mt[2];  // per small m-tile: expert, first row, end row
 };
 
-__global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restrict__ offsets, int El,
-                                                        int64_t cap, int64_t shared_rows, int bm, bool small,
-                                                        SchedShape sh, SchedOut out,
-                                                        int32_t *__restrict__ counters, int64_t n_counters)
+// (A device function run by one block: one thread per expert, at least two
+// waves, whole waves; NE_MAX bounds the experts, the shared one included.
+// offsets may point to LDS.)
+template <int NE_MAX>
+__device__ __forceinline__ void schedule_body(const int32_t *__restrict__ offsets, int El, int64_t cap,
+                                              int64_t shared_rows, int bm, bool small, const SchedShape &sh,
+                                              const SchedOut &out, int32_t *__restrict__ counters,
+                                              int64_t n_counters)
 {
     constexpr int NT = NC_SCHED / 2;  // leftover thresholds 0, 32, 64, 96, 128
     constexpr int NC = NC_SCHED;
     __shared__ int32_t wsum[16][4];
-    __shared__ int32_t vals[1024][3 * NC + 1];  // per expert: its tiles of every base candidate, its rows
+    __shared__ int32_t vals[NE_MAX][3 * NC + 1];  // per expert: its tiles of every base candidate, its rows
     __shared__ int32_t tot[3 * NC];
     __shared__ int32_t ptot[4];
     __shared__ int32_t big[2];  // the largest expert and its rows
@@ -319,14 +325,16 @@ __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restric
         // of 64 and of 128 rows; each expert writes its row, one thread per
         // column sums it (a few dozen experts typically: cheaper than
         // shuffle trees)
+        if (e < NE_MAX) {  // rows of threads past the experts are never read
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            const int2 r = rows_for(n, c);
-            vals[e][3 * c] = r.x;
-            vals[e][3 * c + 1] = (r.y + 63) / 64;
-            vals[e][3 * c + 2] = (r.y + 127) / 128;
+            for (int c = 0; c < NC; ++c) {
+                const int2 r = rows_for(n, c);
+                vals[e][3 * c] = r.x;
+                vals[e][3 * c + 1] = (r.y + 63) / 64;
+                vals[e][3 * c + 2] = (r.y + 127) / 128;
+            }
+            vals[e][3 * NC] = n;
         }
-        vals[e][3 * NC] = n;
         __syncthreads();
         if (e < 3 * NC) {
             int32_t sum = 0;
@@ -438,6 +446,14 @@ __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restric
             }
         }
     }
+}
+
+__global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restrict__ offsets, int El,
+                                                        int64_t cap, int64_t shared_rows, int bm, bool small,
+                                                        SchedShape sh, SchedOut out,
+                                                        int32_t *__restrict__ counters, int64_t n_counters)
+{
+    schedule_body<1024>(offsets, El, cap, shared_rows, bm, small, sh, out, counters, n_counters);
 }
 
 // 256 threads = 4 waves in a 2x2 grid, each wave owns a 32x32 block of the
@@ -1381,6 +1397,130 @@ __global__ __launch_bounds__(GEMM_THREADS) void splitk_reduce(const int32_t *__r
     }
 }
 
+// ---------------------------------------------------------------------------
+// The layer's first launches, fused (moe_layer_forward): routing, the
+// permutation and the grouped FFN's tile schedule, in one launch for small
+// inputs and two for larger ones, instead of a routing launch, one or two
+// permutation launches and a schedule launch.  Each piece computes exactly
+// what its own launch computes.
+// ---------------------------------------------------------------------------
+constexpr int LAYER_NE_MAX = 128;  // experts of the fused schedule (local ones + shared), at most
+
+// Small inputs (the one-workgroup permutation), after the routing launch:
+// one block of 1024 threads permutes the pairs, then schedules the FFN's
+// tiles.  (Routing stays a launch of its own: over many workgroups its
+// memory round trips overlap, in one they would follow each other.)
+__global__ __launch_bounds__(1024) void layer_perm_sched_kernel(const int32_t *__restrict__ ids, int64_t npairs,
+                                                                int e0, int El, int nbits,
+                                                                int32_t *__restrict__ counts,
+                                                                int32_t *__restrict__ offsets,
+                                                                int32_t *__restrict__ row_to_pair,
+                                                                int32_t *__restrict__ pair_to_row, int64_t cap,
+                                                                int64_t sc, SchedShape sh, SchedOut so,
+                                                                int32_t *__restrict__ counters, int64_t n_counters)
+{
+    permute_dev::permute_small_body(ids, npairs, e0, El, nbits, counts, offsets, row_to_pair, pair_to_row);
+    __syncthreads();  // the offsets are visible to the block
+    schedule_body<LAYER_NE_MAX>(offsets, El, cap, sc, BIGM, true, sh, so, counters, n_counters);
+}
+
+// Larger inputs, at most 64 local experts: block c routes the tokens that
+// have a pair in chunk c of the pairs (CH = ROUNDS * 64 pairs, the
+// permutation's chunks), writes those whose first pair lies in the chunk
+// (every token once over the grid) and counts the chunk's pairs per local
+// expert (the permutation's histogram row c).
+template <int G, int S, int ROUNDS>
+__global__ __launch_bounds__(256) void layer_route_count_kernel(const float *__restrict__ logits, int64_t T, int E,
+                                                                int k, int e0, int El, int32_t *__restrict__ ids,
+                                                                float *__restrict__ w,
+                                                                int32_t *__restrict__ chunk_cnt)
+{
+    constexpr int CH = ROUNDS * 64;
+    __shared__ int32_t lid[CH + 2 * MOE_MAX_TOPK];
+    __shared__ float lw[CH + 2 * MOE_MAX_TOPK];
+    __shared__ int32_t hist[64];
+    const int tid = threadIdx.x;
+    const int64_t npairs = T * k, p0 = (int64_t)blockIdx.x * CH;
+    const int64_t p1 = p0 + CH < npairs ? p0 + CH : npairs;
+    const int64_t ta = p0 / k, tb = (p1 + k - 1) / k;  // tokens [ta, tb) have pairs in the chunk
+    const int sub = tid % G;
+    for (int64_t t = ta + tid / G; t < tb; t += 256 / G)
+        route_dev::route_token<G, S>(logits + t * E, E, k, sub, lid + (t - ta) * k, lw + (t - ta) * k);
+    if (tid < 64) hist[tid] = 0;
+    __syncthreads();
+    const int64_t tw = (p0 + k - 1) / k;  // the first token whose first pair lies in the chunk
+    for (int64_t q = tw * k + tid; q < tb * k; q += 256) {
+        ids[q] = lid[q - ta * k];
+        w[q] = lw[q - ta * k];
+    }
+    for (int64_t p = p0 + tid; p < p1; p += 256) {
+        const int le = permute_dev::local_index(lid[p - ta * k], e0, El);
+        if (le < El) atomicAdd(&hist[le], 1);
+    }
+    __syncthreads();
+    if (tid < El) chunk_cnt[(int64_t)blockIdx.x * El + tid] = hist[tid];
+}
+
+// Then blocks 0 .. nb-1 (nb = ceil(nchunks / 4)) scan and scatter the
+// permutation, four chunks each, and block nb schedules the FFN's tiles from
+// the expert totals of the histogram (it does not wait for the scatter).
+template <int ROUNDS>
+__global__ __launch_bounds__(256) void layer_scan_sched_kernel(const int32_t *__restrict__ ids, int64_t npairs,
+                                                               int e0, int El, int nbits,
+                                                               const int32_t *__restrict__ chunk_cnt, int64_t nchunks,
+                                                               int32_t *__restrict__ counts,
+                                                               int32_t *__restrict__ offsets,
+                                                               int32_t *__restrict__ row_to_pair,
+                                                               int32_t *__restrict__ pair_to_row, int64_t cap,
+                                                               int64_t sc, SchedShape sh, SchedOut so,
+                                                               int32_t *__restrict__ counters, int64_t n_counters)
+{
+    const int64_t nb = (nchunks + 3) / 4;
+    if ((int64_t)blockIdx.x < nb) {
+        permute_dev::scan_scatter_body<ROUNDS>(ids, npairs, e0, El, nbits, chunk_cnt, nchunks, counts, offsets,
+                                               row_to_pair, pair_to_row, blockIdx.x);
+        return;
+    }
+    // expert totals: thread t sums expert t % El over chunks t / El, + S, ...
+    // (S = 256 / El column groups), then one lane per expert adds the groups
+    // and the lanes scan the totals into the experts' first rows
+    constexpr int UNR = 8;
+    __shared__ int32_t part[256];
+    __shared__ int32_t soff[64 + 1];
+    const int t = threadIdx.x, S = 256 / El;
+    int32_t tot = 0;
+    if (t < S * El) {
+        const int e = t % El;
+        for (int64_t c = t / El; c < nchunks; c += (int64_t)S * UNR) {
+            int32_t v[UNR];
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) {
+                const int64_t cu = c + (int64_t)u * S;
+                v[u] = cu < nchunks ? chunk_cnt[cu * El + e] : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) tot += v[u];
+        }
+    }
+    part[t] = tot;
+    __syncthreads();
+    if (t < 64) {
+        int32_t total = 0;
+        if (t < El)
+            for (int g = 0; g < S; ++g) total += part[g * El + t];
+        int32_t incl = total;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int32_t o = __shfl_up(incl, off, 64);
+            if (t >= off) incl += o;
+        }
+        if (t < El) soff[t] = incl - total;
+        if (t == El - 1) soff[El] = incl;
+    }
+    __syncthreads();
+    schedule_body<LAYER_NE_MAX>(soff, El, cap, sc, BIGM, true, sh, so, counters, n_counters);
+}
+
 }  // namespace
 
 namespace {
@@ -1474,73 +1614,85 @@ bool ffn_large_tiles(int64_t x_rows, int64_t rows, int H, int Is)
     return x_rows * (int64_t)H * 2 < lim && rows * (int64_t)H * 2 < lim && rows * (int64_t)Is * 2 < lim;
 }
 
-hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *row_index, int kdiv,
-                              const int32_t *offsets, int El, int64_t cap, int H, int Is,
-                              const uint16_t *w13, const uint16_t *w2, uint16_t *y, int64_t shared_begin,
-                              int64_t shared_rows, const uint16_t *sw13, const uint16_t *sw2,
-                              uint16_t *shared_y, void *ws, hipStream_t s)
-{
-    // row space: the routed rows [0, cap), then the shared expert's rows
-    const int64_t sc = shared_rows;
-    const int ne = El + (sc > 0 ? 1 : 0);
-    const int64_t rows = cap + sc;
-    if (rows == 0) return hipSuccess;
-    const FfnLayout L(rows, ne, H, Is);
-    char *base = static_cast<char *>(ws);
-    int32_t *pre = reinterpret_cast<int32_t *>(base);                     // large class, gate-up
-    int32_t *pre_ld = reinterpret_cast<int32_t *>(base + L.off_pre_ld);  // large class, down
-    int32_t *pre_s = reinterpret_cast<int32_t *>(base + L.off_pre_s);    // small class, gate-up
-    int32_t *pre_sd = reinterpret_cast<int32_t *>(base + L.off_pre_sd);  // small class, down
-    int32_t *split = reinterpret_cast<int32_t *>(base + L.off_split);    // class cut, gate-up
-    int32_t *split_d = reinterpret_cast<int32_t *>(base + L.off_split_d);
-    int4 *mt_g = reinterpret_cast<int4 *>(base + L.off_mt);  // small m-tiles, gate-up
-    int4 *mt_d = reinterpret_cast<int4 *>(base + L.off_mt_d);
-    int32_t *cnt = reinterpret_cast<int32_t *>(base + L.off_cnt);
-    float *part_s = reinterpret_cast<float *>(base + L.off_part_s);
-    float *part = reinterpret_cast<float *>(base + L.off_part);
-    uint16_t *h = reinterpret_cast<uint16_t *>(base + L.off_h);
-    uint16_t *h_sh = h + cap * Is;  // the shared expert's h rows
-    const bool big = ffn_large_tiles(row_index ? x_rows : rows, rows, H, Is);
-    if (sc > 0 && !big) return hipErrorNotSupported;  // the host API checks this first
-    hipError_t err;
+namespace {
+
+// One grouped-FFN call: its row space (the routed rows [0, cap), then the
+// shared expert's rows), the workspace parts and the schedule's arguments.
+struct FfnCall {
+    FfnLayout L;
+    int El, ne, H, Is;
+    int64_t cap, sc, rows, n_cnt;
+    bool big;
+    int32_t *pre, *pre_ld, *pre_s, *pre_sd, *split, *split_d, *cnt;
+    int4 *mt_g, *mt_d;
+    float *part_s, *part;
+    uint16_t *h, *h_sh;
+    SchedShape sh;
+    SchedOut so;
+    FfnCall(int64_t x_rows, bool gather, int El_, int64_t cap_, int H_, int Is_, int64_t sc_, void *ws)
+        : L(cap_ + sc_, El_ + (sc_ > 0 ? 1 : 0), H_, Is_), El(El_), ne(El_ + (sc_ > 0 ? 1 : 0)), H(H_), Is(Is_),
+          cap(cap_), sc(sc_), rows(cap_ + sc_)
     {
-        KernelTimer timer(MOE_K_SCHEDULE, s);
-        const unsigned threads = (unsigned)(ceil_div(ne > 128 ? ne : 128, 64) * 64);
-        const SchedOut so{{pre, pre_ld}, {pre_s, pre_sd}, {split, split_d}, {mt_g, mt_d}};
-        schedule_kernel<<<dim3(1), dim3(threads), 0, s>>>(
-            offsets, El, cap, sc, big ? BIGM : BM, big,
-            sched_shape(H, Is, L.grid), so,
-            cnt, big ? L.t_gu + L.t_dn + L.ts_gu + L.ts_dn : 0);
-        if ((err = hipGetLastError()) != hipSuccess) return err;
+        char *base = static_cast<char *>(ws);
+        pre = reinterpret_cast<int32_t *>(base);                     // large class, gate-up
+        pre_ld = reinterpret_cast<int32_t *>(base + L.off_pre_ld);  // large class, down
+        pre_s = reinterpret_cast<int32_t *>(base + L.off_pre_s);    // small class, gate-up
+        pre_sd = reinterpret_cast<int32_t *>(base + L.off_pre_sd);  // small class, down
+        split = reinterpret_cast<int32_t *>(base + L.off_split);    // class cut, gate-up
+        split_d = reinterpret_cast<int32_t *>(base + L.off_split_d);
+        mt_g = reinterpret_cast<int4 *>(base + L.off_mt);  // small m-tiles, gate-up
+        mt_d = reinterpret_cast<int4 *>(base + L.off_mt_d);
+        cnt = reinterpret_cast<int32_t *>(base + L.off_cnt);
+        part_s = reinterpret_cast<float *>(base + L.off_part_s);
+        part = reinterpret_cast<float *>(base + L.off_part);
+        h = reinterpret_cast<uint16_t *>(base + L.off_h);
+        h_sh = h + cap * Is;  // the shared expert's h rows
+        big = ffn_large_tiles(gather ? x_rows : rows, rows, H, Is);
+        n_cnt = big ? L.t_gu + L.t_dn + L.ts_gu + L.ts_dn : 0;
+        sh = sched_shape(H, Is, L.grid);
+        so = SchedOut{{pre, pre_ld}, {pre_s, pre_sd}, {split, split_d}, {mt_g, mt_d}};
     }
-    if (big) {
-        int32_t *c_gu = cnt, *c_dn = cnt + L.t_gu, *cs_gu = c_dn + L.t_dn, *cs_dn = cs_gu + L.ts_gu;
+    int bm() const { return big ? BIGM : BM; }
+};
+
+// The GEMM launches of a call whose schedule is already in the workspace.
+hipError_t launch_gemms(const FfnCall &c, const uint16_t *x, int64_t x_rows, const int32_t *row_index, int kdiv,
+                        const int32_t *offsets, const uint16_t *w13, const uint16_t *w2, uint16_t *y,
+                        int64_t shared_begin, const uint16_t *sw13, const uint16_t *sw2, uint16_t *shared_y,
+                        hipStream_t s)
+{
+    const FfnLayout &L = c.L;
+    const int El = c.El, ne = c.ne, H = c.H, Is = c.Is;
+    const int64_t cap = c.cap, sc = c.sc, rows = c.rows;
+    hipError_t err;
+    if (c.big) {
+        int32_t *c_gu = c.cnt, *c_dn = c.cnt + L.t_gu, *cs_gu = c_dn + L.t_dn, *cs_dn = cs_gu + L.ts_gu;
         {
             KernelTimer timer(MOE_K_GATE_UP, s);
-            const GemmArgs g{x,   row_index, kdiv, x_rows, offsets, split, El, ne, cap, sc, shared_begin,
-                             Is,  H,         w13,  (int64_t)2 * Is * H, sw13, Is, h, h_sh};
+            const GemmArgs g{x,   row_index, kdiv, x_rows, offsets, c.split, El, ne, cap, sc, shared_begin,
+                             Is,  H,         w13,  (int64_t)2 * Is * H, sw13, Is, c.h, c.h_sh};
             gemm_grouped<true><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
-                g, TileClass{pre_s, mt_g, cs_gu, part_s}, TileClass{pre, nullptr, c_gu, part});
+                g, TileClass{c.pre_s, c.mt_g, cs_gu, c.part_s}, TileClass{c.pre, nullptr, c_gu, c.part});
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         if (H / BIG_BK >= SPLIT_MIN_NK) {  // the large tiles may have been split over K
             KernelTimer timer(MOE_K_SPLITK_REDUCE, s);
             splitk_reduce<true><<<dim3(REDUCE_GRID), dim3(GEMM_THREADS), 0, s>>>(
-                offsets, split, pre, El, ne, cap, sc, Is, H, L.grid, part, h, h_sh);
+                offsets, c.split, c.pre, El, ne, cap, sc, Is, H, L.grid, c.part, c.h, c.h_sh);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         {
             KernelTimer timer(MOE_K_DOWN, s);
-            const GemmArgs g{h, nullptr, 1, rows, offsets, split_d, El, ne, cap, sc, shared_begin,
-                             H, Is,      w2, (int64_t)H * Is, sw2, 0, y, shared_y};
+            const GemmArgs g{c.h, nullptr, 1, rows, offsets, c.split_d, El, ne, cap, sc, shared_begin,
+                             H,   Is,      w2, (int64_t)H * Is, sw2, 0, y, shared_y};
             gemm_grouped<false><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
-                g, TileClass{pre_sd, mt_d, cs_dn, part_s}, TileClass{pre_ld, nullptr, c_dn, part});
+                g, TileClass{c.pre_sd, c.mt_d, cs_dn, c.part_s}, TileClass{c.pre_ld, nullptr, c_dn, c.part});
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         if (Is / BIG_BK >= SPLIT_MIN_NK) {
             KernelTimer timer(MOE_K_SPLITK_REDUCE, s);
             splitk_reduce<false><<<dim3(REDUCE_GRID), dim3(GEMM_THREADS), 0, s>>>(
-                offsets, split_d, pre_ld, El, ne, cap, sc, H, Is, L.grid, part, y, shared_y);
+                offsets, c.split_d, c.pre_ld, El, ne, cap, sc, H, Is, L.grid, c.part, y, shared_y);
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         return hipSuccess;
@@ -1553,7 +1705,7 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
         int64_t tiles = mt * ceil_div(Is, BN);
         int64_t grid = tiles < 2048 ? tiles : 2048;
         gemm_kernel<true><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
-            x, row_index, kdiv, offsets, pre, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, h);
+            x, row_index, kdiv, offsets, c.pre, El, cap, Is, H, w13, (int64_t)2 * Is * H, Is, c.h);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     {
@@ -1561,10 +1713,132 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
         int64_t tiles = mt * ceil_div(H, BN);
         int64_t grid = tiles < 2048 ? tiles : 2048;
         gemm_kernel<false><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
-            h, nullptr, 1, offsets, pre, El, cap, H, Is, w2, (int64_t)H * Is, 0, y);
+            c.h, nullptr, 1, offsets, c.pre, El, cap, H, Is, w2, (int64_t)H * Is, 0, y);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *row_index, int kdiv,
+                              const int32_t *offsets, int El, int64_t cap, int H, int Is,
+                              const uint16_t *w13, const uint16_t *w2, uint16_t *y, int64_t shared_begin,
+                              int64_t shared_rows, const uint16_t *sw13, const uint16_t *sw2,
+                              uint16_t *shared_y, void *ws, hipStream_t s)
+{
+    if (cap + shared_rows == 0) return hipSuccess;
+    const FfnCall c(x_rows, row_index != nullptr, El, cap, H, Is, shared_rows, ws);
+    if (shared_rows > 0 && !c.big) return hipErrorNotSupported;  // the host API checks this first
+    {
+        KernelTimer timer(MOE_K_SCHEDULE, s);
+        const unsigned threads = (unsigned)(ceil_div(c.ne > 128 ? c.ne : 128, 64) * 64);
+        schedule_kernel<<<dim3(1), dim3(threads), 0, s>>>(offsets, El, cap, shared_rows, c.bm(), c.big, c.sh, c.so,
+                                                          c.cnt, c.n_cnt);
+        hipError_t err = hipGetLastError();
+        if (err != hipSuccess) return err;
+    }
+    return launch_gemms(c, x, x_rows, row_index, kdiv, offsets, w13, w2, y, shared_begin, sw13, sw2, shared_y, s);
+}
+
+namespace {
+
+// The token group of the fused routing: 16 lanes per token, each holding
+// E / 16 logits (64 lanes above 512 experts), so a block of 256 threads
+// routes 16 tokens at a time.  (The weights do not depend on the group
+// width: route_token sums them in rank order.)
+template <template <int, int> class F, typename... A>
+hipError_t by_experts(int E, A... a)
+{
+    if (E <= 8) return F<8, 1>::go(a...);
+    if (E <= 16) return F<16, 1>::go(a...);
+    if (E <= 32) return F<16, 2>::go(a...);
+    if (E <= 64) return F<16, 4>::go(a...);
+    if (E <= 128) return F<16, 8>::go(a...);
+    if (E <= 256) return F<16, 16>::go(a...);
+    if (E <= 512) return F<16, 32>::go(a...);
+    return F<64, 16>::go(a...);
+}
+
+template <int G, int S>
+struct LaunchRouteCount {
+    static hipError_t go(const float *logits, int64_t T, int E, int k, int e0, int El, int32_t *ids, float *w,
+                         int32_t *chunk_cnt, int64_t nchunks, bool short_chunks, hipStream_t s)
+    {
+        if (short_chunks)
+            layer_route_count_kernel<G, S, 4><<<dim3((unsigned)nchunks), dim3(256), 0, s>>>(logits, T, E, k, e0, El,
+                                                                                              ids, w, chunk_cnt);
+        else
+            layer_route_count_kernel<G, S, 16><<<dim3((unsigned)nchunks), dim3(256), 0, s>>>(logits, T, E, k, e0, El,
+                                                                                               ids, w, chunk_cnt);
+        return hipGetLastError();
+    }
+};
+
+}  // namespace
+
+bool layer_fused_prep(int64_t T, int k, int El, int H, int Is, int64_t sc)
+{
+    const int64_t npairs = T * k, cap = T * (k < El ? k : El);
+    int nbits = 0;
+    while ((1 << nbits) < El + 2) ++nbits;
+    const bool fuse = npairs > 0 && El <= 64 && El + (sc > 0 ? 1 : 0) <= LAYER_NE_MAX &&
+                      ffn_large_tiles(T, cap + sc, H, Is);
+    const bool small = npairs <= permute_dev::SMALL_PAIRS && npairs * (nbits + 2) <= permute_dev::SMALL_WORK;
+    return fuse && (small || permute_chunks(T, k, El) <= permute_dev::SCAN_SCATTER_MAX_CHUNKS);
+}
+
+hipError_t launch_layer(const uint16_t *x, const float *logits, int64_t T, int E, int k, int e0, int El, int H,
+                        int Is, const uint16_t *w13, const uint16_t *w2, int64_t sb, int64_t sc,
+                        const uint16_t *sw13, const uint16_t *sw2, int32_t *ids, float *w, int32_t *counts,
+                        int32_t *offsets, int32_t *r2p, int32_t *p2r, uint16_t *y, uint16_t *shared_y,
+                        uint16_t *out, int32_t *ws_perm, void *ws_ffn, hipStream_t s)
+{
+    const int64_t npairs = T * k, cap = T * (k < El ? k : El);
+    hipError_t err;
+    if (!layer_fused_prep(T, k, El, H, Is, sc)) {
+        // the separate launches of the four calls
+        if ((err = launch_route(logits, T, E, k, ids, w, s)) != hipSuccess) return err;
+        if ((err = launch_permute(ids, T, k, e0, El, counts, offsets, r2p, p2r, nullptr, 0, nullptr, cap, ws_perm,
+                                  s)) != hipSuccess)
+            return err;
+        if ((err = launch_grouped_ffn(x, T, r2p, k, offsets, El, cap, H, Is, w13, w2, y, sb, sc, sw13, sw2,
+                                      shared_y, ws_ffn, s)) != hipSuccess)
+            return err;
+        return launch_combine(y, cap, p2r, w, T, k, H, sc > 0 ? shared_y : nullptr, sb, sc, 0, out, s);
+    }
+    const FfnCall c(T, true, El, cap, H, Is, sc, ws_ffn);
+    int nbits = 0;
+    while ((1 << nbits) < El + 2) ++nbits;
+    const bool small = npairs <= permute_dev::SMALL_PAIRS && npairs * (nbits + 2) <= permute_dev::SMALL_WORK;
+    if (small && (err = launch_route(logits, T, E, k, ids, w, s)) != hipSuccess) return err;
+    {
+        KernelTimer timer(MOE_K_LAYER_PREP, s);
+        if (small) {
+            layer_perm_sched_kernel<<<dim3(1), dim3(1024), 0, s>>>(ids, npairs, e0, El, nbits, counts, offsets, r2p,
+                                                                    p2r, cap, sc, c.sh, c.so, c.cnt, c.n_cnt);
+            err = hipGetLastError();
+        } else {
+            const int64_t nchunks = permute_chunks(T, k, El);
+            const bool short_chunks = permute_dev::chunk_pairs(npairs, El) == 256;
+            err = by_experts<LaunchRouteCount>(E, logits, T, E, k, e0, El, ids, w, ws_perm, nchunks, short_chunks, s);
+            if (err != hipSuccess) return err;
+            const unsigned blocks = (unsigned)(ceil_div(nchunks, 4) + 1);
+            if (short_chunks)
+                layer_scan_sched_kernel<4><<<dim3(blocks), dim3(256), 0, s>>>(
+                    ids, npairs, e0, El, nbits, ws_perm, nchunks, counts, offsets, r2p, p2r, cap, sc, c.sh, c.so, c.cnt,
+                    c.n_cnt);
+            else
+                layer_scan_sched_kernel<16><<<dim3(blocks), dim3(256), 0, s>>>(
+                    ids, npairs, e0, El, nbits, ws_perm, nchunks, counts, offsets, r2p, p2r, cap, sc, c.sh, c.so, c.cnt,
+                    c.n_cnt);
+            err = hipGetLastError();
+        }
+        if (err != hipSuccess) return err;
+    }
+    if ((err = launch_gemms(c, x, T, r2p, k, offsets, w13, w2, y, sb, sw13, sw2, shared_y, s)) != hipSuccess)
+        return err;
+    return launch_combine(y, cap, p2r, w, T, k, H, sc > 0 ? shared_y : nullptr, sb, sc, 0, out, s);
 }
 
 }  // namespace moe

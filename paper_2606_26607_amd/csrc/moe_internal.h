@@ -85,6 +85,17 @@ hipError_t launch_kv_move(int n_src, const uint16_t *const *sk, const uint16_t *
                           int head_dim, int hs0, int hd0, int nh, const int32_t *src_slot, const int32_t *dst_slot,
                           hipStream_t s);
 
+// The whole layer (moe_layer_forward): routing, permutation (no x_perm)
+// and tile schedule in fused launches where layer_fused_prep says so, else
+// the separate launches of the four calls; then the GEMMs and the combine.
+// ws_perm: moe_permute_workspace_size bytes; ws_ffn: the grouped FFN's.
+bool layer_fused_prep(int64_t T, int k, int El, int H, int Is, int64_t sc);
+hipError_t launch_layer(const uint16_t *x, const float *logits, int64_t T, int E, int k, int e0, int El, int H,
+                        int Is, const uint16_t *w13, const uint16_t *w2, int64_t sb, int64_t sc,
+                        const uint16_t *sw13, const uint16_t *sw2, int32_t *ids, float *w, int32_t *counts,
+                        int32_t *offsets, int32_t *r2p, int32_t *p2r, uint16_t *y, uint16_t *shared_y,
+                        uint16_t *out, int32_t *ws_perm, void *ws_ffn, hipStream_t s);
+
 hipError_t launch_combine(const uint16_t *y, int64_t y_rows, const int32_t *pair_to_row,
                           const float *w, int64_t T, int k, int H, const uint16_t *shared_y,
                           int64_t sb, int64_t sc, int accumulate, uint16_t *out, hipStream_t s);

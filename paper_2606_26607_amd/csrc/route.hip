@@ -1,82 +1,11 @@
-// Gating: softmax top-k over router logits, one lane group per token.
-//
-// A token's E logits are spread over a group of G lanes (G = 8..64, a power
-// of two), S logits per lane, G*S >= E.  Each logit becomes
-// a 64-bit key whose high word orders floats (with -0.0 folded onto +0.0)
-// and whose low word is ~id, so the largest key is the largest logit with
-// the lowest expert id.  k rounds of a group-wide max over the keys pick the
-// experts in rank order; the weights are exp(l_j - l_0) / sum_i exp(l_i - l_0)
-// over the kept logits, which equals the full softmax renormalised over the
-// kept experts.
-#include <type_traits>
-
-#include "moe_internal.h"
+// Gating kernel: softmax top-k over router logits, one lane group per token
+// (route_dev.h).
+#include "route_dev.h"
 
 namespace moe {
 namespace {
 
-__device__ __forceinline__ uint32_t order_key(float f)
-{
-    uint32_t u = __float_as_uint(f);
-    if ((u << 1) == 0) u = 0;  // -0.0 -> +0.0
-    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
-__device__ __forceinline__ float key_value(uint32_t o)
-{
-    uint32_t u = (o & 0x80000000u) ? (o & 0x7fffffffu) : ~o;
-    return __uint_as_float(u);
-}
-
-// Lane exchange inside a row of 16 lanes (DPP, no LDS round trip):
-// CTRL 0xB1 swaps neighbours (quad_perm 1,0,3,2), 0x4E swaps pairs
-// (quad_perm 2,3,0,1), 0x141 mirrors each half row, 0x140 mirrors the row.
-template <int CTRL>
-__device__ __forceinline__ uint32_t dpp32(uint32_t v)
-{
-    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true);
-}
-
-// The steps that combine a group of G lanes (G <= 16 uses DPP: after the two
-// quad swaps every quad agrees, the half-row mirror joins the two quads of a
-// half row, the row mirror joins the halves).
-template <int G, typename T, typename Op>
-__device__ __forceinline__ T group_reduce(T v, Op op)
-{
-    if constexpr (G <= 16) {
-        auto step = [&](auto ctrl) {
-            constexpr int C = decltype(ctrl)::value;
-            if constexpr (sizeof(T) == 8) {
-                const uint64_t u = *reinterpret_cast<uint64_t *>(&v);
-                const uint64_t o = (uint64_t)dpp32<C>((uint32_t)u) | ((uint64_t)dpp32<C>((uint32_t)(u >> 32)) << 32);
-                v = op(v, *reinterpret_cast<const T *>(&o));
-            } else {
-                const uint32_t o = dpp32<C>(*reinterpret_cast<uint32_t *>(&v));
-                v = op(v, *reinterpret_cast<const T *>(&o));
-            }
-        };
-        step(std::integral_constant<int, 0xB1>{});
-        if constexpr (G >= 4) step(std::integral_constant<int, 0x4E>{});
-        if constexpr (G >= 8) step(std::integral_constant<int, 0x141>{});
-        if constexpr (G >= 16) step(std::integral_constant<int, 0x140>{});
-    } else {
-#pragma unroll
-        for (int off = G / 2; off > 0; off >>= 1) v = op(v, __shfl_xor(v, off, G));
-    }
-    return v;
-}
-
-template <int G>
-__device__ __forceinline__ uint64_t group_max(uint64_t v)
-{
-    return group_reduce<G>(v, [](uint64_t a, uint64_t b) { return a > b ? a : b; });
-}
-
-template <int G>
-__device__ __forceinline__ float group_sum(float v)
-{
-    return group_reduce<G>(v, [](float a, float b) { return a + b; });
-}
+using route_dev::route_token;
 
 template <int G, int S>
 __global__ __launch_bounds__(256) void route_kernel(const float *__restrict__ logits, int64_t T,
@@ -86,35 +15,8 @@ __global__ __launch_bounds__(256) void route_kernel(const float *__restrict__ lo
     constexpr int TPB = 256 / G;  // tokens per block per sweep
     const int sub = threadIdx.x % G;
     for (int64_t t = (int64_t)blockIdx.x * TPB + threadIdx.x / G; t < T;
-         t += (int64_t)gridDim.x * TPB) {
-        const float *row = logits + t * E;
-        uint64_t key[S];
-#pragma unroll
-        for (int m = 0; m < S; ++m) {
-            int e = sub + m * G;
-            key[m] = e < E ? ((uint64_t)order_key(row[e]) << 32) | (uint32_t)(~e) : 0ull;
-        }
-        uint64_t mine = 0, top = 0;
-        for (int j = 0; j < k; ++j) {
-            uint64_t best = 0;
-#pragma unroll
-            for (int m = 0; m < S; ++m) best = key[m] > best ? key[m] : best;
-            uint64_t win = group_max<G>(best);
-#pragma unroll
-            for (int m = 0; m < S; ++m)
-                if (key[m] == win) key[m] = 0;  // ids are unique: exactly one slot matches
-            if (j == 0) top = win;
-            if (sub == j) mine = win;
-        }
-        float l0 = key_value((uint32_t)(top >> 32));
-        float ex = 0.f;
-        if (sub < k) ex = expf(key_value((uint32_t)(mine >> 32)) - l0);
-        float z = group_sum<G>(ex);
-        if (sub < k) {
-            ids[t * k + sub] = (int32_t)(~(uint32_t)mine);
-            w[t * k + sub] = ex / z;
-        }
-    }
+         t += (int64_t)gridDim.x * TPB)
+        route_token<G, S>(logits + t * E, E, k, sub, ids + t * k, w + t * k);
 }
 
 template <int G, int S>
@@ -137,7 +39,8 @@ hipError_t launch_route(const float *logits, int64_t T, int E, int k, int32_t *i
     // Many tokens: 16 lanes per token, each holding several logits (a round
     // of the top-k is S local compares and 4 DPP steps, and a wavefront
     // serves 4 tokens).  Few tokens: 64 lanes per token, so the work spreads
-    // over more wavefronts and each lane holds fewer logits.
+    // over more wavefronts and each lane holds fewer logits.  (The fused
+    // layer launches make the same choice: ffn.hip, by_experts.)
     if (E <= 8) return go<8, 1>(logits, T, E, k, ids, w, s);
     if (E <= 16) return go<16, 1>(logits, T, E, k, ids, w, s);
     if (T >= 4096) {

@@ -101,6 +101,37 @@ def test_permute_noalloc_rejects():
     assert moe.permute_workspace_size(1 << 18, 8, 256) <= limit         # 1024-pair chunks
 
 
+def test_layer_forward_rejects():
+    """moe_layer_forward checks what the four calls check, on the host."""
+    L = moe.lib()
+    big = 1 << 30
+    args = dict(x=FAKE, lg=FAKE, T=16, E=8, k=2, e0=0, El=8, H=256, Is=256, w13=FAKE, w2=FAKE, sb=0, sc=0,
+                sw13=None, sw2=None, ids=FAKE, w=FAKE, counts=FAKE, offsets=FAKE, r2p=FAKE, p2r=FAKE, y=FAKE,
+                sy=None, out=FAKE, ws=ctypes.c_void_p(0x100000), wsb=big)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return L.moe_layer_forward(a["x"], a["lg"], a["T"], a["E"], a["k"], a["e0"], a["El"], a["H"], a["Is"],
+                                   a["w13"], a["w2"], a["sb"], a["sc"], a["sw13"], a["sw2"], a["ids"], a["w"],
+                                   a["counts"], a["offsets"], a["r2p"], a["p2r"], a["y"], a["sy"], a["out"], a["ws"],
+                                   a["wsb"], None)
+    assert call(k=0) == INVALID
+    assert call(k=17, E=32) == UNSUPPORTED
+    assert call(e0=4) == INVALID                  # local experts past E
+    assert call(H=60) == UNSUPPORTED              # not a multiple of 8
+    assert call(offsets=None) == INVALID
+    assert call(counts=None) == INVALID
+    assert call(lg=None) == INVALID
+    assert call(out=None) == INVALID
+    assert call(sb=10, sc=8) == INVALID           # shared rows past T
+    assert call(sc=4) == INVALID                  # shared rows without shared weights
+    assert call(sc=4, sw13=FAKE, sw2=FAKE, sy=FAKE, H=136) == UNSUPPORTED   # shared expert needs H % 64 == 0
+    assert call(wsb=16) == WORKSPACE
+    assert call(ws=None) == WORKSPACE
+    assert moe.layer_workspace_size(16, 2, 8, 256, 256) >= (moe.permute_workspace_size(16, 2, 8) +
+                                                            moe.ffn_workspace_size(32, 8, 256, 256))
+
+
 def test_ffn_rejects():
     L = moe.lib()
     big = 1 << 30
