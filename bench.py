@@ -435,6 +435,8 @@ def measure(cfg, args, torch, mi, moe, headline: bool):
 
     replay_ms = []
     single_ms = None
+    graph_kern = {}  # GEMM durations inside the graph replays (device timestamps)
+    graph_kern_replay_ms = None  # the step time of the replay they come from
     if args.eager:
         ms_per_step = eager_ms
     else:
@@ -450,13 +452,21 @@ def measure(cfg, args, torch, mi, moe, headline: bool):
             step()
         torch.cuda.current_stream().wait_stream(side)
         torch.cuda.synchronize()
+        # the captured GEMM launches take device-timestamp slots, so their
+        # durations inside the replays can be read back (no event can be
+        # recorded between the kernels of a graph)
+        moe.timing_device_clear()
+        moe.timing_device_enable(True)
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
             for _ in range(args.steps):
                 step()
+        moe.timing_device_enable(False)
         graph.replay()  # untimed: first replay of the graph
         torch.cuda.synchronize()
-        for _ in range(REPLAYS):
+        for r in range(REPLAYS):
+            if r == REPLAYS - 1:
+                moe.timing_device_reset()  # the last timed replay also gives the GEMMs' device times
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
             graph.replay()
@@ -464,6 +474,11 @@ def measure(cfg, args, torch, mi, moe, headline: bool):
             torch.cuda.synchronize()
             replay_ms.append(a.elapsed_time(b) / args.steps)
         ms_per_step = float(np.median(replay_ms))
+        for kind in ("gate_up", "down"):
+            ms, n = moe.timing_device_read(kind)
+            if n:
+                graph_kern[kind] = dict(avg_us=1e3 * ms / n, launches=n)
+        graph_kern_replay_ms = replay_ms[-1]
         del graph
         # Latency view: one step per graph, replayed K times in a row with an
         # event between consecutive replays (replay i takes from event i to
@@ -509,30 +524,42 @@ def measure(cfg, args, torch, mi, moe, headline: bool):
             kern[kind] = dict(avg_us=1e3 * ms / n, launches=n)
     log(f"[bench] {cfg.name}: step {ms_per_step:.4f} ms (median of {len(replay_ms)} replays of a "
         f"{args.steps}-step graph; {single_ms or 0:.4f} per one-step graph); kernels: " +
-        ", ".join(f"{k}={v['avg_us']:.1f}us x{v['launches']}" for k, v in kern.items()))
+        ", ".join(f"{k}={v['avg_us']:.1f}us x{v['launches']}" for k, v in kern.items()) +
+        "; in the graph: " + ", ".join(f"{k}={v['avg_us']:.1f}us" for k, v in graph_kern.items()) +
+        (f" (replay step {graph_kern_replay_ms:.4f} ms)" if graph_kern_replay_ms else ""))
 
     decode = cfg.name.startswith("dsv3")
     # dominant kernel: the gate-up GEMM (2/3 of the flops and of the weight
     # bytes); its launches per step (the routed experts and, where present,
     # the shared expert) are summed.  Prefill is priced on MFMA, decode
     # (a few rows per expert, weights streamed once) on HBM.
+    # The duration is the one inside the timed graph replays (device
+    # timestamps); the host-launched pass's events are reported beside it.
     dom = "gate_up"
     gu = kern.get(dom)
+    gg = graph_kern.get(dom)
     roof = None
     if gu is not None:
-        dur_s = gu["avg_us"] * 1e-6 * gu["launches"] / args.steps   # kernel time per step
+        per_step = gu["launches"] / args.steps
+        ev_s = gu["avg_us"] * 1e-6 * per_step   # kernel time per step, events, host-launched pass
+        dur_s = gg["avg_us"] * 1e-6 * per_step if gg else ev_s
+        how = ("device timestamps of the launches in the last of the timed graph replays" if gg else
+               "HIP events around the launches of the host-launched pass")
         if decode:
             achieved = work["gate_up_bytes"] / dur_s / 1e9
             roof = dict(bound="hbm", achieved=achieved, peak=PEAK_HBM_GBS, unit="GB/s",
                         frac=achieved / PEAK_HBM_GBS, traffic=measured_traffic(cfg.name, "step"), kernel=dom,
-                        launches_per_step=gu["launches"] // args.steps,
-                        algorithmic_per_step=work["gate_up_bytes"])
+                        launches_per_step=per_step, algorithmic_per_step=work["gate_up_bytes"],
+                        duration_us=dur_s * 1e6 / per_step, duration_from=how,
+                        achieved_events_host_launched=work["gate_up_bytes"] / ev_s / 1e9)
         else:
             achieved = work["gate_up_flops"] / dur_s / 1e12
             roof = dict(bound="mfma", achieved=achieved, peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
                         frac=achieved / PEAK_BF16_TFLOPS, traffic=measured_traffic(cfg.name), kernel=dom,
                         algorithmic_per_launch=work["gate_up_flops"],
-                        algorithmic_bytes_per_launch=work["gate_up_bytes"])
+                        algorithmic_bytes_per_launch=work["gate_up_bytes"],
+                        duration_us=dur_s * 1e6 / per_step, duration_from=how,
+                        achieved_events_host_launched=work["gate_up_flops"] / ev_s / 1e12)
     step_s = ms_per_step * 1e-3
     res = {
         "ms_per_step": ms_per_step,
@@ -546,6 +573,8 @@ def measure(cfg, args, torch, mi, moe, headline: bool):
         "chain_gbs": work["bytes"] / step_s / 1e9,
         "chain_frac_hbm": work["bytes"] / step_s / 1e9 / PEAK_HBM_GBS,
         "kernels_us": {k: round(v["avg_us"], 2) for k, v in kern.items()},
+        "kernels_us_in_graph": {k: round(v["avg_us"], 2) for k, v in graph_kern.items()},
+        "kernels_us_in_graph_replay_ms_per_step": graph_kern_replay_ms,
         "eager_ms_per_step": eager_ms,
         "cold_ms_per_step": cold_ms,
         "roofline": roof,
@@ -715,7 +744,8 @@ def main():
             entry = {"config": config_block(c, cwork, not args.eager),
                      "ms_per_step": r["ms_per_step"], "value": r["value"], "unit": "tokens/s",
                      "ms_per_step_single_step_graph": r["ms_per_step_single_step_graph"],
-                     "kernels_us": r["kernels_us"], "roofline": r["roofline"],
+                     "kernels_us": r["kernels_us"], "kernels_us_in_graph": r["kernels_us_in_graph"],
+                     "roofline": r["roofline"],
                      "chain_frac_mfma": r["chain_frac_mfma"], "chain_frac_hbm": r["chain_frac_hbm"],
                      "chain_tflops": r["chain_tflops"], "chain_gbs": r["chain_gbs"],
                      "eager_ms_per_step": r["eager_ms_per_step"]}

@@ -401,6 +401,29 @@ typedef enum moe_kernel_kind {
     MOE_K_COUNT = 11
 } moe_kernel_kind;
 
+/*
+ * Device-side timestamps of the grouped GEMM launches (MOE_K_GATE_UP and
+ * MOE_K_DOWN of the large-tile path), which also time launches replayed
+ * from a HIP graph, where no event can be recorded between kernels.  While
+ * enabled, each such launch takes the next slot of a static device table of
+ * 4096 slots (a captured launch takes it at capture time, so every replay
+ * of it writes that slot) and its workgroups record the earliest start and
+ * the latest end, in ticks of the device's 100 MHz constant clock (kept per
+ * die to spread the atomics; a launch's duration is from its earliest start
+ * on any die to its latest end on any die).
+ * moe_timing_device_reset synchronises the device and clears the recorded
+ * times (slots stay assigned); moe_timing_device_read synchronises the device
+ * and returns, for one kind, the summed duration (ms) and count of the
+ * launches that ran since the reset (a slot run several times since then
+ * spans from its first start to its last end); moe_timing_device_clear
+ * forgets the slots (launches captured before it must not be replayed while
+ * device timing is read).  The table is shared by every caller on a device.
+ */
+moe_status moe_timing_device_enable(int enable);
+moe_status moe_timing_device_clear(void);
+moe_status moe_timing_device_reset(void);
+moe_status moe_timing_device_read(int kind, double *total_ms, int64_t *launches);
+
 moe_status moe_timing_enable(int enable);
 /* Time only the kinds whose bit (1 << kind) is set in `kinds` (0 disables);
  * bits at or above MOE_K_COUNT give MOE_ERR_INVALID_ARG. */

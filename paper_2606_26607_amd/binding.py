@@ -84,6 +84,10 @@ def lib():
         "moe_partition_requests": ([vp, i32, i32, vp, vp, vp], i32),
         "moe_kv_fits": ([i32, vp, i32, vp, i32, i32, i32, i64, ctypes.POINTER(ctypes.c_int)], i32),
         "moe_policy_crossover": ([vp, vp, vp, i32, ctypes.POINTER(ctypes.c_double)], i32),
+        "moe_timing_device_enable": ([i32], i32),
+        "moe_timing_device_clear": ([], i32),
+        "moe_timing_device_reset": ([], i32),
+        "moe_timing_device_read": ([i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)], i32),
         "moe_timing_enable": ([i32], i32),
         "moe_timing_enable_mask": ([ctypes.c_uint32], i32),
         "moe_timing_reset": ([], i32),
@@ -636,3 +640,27 @@ class MoeLayer:
         combine(self.y, self.bufs["pair_to_row"], self.topk_w, out=self.out, shared_y=shared_y,
                 shared_begin=self.sb, stream=stream)
         return self.out
+
+
+def timing_device_enable(on: bool) -> None:
+    """Grouped GEMM launches made while on take device-timestamp slots
+    (captured launches too, so graph replays are timed)."""
+    _check(lib().moe_timing_device_enable(1 if on else 0))
+
+
+def timing_device_clear() -> None:
+    _check(lib().moe_timing_device_clear())
+
+
+def timing_device_reset() -> None:
+    _check(lib().moe_timing_device_reset())
+
+
+def timing_device_read(kind: str):
+    """(summed ms, launches) of the device-timed launches of `kind` that ran
+    since the last reset."""
+    ms = ctypes.c_double(0)
+    n = ctypes.c_int64(0)
+    _check(lib().moe_timing_device_read(KERNEL_KINDS[kind], ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
+

@@ -10,7 +10,9 @@
 // and experts with no rows cost nothing.  The gate-up workgroup owns the
 // matching gate and up columns, so SwiGLU is applied in registers before h
 // is written.
+#include <mutex>
 #include <type_traits>
+#include <vector>
 
 #include "moe_internal.h"
 #include "permute_dev.h"
@@ -1298,6 +1300,19 @@ __device__ __forceinline__ SmallGroup small_group(int64_t tl, int64_t ts, int nk
     return SmallGroup{v, p.mode == SM_WHOLE_ALL ? G : n_idle, deal};
 }
 
+// Device-side launch timestamps (moe_timing_device_*): per slot, the
+// earliest workgroup start and the latest workgroup end of one launch, in
+// ticks of the 100 MHz constant clock.  A launch takes a slot on the host
+// (at capture time when it is captured), so launches replayed from a HIP
+// graph, where no event can be recorded between kernels, are timed too.
+// Each die keeps its own start and end (workgroup b runs on die b % 8, as
+// the hardware deals workgroups to the dies round robin), which spreads the
+// atomics over eight words; the dies' counters agree to well under a
+// microsecond, so a launch's duration is its earliest start on any die to
+// its latest end on any die.
+constexpr int DEV_TS_SLOTS = 4096;
+__device__ unsigned long long g_dev_ts[2][8][DEV_TS_SLOTS];  // [0]: start (min), [1]: end (max), per die
+
 // One grouped GEMM launch: the large-tile class (256-row tiles) and the
 // small-row class (64- or 128-row tiles as the schedule chose, K-split over
 // its workgroups: these stream weights, and spreading them over many CUs is
@@ -1306,9 +1321,10 @@ __device__ __forceinline__ SmallGroup small_group(int64_t tl, int64_t ts, int nk
 // small-row share without waiting for anyone.
 template <bool GATED>
 __global__ __attribute__((amdgpu_flat_work_group_size(GEMM_THREADS, GEMM_THREADS), amdgpu_waves_per_eu(2, 2)))
-void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
+void gemm_grouped(GemmArgs g, TileClass small, TileClass large, int tslot)
 {
     __shared__ uint4 ring[BIG_RING];
+    if (tslot >= 0 && threadIdx.x == 0) atomicMin(&g_dev_ts[0][blockIdx.x & 7][tslot], __builtin_amdgcn_s_memrealtime());
     constexpr int OUTN = GATED ? BIGN / 2 : BIGN;
     // die-major id: the hardware deals workgroups to the 8 dies round robin
     const int vx = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
@@ -1334,6 +1350,10 @@ void gemm_grouped(GemmArgs g, TileClass small, TileClass large)
             ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, small.tile_prefix, small.mtile, g.El, g.ne, g.cap,
             g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh,
             small.tile_cnt, small.partials, sg.v, sg.size, sg.deal);
+    if (tslot >= 0) {
+        __syncthreads();  // every wave of the workgroup is done
+        if (threadIdx.x == 0) atomicMax(&g_dev_ts[1][blockIdx.x & 7][tslot], __builtin_amdgcn_s_memrealtime());
+    }
 }
 
 // Combines the split-K partials of the large-tile class after its GEMM
@@ -1525,6 +1545,20 @@ __global__ __launch_bounds__(256) void layer_scan_sched_kernel(const int32_t *__
 
 namespace {
 
+std::mutex g_dts_mu;
+bool g_dts_on = false;
+std::vector<int> g_dts_kind;  // slot -> kernel kind
+
+// The next device-timestamp slot for a launch of `kind`, or -1 when device
+// timing is off or the table is full.
+int device_ts_slot(int kind)
+{
+    std::lock_guard<std::mutex> lk(g_dts_mu);
+    if (!g_dts_on || g_dts_kind.size() >= (size_t)DEV_TS_SLOTS) return -1;
+    g_dts_kind.push_back(kind);
+    return (int)g_dts_kind.size() - 1;
+}
+
 int device_cus()
 {
     int dev = 0, cus = 0;
@@ -1672,7 +1706,8 @@ hipError_t launch_gemms(const FfnCall &c, const uint16_t *x, int64_t x_rows, con
             const GemmArgs g{x,   row_index, kdiv, x_rows, offsets, c.split, El, ne, cap, sc, shared_begin,
                              Is,  H,         w13,  (int64_t)2 * Is * H, sw13, Is, c.h, c.h_sh};
             gemm_grouped<true><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
-                g, TileClass{c.pre_s, c.mt_g, cs_gu, c.part_s}, TileClass{c.pre, nullptr, c_gu, c.part});
+                g, TileClass{c.pre_s, c.mt_g, cs_gu, c.part_s}, TileClass{c.pre, nullptr, c_gu, c.part},
+                device_ts_slot(MOE_K_GATE_UP));
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         if (H / BIG_BK >= SPLIT_MIN_NK) {  // the large tiles may have been split over K
@@ -1686,7 +1721,8 @@ hipError_t launch_gemms(const FfnCall &c, const uint16_t *x, int64_t x_rows, con
             const GemmArgs g{c.h, nullptr, 1, rows, offsets, c.split_d, El, ne, cap, sc, shared_begin,
                              H,   Is,      w2, (int64_t)H * Is, sw2, 0, y, shared_y};
             gemm_grouped<false><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
-                g, TileClass{c.pre_sd, c.mt_d, cs_dn, c.part_s}, TileClass{c.pre_ld, nullptr, c_dn, c.part});
+                g, TileClass{c.pre_sd, c.mt_d, cs_dn, c.part_s}, TileClass{c.pre_ld, nullptr, c_dn, c.part},
+                device_ts_slot(MOE_K_DOWN));
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         if (Is / BIG_BK >= SPLIT_MIN_NK) {
@@ -1842,3 +1878,63 @@ hipError_t launch_layer(const uint16_t *x, const float *logits, int64_t T, int E
 }
 
 }  // namespace moe
+
+// Device-side timestamps of the grouped GEMM launches (see include/libmoe.h).
+extern "C" moe_status moe_timing_device_enable(int enable)
+{
+    std::lock_guard<std::mutex> lk(moe::g_dts_mu);
+    moe::g_dts_on = enable != 0;
+    return MOE_OK;
+}
+
+extern "C" moe_status moe_timing_device_clear(void)
+{
+    std::lock_guard<std::mutex> lk(moe::g_dts_mu);
+    moe::g_dts_kind.clear();
+    return MOE_OK;
+}
+
+extern "C" moe_status moe_timing_device_reset(void)
+{
+    void *p = nullptr;
+    hipError_t err = hipGetSymbolAddress(&p, HIP_SYMBOL(moe::g_dev_ts));
+    if (err == hipSuccess) err = hipDeviceSynchronize();
+    const size_t half = sizeof(unsigned long long) * 8 * moe::DEV_TS_SLOTS;
+    if (err == hipSuccess) err = hipMemset(p, 0xff, half);                             // starts: max
+    if (err == hipSuccess) err = hipMemset(static_cast<char *>(p) + half, 0, half);  // ends: 0
+    if (err == hipSuccess) err = hipDeviceSynchronize();
+    if (err != hipSuccess) return moe::set_error(MOE_ERR_HIP, "moe_timing_device_reset: %s", hipGetErrorString(err));
+    return MOE_OK;
+}
+
+extern "C" moe_status moe_timing_device_read(int kind, double *total_ms, int64_t *launches)
+{
+    if (total_ms == nullptr || launches == nullptr || kind < 0 || kind >= MOE_K_COUNT)
+        return moe::set_error(MOE_ERR_INVALID_ARG, "moe_timing_device_read: bad kind %d or null output", kind);
+    std::vector<unsigned long long> ts(2 * 8 * moe::DEV_TS_SLOTS);
+    hipError_t err = hipDeviceSynchronize();
+    if (err == hipSuccess)
+        err = hipMemcpyFromSymbol(ts.data(), HIP_SYMBOL(moe::g_dev_ts), ts.size() * sizeof(unsigned long long), 0,
+                                  hipMemcpyDeviceToHost);
+    if (err != hipSuccess) return moe::set_error(MOE_ERR_HIP, "moe_timing_device_read: %s", hipGetErrorString(err));
+    std::lock_guard<std::mutex> lk(moe::g_dts_mu);
+    double sum = 0.0;
+    int64_t n = 0;
+    for (size_t i = 0; i < moe::g_dts_kind.size(); ++i) {
+        if (moe::g_dts_kind[i] != kind) continue;
+        unsigned long long first = ~0ull, last = 0;  // over the dies
+        for (int d = 0; d < 8; ++d) {
+            const unsigned long long a = ts[(size_t)d * moe::DEV_TS_SLOTS + i];
+            const unsigned long long b = ts[(size_t)(8 + d) * moe::DEV_TS_SLOTS + i];
+            if (b == 0 || a == ~0ull || b < a) continue;  // no workgroup of this die ran since the reset
+            first = a < first ? a : first;
+            last = b > last ? b : last;
+        }
+        if (last == 0) continue;
+        sum += (double)(last - first) * 1e-5;  // 100 MHz ticks -> ms
+        ++n;
+    }
+    *total_ms = sum;
+    *launches = n;
+    return MOE_OK;
+}

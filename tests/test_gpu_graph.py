@@ -110,3 +110,47 @@ def test_multi_step_graph_matches_eager():
         n = int(ref[2][-1])
         np.testing.assert_array_equal(got[0], ref[0], err_msg=f"replay {rep}: out")
         np.testing.assert_array_equal(got[3][:n], ref[3][:n], err_msg=f"replay {rep}: y")
+
+
+def test_device_timestamps_time_graph_replays():
+    """GEMM launches captured while device timing is on are timed in every
+    replay: after a reset, one replay of a graph of three forwards gives three
+    gate-up and three down durations, close to the host-launched events."""
+    cfg = mi.CONFIGS["c4"].with_(T=4096)
+    inp = mi.make_inputs(cfg)
+    layer = _layer(cfg, inp)
+    x = dev_bf16(inp.x)
+    lg = torch.from_numpy(inp.logits).cuda()
+    layer.forward(x, lg)
+    moe.timing_reset()
+    moe.timing_enable(True)
+    for _ in range(3):
+        layer.forward(x, lg)
+    torch.cuda.synchronize()
+    moe.timing_enable(False)
+    ev_ms, ev_n = moe.timing_read("gate_up")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        layer.forward(x, lg)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    moe.timing_device_clear()
+    moe.timing_device_enable(True)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(3):
+            layer.forward(x, lg)
+    moe.timing_device_enable(False)
+    graph.replay()
+    torch.cuda.synchronize()
+    moe.timing_device_reset()
+    assert moe.timing_device_read("gate_up") == (0.0, 0)
+    graph.replay()
+    torch.cuda.synchronize()
+    for kind in ("gate_up", "down"):
+        ms, n = moe.timing_device_read(kind)
+        assert n == 3 and ms > 0, (kind, ms, n)
+    ms, n = moe.timing_device_read("gate_up")
+    assert 0.5 < (ms / n) / (ev_ms / ev_n) < 1.5
+    moe.timing_device_clear()
