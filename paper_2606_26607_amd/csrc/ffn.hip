@@ -44,6 +44,18 @@ __device__ __forceinline__ int64_t expert_end(const int32_t *__restrict__ offset
     return e < El ? clamp_row(offsets[e + 1], cap) : cap + shared_rows;
 }
 
+// A read of metadata that earlier launches wrote and the grouped GEMM only
+// reads (the schedule's tile lists and cuts, the experts' row offsets),
+// through the constant address space: it becomes a scalar load, which waits
+// on the scalar memory counter.  A vector load would wait on the vector
+// counter, which also counts the workgroup's output stores of its previous
+// tile, so each lookup at a tile change would wait for those stores to land.
+template <class T>
+__device__ __forceinline__ T ld_meta(const T *p)
+{
+    return *(const __attribute__((address_space(4))) T *)p;
+}
+
 // SwiGLU of one gate/up pair: silu(g) * u = g / (1 + e^-g) * u, with the
 // hardware reciprocal (the result is rounded to bf16).
 __device__ __forceinline__ float silu_mul(float g, float u)
@@ -573,6 +585,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t *__restrict__ 
 constexpr int BIG_BK = 64;        // K per slice
 constexpr int CPR = BIG_BK / 8;   // 16-byte chunks per LDS row
 constexpr int RPI = 64 / CPR;     // rows per DMA instruction
+static_assert(RPI == 8, "a lane's DMA row is lane / 8");
 constexpr int A_SLOTS = 2, B_SLOTS = 3;        // large tiles: A(s+1), B(s+2) in flight
 constexpr int SA_SLOTS = 3, SB_SLOTS = 4;      // small-row tiles: A(s+2), B(s+3) in flight
 constexpr int BIG_RING_CHUNKS = (A_SLOTS * 256 + B_SLOTS * 256) * CPR;  // 160 KB of 16-byte chunks
@@ -743,12 +756,12 @@ __device__ __forceinline__ TileCoord tile_coord(int64_t tile, const int32_t *__r
     if constexpr (TAIL) {
         // the class has fewer than 2^31 tiles (checked on the host); its
         // m-tiles are listed by the schedule, so one load finds the expert
-        const uint32_t ms = (uint32_t)tile_prefix[ne];
+        const uint32_t ms = (uint32_t)ld_meta(tile_prefix + ne);
         const int nt = (int)((uint32_t)tile / ms);
-        const int4 m = mtile[(uint32_t)tile - (uint32_t)nt * ms];
-        c.e = m.x;
-        c.r0 = m.y;
-        c.r1 = m.z;
+        const int32_t *m = reinterpret_cast<const int32_t *>(mtile + ((uint32_t)tile - (uint32_t)nt * ms));
+        c.e = ld_meta(m);
+        c.r0 = ld_meta(m + 1);
+        c.r1 = ld_meta(m + 2);
         c.n0 = nt * OUTN;
         c.nvalid = N - c.n0 < OUTN ? N - c.n0 : OUTN;
         return c;
@@ -756,14 +769,16 @@ __device__ __forceinline__ TileCoord tile_coord(int64_t tile, const int32_t *__r
         int lo = 0, hi = ne - 1;
         while (lo < hi) {
             int mid = (lo + hi + 1) >> 1;
-            if ((int64_t)tile_prefix[mid] * n_tiles <= tile) lo = mid; else hi = mid - 1;
+            if ((int64_t)ld_meta(tile_prefix + mid) * n_tiles <= tile) lo = mid; else hi = mid - 1;
         }
-        const int64_t local = tile - (int64_t)tile_prefix[lo] * n_tiles;
-        const int mte = tile_prefix[lo + 1] - tile_prefix[lo];
-        const int nt = (int)(local / mte), mt = (int)(local % mte);
+        const int32_t p0 = ld_meta(tile_prefix + lo), p1 = ld_meta(tile_prefix + lo + 1);
+        const int64_t local = tile - (int64_t)p0 * n_tiles;
+        const int mte = p1 - p0;
+        const int64_t nt64 = div_g(local, mte);
+        const int nt = (int)nt64, mt = (int)(local - nt64 * mte);
         c.e = lo;
-        const int64_t rb = expert_begin(offsets, El, cap, lo);
-        const int64_t re = split[lo];
+        const int64_t rb = lo < El ? clamp_row(ld_meta(offsets + lo), cap) : cap;
+        const int64_t re = ld_meta(split + lo);
         c.r0 = rb + (int64_t)mt * BMt;
         c.r1 = re < c.r0 + BMt ? re : c.r0 + BMt;
         c.n0 = nt * OUTN;
@@ -963,11 +978,26 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
             const int trow = (wave * A_INS + q) * RPI + lrow;     // row of the tile
             const int kc = (lane & 7) ^ lrow ^ ((wave * A_INS + q) & 1);  // position ^ swz(row)
             const int64_t r = r0 + trow;
+            // Gathered rows: the RPI row indices of this instruction's rows
+            // are read with scalar loads (the rows are the same for the whole
+            // wave), so they do not wait for the output stores of the
+            // workgroup's previous tile; each lane takes its own.  Rows at or
+            // past cap (the shared expert's) take none, and the indices read
+            // are clamped into the array.
+            int32_t ri = 0;
+            const int64_t rb = r0 + (wave * A_INS + q) * RPI;
+            if (row_index != nullptr && rb < cap) {
+#pragma unroll
+                for (int j = 0; j < RPI; ++j) {
+                    const int32_t vj = ld_meta(row_index + (rb + j < cap ? rb + j : cap - 1));
+                    ri = lrow == j ? vj : ri;
+                }
+            }
             int64_t off;
             if (r >= r1) off = a_bytes;                            // past the expert: zeros
             else if (row_index) {
                 // the shared expert's rows are tokens shared_begin, ...
-                const int64_t tok = r < cap ? (int64_t)(row_index[r] / kdiv) : shared_begin + (r - cap);
+                const int64_t tok = r < cap ? (int64_t)(ri / kdiv) : shared_begin + (r - cap);
                 off = (tok * K + kc * 8) * 2;
             }
             else off = ((int64_t)trow * K + kc * 8) * 2;
