@@ -674,6 +674,15 @@ __device__ __forceinline__ void issue_b(const SliceSrc &a, uint32_t slot, int k0
     dma16(a.rb, slot + (a.wave * B_INS + q) * 1024, a.vob[q], (uint32_t)k0 * 2u);
 }
 
+// Instruction q of this wave's run of NI instructions of one operand (A or
+// B, whichever the wave loads; its descriptor in a.ra, its offsets in
+// a.voa), into a ring slot: operand rows RPI * (a.wave * NI + q) onwards.
+template <int NI>
+__device__ __forceinline__ void issue_own(const SliceSrc &a, uint32_t slot, int k0, int q)
+{
+    dma16(a.ra, slot + (a.wave * NI + q) * 1024, a.voa[q], (uint32_t)k0 * 2u);
+}
+
 template <int MB, int NB>
 struct Frags {
     bf16x8_t a[2][MB], b[2][NB];
@@ -717,6 +726,32 @@ __device__ __forceinline__ void mfma_step(f32x16_t (&acc)[MB][NB], const Frags<M
                 for (int q = qa; q < qb; ++q) {
                     if (IS_B) issue_b<BNt>(src, slot, k0, q0 + q);
                     else issue_a<BMt>(src, slot, k0, q0 + q);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    }
+}
+
+// The MFMAs of one k-step with NQ of this wave's own-operand loads
+// (issue_own, numbered q0 .. q0+NQ-1) spread evenly between them, issued
+// only when `on` (uniform over the wave).
+template <int NI, int NQ, int MB, int NB>
+__device__ __forceinline__ void mfma_step_own(f32x16_t (&acc)[MB][NB], const Frags<MB, NB> &f, int sl,
+                                              const SliceSrc &src, uint32_t slot, int k0, int q0, bool on)
+{
+    constexpr int TOT = MB * NB;
+#pragma unroll
+    for (int t = 0; t < TOT; ++t) {
+        const int i = t / NB, j = t % NB;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[sl][i], f.b[sl][j], acc[i][j], 0, 0, 0);
+        if constexpr (NQ > 0) {
+            const int qa = t * NQ / TOT, qb = (t + 1) * NQ / TOT;
+            if (qb > qa) {
+                __builtin_amdgcn_sched_barrier(0);
+                if (on) {
+#pragma unroll
+                    for (int q = qa; q < qb; ++q) issue_own<NI>(src, slot, k0, q0 + q);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -896,6 +931,11 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
     constexpr int RING = ASL * A_STAGE + BSL * B_STAGE;
     static_assert(RING <= BIG_RING_CHUNKS, "rings exceed the workgroup's LDS");
     static_assert(A_INS >= 1 && B_INS >= 2 && B_INS % 2 == 0, "DMA instruction split");
+    // Large tiles split the loads by operand: waves 0-3 load all of A, waves
+    // 4-7 all of B, NI instructions each (see do_work).
+    constexpr bool ROLES = !TAIL;
+    constexpr int NI = 2 * A_INS;
+    static_assert(!ROLES || (2 * B_INS == NI && NI <= 8 && LA == 1 && GEMM_WAVES == 8), "operand roles");
     static_assert(BMt * OUTN * 2 <= RING * 16, "epilogue staging must fit the rings");
     constexpr int SLOT = MB * NB * 16 * GEMM_THREADS;  // floats per partial slot
 
@@ -962,21 +1002,42 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
         const uint16_t *We = e < El ? W + (int64_t)e * w_stride : Wsh;
         uint16_t *Cb = e < El ? C + r0 * N : Csh + (r0 - cap) * N;
 
+        // Which operand rows this wave loads.  Large tiles: waves 0-3 load
+        // all of A and waves 4-7 all of B.  A SIMD runs waves i and i + 4,
+        // and the first wins the MFMA arbitration: it finishes each slice
+        // ahead of the second and waits at the barrier, while the second
+        // reaches its loads (spread over its MFMAs) later; with the loads
+        // split evenly, the second then waited for its share of the next A
+        // slice while the SIMD's MFMAs stood idle.  So the early waves load
+        // the next slice's A and the late ones B two slices ahead, which has
+        // landed by the time they need it.  Small-row tiles: every wave loads
+        // A_INS instructions of A and B_INS of B.
+        const bool loads_a = !ROLES || wave < GEMM_WAVES / 2;  // uniform over the wave
+        const int wb = ROLES ? wave - GEMM_WAVES / 2 : wave;   // index among the B loaders
+        const int b_ins = ROLES ? NI : B_INS;
         // this wave's B rows lie in one part (gate or up) when gated
-        const int bpart = GATED ? ((wave * B_INS * RPI) / (BNt / 2)) : 0;
-        const int brow0 = wave * B_INS * RPI - bpart * (BNt / 2);  // first B row of this wave in its part
+        const int bpart = GATED ? ((wb * b_ins * RPI) / (BNt / 2)) : 0;
+        const int brow0 = wb * b_ins * RPI - bpart * (BNt / 2);  // first B row of this wave in its part
         SliceSrc src;
-        src.wave = wave;
+        src.wave = ROLES && !loads_a ? wb : wave;
         // A rows come from the permuted buffer (rows r0.. contiguous) or, with
         // row_index, straight from the token matrix (the fused row gather)
         const int64_t a_bytes = row_index ? a_rows * K * 2 : (r1 - r0) * K * 2;
-        src.ra = buffer_desc(row_index ? A : A + r0 * K, a_bytes);
+        const i32x4_t desc_a = buffer_desc(row_index ? A : A + r0 * K, a_bytes);
         const int64_t b_bytes = (int64_t)nvalid * K * 2;
-        src.rb = buffer_desc(We + (int64_t)((GATED && bpart) ? up_off + n0 : n0) * K, b_bytes);
-#pragma unroll
-        for (int q = 0; q < A_INS; ++q) {
-            const int trow = (wave * A_INS + q) * RPI + lrow;     // row of the tile
-            const int kc = (lane & 7) ^ lrow ^ ((wave * A_INS + q) & 1);  // position ^ swz(row)
+        const i32x4_t desc_b = buffer_desc(We + (int64_t)((GATED && bpart) ? up_off + n0 : n0) * K, b_bytes);
+        // K, kdiv and the lane pass through empty asm statements so that the
+        // offsets below are computed per tile: hoisted out of the tile loop,
+        // their tile-independent parts would be kept in spilled registers
+        // and reloaded from scratch at every tile, each reload waiting
+        // (vector memory counter) for the previous tile's output stores.
+        int Kt = K, kd = kdiv, ln = lane;
+        asm volatile("" : "+s"(Kt), "+s"(kd), "+v"(ln));
+        const int lr = ln >> 3;  // this lane's row within a DMA instruction
+        // this lane's byte offset in A instruction g (LDS rows RPI*g ..)
+        auto a_off = [&](int g) -> uint32_t {
+            const int trow = g * RPI + lr;                       // row of the tile
+            const int kc = (ln & 7) ^ lr ^ (g & 1);                // position ^ swz(row)
             const int64_t r = r0 + trow;
             // Gathered rows: the RPI row indices of this instruction's rows
             // are read with scalar loads (the rows are the same for the whole
@@ -985,29 +1046,52 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
             // past cap (the shared expert's) take none, and the indices read
             // are clamped into the array.
             int32_t ri = 0;
-            const int64_t rb = r0 + (wave * A_INS + q) * RPI;
-            if (row_index != nullptr && rb < cap) {
+            const int64_t rb = r0 + (int64_t)g * RPI;
+            if (row_index != nullptr && rb + RPI <= cap) {
+                typedef int32_t rows_t __attribute__((ext_vector_type(RPI), aligned(4)));
+                const rows_t vj = ld_meta(reinterpret_cast<const rows_t *>(row_index + rb));  // one scalar load
+#pragma unroll
+                for (int j = 0; j < RPI; ++j) ri = lr == j ? vj[j] : ri;
+            } else if (row_index != nullptr && rb < cap) {
 #pragma unroll
                 for (int j = 0; j < RPI; ++j) {
                     const int32_t vj = ld_meta(row_index + (rb + j < cap ? rb + j : cap - 1));
-                    ri = lrow == j ? vj : ri;
+                    ri = lr == j ? vj : ri;
                 }
             }
             int64_t off;
             if (r >= r1) off = a_bytes;                            // past the expert: zeros
             else if (row_index) {
                 // the shared expert's rows are tokens shared_begin, ...
-                const int64_t tok = r < cap ? (int64_t)(ri / kdiv) : shared_begin + (r - cap);
-                off = (tok * K + kc * 8) * 2;
+                const int64_t tok = r < cap ? (int64_t)(ri / kd) : shared_begin + (r - cap);
+                off = (tok * Kt + kc * 8) * 2;
             }
-            else off = ((int64_t)trow * K + kc * 8) * 2;
-            src.voa[q] = (uint32_t)off;
-        }
+            else off = ((int64_t)trow * Kt + kc * 8) * 2;
+            return (uint32_t)off;
+        };
+        // ... in this wave's B instruction q, instruction g of the operand
+        auto b_off = [&](int q, int g) -> uint32_t {
+            const int prow = brow0 + q * RPI + lr;                 // row within its part
+            const int kc = (ln & 7) ^ lr ^ (g & 1);                // LDS row g*RPI+lr
+            return prow < nvalid ? (uint32_t)(((int64_t)prow * Kt + kc * 8) * 2) : (uint32_t)b_bytes;
+        };
+        if constexpr (ROLES) {
+            // one descriptor and one set of offsets: the operand this wave loads
+            src.ra = loads_a ? desc_a : desc_b;
+            if (loads_a) {
 #pragma unroll
-        for (int q = 0; q < B_INS; ++q) {
-            const int prow = brow0 + q * RPI + lrow;              // row within its part
-            const int kc = (lane & 7) ^ lrow ^ ((wave * B_INS + q) & 1);  // LDS row (wave*B_INS+q)*RPI+lrow
-            src.vob[q] = prow < nvalid ? (uint32_t)(((int64_t)prow * K + kc * 8) * 2) : (uint32_t)b_bytes;
+                for (int q = 0; q < NI; ++q) src.voa[q] = a_off(wave * NI + q);
+            } else {
+#pragma unroll
+                for (int q = 0; q < NI; ++q) src.voa[q] = b_off(q, wb * NI + q);
+            }
+        } else {
+            src.ra = desc_a;
+            src.rb = desc_b;
+#pragma unroll
+            for (int q = 0; q < A_INS; ++q) src.voa[q] = a_off(wave * A_INS + q);
+#pragma unroll
+            for (int q = 0; q < B_INS; ++q) src.vob[q] = b_off(q, wave * B_INS + q);
         }
 
         f32x16_t acc[MB][NB];
@@ -1027,67 +1111,128 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
         auto b_slot = [&](int j) { return ring_base + (uint32_t)((ASL * A_STAGE + (j % BSL) * B_STAGE) * 16); };
         auto a_ptr = [&](int j) { return a_ring + (j % ASL) * A_STAGE; };
         auto b_ptr = [&](int j) { return b_ring + (j % BSL) * B_STAGE; };
-        // prologue: B(0), then (A(t), B(t+1)) for t < LA; wait for A(0), B(0)
-#pragma unroll
-        for (int q = 0; q < B_INS; ++q) issue_b<BNt>(src, b_slot(0), kof(0), q);
-#pragma unroll
-        for (int t = 0; t < LA; ++t) {
-            if (t < ns) {
-#pragma unroll
-                for (int q = 0; q < A_INS; ++q) issue_a<BMt>(src, a_slot(t), kof(t), q);
-            }
-            if (t + 1 < ns) {
-#pragma unroll
-                for (int q = 0; q < B_INS; ++q) issue_b<BNt>(src, b_slot(t + 1), kof(t + 1), q);
-            }
-        }
-        // issued after A(0): B(1), then the pairs 1 .. LA-1
-        if (ns > LA) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(B_INS + (LA - 1) * (A_INS + B_INS)) : "memory");
-        else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-        lds_barrier();
-        load_frags(f, 0, a_ptr(0), b_ptr(0), 0, arow, brow);
-
-        // One slice.  HAVE_A: A(s+LA) exists; HAVE_B: B(s+LA+1) exists; loads
-        // absent at the tail keep the MFMA runs free of branches.
-        auto slice = [&](int s, auto have_a, auto have_b) {
-            constexpr bool HA = decltype(have_a)::value, HB = decltype(have_b)::value;
-            // loads issued after A(s+1) when this slice hands over: B(s+2) ..
-            // B(s+LA), A(s+2) .. A(s+LA) and the first half of B(s+LA+1)
-            constexpr int AFTER = HA ? (LA - 1) * (A_INS + B_INS) + (HB ? B_INS / 2 : 0) : 0;
-            const uint4 *sa = a_ptr(s), *sb = b_ptr(s);
-            load_frags(f, 1, sa, sb, 1, arow, brow);
-            __builtin_amdgcn_sched_barrier(0);
-            mfma_step<0, HA ? A_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 0, src, a_slot(s + LA), kof(s + LA), 0);
-            __builtin_amdgcn_sched_barrier(0);
-            load_frags(f, 0, sa, sb, 2, arow, brow);
-            __builtin_amdgcn_sched_barrier(0);
-            mfma_step<0, HA ? A_INS - A_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 1, src, a_slot(s + LA),
-                                                                   kof(s + LA), A_INS / 2);
-            __builtin_amdgcn_sched_barrier(0);
-            load_frags(f, 1, sa, sb, 3, arow, brow);
-            __builtin_amdgcn_sched_barrier(0);
-            mfma_step<1, HB ? B_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 0, src, b_slot(s + LA + 1), kof(s + LA + 1),
-                                                           0);
-            __builtin_amdgcn_sched_barrier(0);
-            if (HA || s + 1 < ns) {
-                // hand over to slice s+1 once A(s+1) (and B(s+1), issued before
-                // it) have landed
-                if (AFTER > 0) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(AFTER) : "memory");
-                else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-                lds_barrier();
-                load_frags(f, 0, a_ptr(s + 1), b_ptr(s + 1), 0, arow, brow);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            mfma_step<1, HB ? B_INS - B_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 1, src, b_slot(s + LA + 1),
-                                                                   kof(s + LA + 1), B_INS / 2);
-            __builtin_amdgcn_sched_barrier(0);
-        };
         using T_ = std::true_type;
         using F_ = std::false_type;
-        int s = 0;
-        for (; s + LA + 1 < ns; ++s) slice(s, T_{}, T_{});
-        for (; s + LA < ns; ++s) slice(s, T_{}, F_{});
-        for (; s < ns; ++s) slice(s, F_{}, F_{});
+        if constexpr (ROLES) {
+            // prologue: A(0) on the A loaders, B(0) and B(1) on the B loaders
+            if (loads_a) {
+#pragma unroll
+                for (int q = 0; q < NI; ++q) issue_own<NI>(src, a_slot(0), kof(0), q);
+                asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+            } else {
+#pragma unroll
+                for (int q = 0; q < NI; ++q) issue_own<NI>(src, b_slot(0), kof(0), q);
+                if (ns > 1) {
+#pragma unroll
+                    for (int q = 0; q < NI; ++q) issue_own<NI>(src, b_slot(1), kof(1), q);
+                    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(NI) : "memory");
+                } else {
+                    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+                }
+            }
+            lds_barrier();
+            load_frags(f, 0, a_ptr(0), b_ptr(0), 0, arow, brow);
+
+            // One slice: under k-steps 0-1 the A loaders issue A(s+1) (HA: it
+            // exists) and the B loaders B(s+2) (HB: it exists).
+            auto slice = [&](int s, auto has_a, auto has_b) {
+                constexpr bool HA = decltype(has_a)::value, HB = decltype(has_b)::value;
+                constexpr int NQ = HA || HB ? NI / 2 : 0;
+                const bool on = loads_a ? HA : HB;
+                const uint32_t dst = loads_a ? a_slot(s + 1) : b_slot(s + 2);
+                const int kn = loads_a ? kof(s + 1) : kof(s + 2);
+                const uint4 *sa = a_ptr(s), *sb = b_ptr(s);
+                load_frags(f, 1, sa, sb, 1, arow, brow);
+                __builtin_amdgcn_sched_barrier(0);
+                mfma_step_own<NI, NQ>(acc, f, 0, src, dst, kn, 0, on);
+                __builtin_amdgcn_sched_barrier(0);
+                load_frags(f, 0, sa, sb, 2, arow, brow);
+                __builtin_amdgcn_sched_barrier(0);
+                mfma_step_own<NI, NQ>(acc, f, 1, src, dst, kn, NI / 2, on);
+                __builtin_amdgcn_sched_barrier(0);
+                load_frags(f, 1, sa, sb, 3, arow, brow);
+                __builtin_amdgcn_sched_barrier(0);
+                mfma_step_own<NI, 0>(acc, f, 0, src, dst, kn, 0, false);
+                __builtin_amdgcn_sched_barrier(0);
+                if (s + 1 < ns) {
+                    // hand over to slice s+1 once this wave's loads of it
+                    // have landed: A(s+1), issued under this slice, or
+                    // B(s+1), issued under the last one (B(s+2) may still be
+                    // in flight)
+                    if (!loads_a && HB) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(NI) : "memory");
+                    else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+                    lds_barrier();
+                    load_frags(f, 0, a_ptr(s + 1), b_ptr(s + 1), 0, arow, brow);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                mfma_step_own<NI, 0>(acc, f, 1, src, dst, kn, 0, false);
+                __builtin_amdgcn_sched_barrier(0);
+            };
+            int s = 0;
+            for (; s + 2 < ns; ++s) slice(s, T_{}, T_{});
+            for (; s + 1 < ns; ++s) slice(s, T_{}, F_{});
+            for (; s < ns; ++s) slice(s, F_{}, F_{});
+        } else {
+            // prologue: B(0), then (A(t), B(t+1)) for t < LA; wait for A(0), B(0)
+    #pragma unroll
+            for (int q = 0; q < B_INS; ++q) issue_b<BNt>(src, b_slot(0), kof(0), q);
+    #pragma unroll
+            for (int t = 0; t < LA; ++t) {
+                if (t < ns) {
+    #pragma unroll
+                    for (int q = 0; q < A_INS; ++q) issue_a<BMt>(src, a_slot(t), kof(t), q);
+                }
+                if (t + 1 < ns) {
+    #pragma unroll
+                    for (int q = 0; q < B_INS; ++q) issue_b<BNt>(src, b_slot(t + 1), kof(t + 1), q);
+                }
+            }
+            // issued after A(0): B(1), then the pairs 1 .. LA-1
+            if (ns > LA) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(B_INS + (LA - 1) * (A_INS + B_INS)) : "memory");
+            else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+            lds_barrier();
+            load_frags(f, 0, a_ptr(0), b_ptr(0), 0, arow, brow);
+
+            // One slice.  HAVE_A: A(s+LA) exists; HAVE_B: B(s+LA+1) exists; loads
+            // absent at the tail keep the MFMA runs free of branches.
+            auto slice = [&](int s, auto have_a, auto have_b) {
+                constexpr bool HA = decltype(have_a)::value, HB = decltype(have_b)::value;
+                // loads issued after A(s+1) when this slice hands over: B(s+2) ..
+                // B(s+LA), A(s+2) .. A(s+LA) and the first half of B(s+LA+1)
+                constexpr int AFTER = HA ? (LA - 1) * (A_INS + B_INS) + (HB ? B_INS / 2 : 0) : 0;
+                const uint4 *sa = a_ptr(s), *sb = b_ptr(s);
+                load_frags(f, 1, sa, sb, 1, arow, brow);
+                __builtin_amdgcn_sched_barrier(0);
+                mfma_step<0, HA ? A_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 0, src, a_slot(s + LA), kof(s + LA), 0);
+                __builtin_amdgcn_sched_barrier(0);
+                load_frags(f, 0, sa, sb, 2, arow, brow);
+                __builtin_amdgcn_sched_barrier(0);
+                mfma_step<0, HA ? A_INS - A_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 1, src, a_slot(s + LA),
+                                                                       kof(s + LA), A_INS / 2);
+                __builtin_amdgcn_sched_barrier(0);
+                load_frags(f, 1, sa, sb, 3, arow, brow);
+                __builtin_amdgcn_sched_barrier(0);
+                mfma_step<1, HB ? B_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 0, src, b_slot(s + LA + 1), kof(s + LA + 1),
+                                                               0);
+                __builtin_amdgcn_sched_barrier(0);
+                if (HA || s + 1 < ns) {
+                    // hand over to slice s+1 once A(s+1) (and B(s+1), issued before
+                    // it) have landed
+                    if (AFTER > 0) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(AFTER) : "memory");
+                    else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+                    lds_barrier();
+                    load_frags(f, 0, a_ptr(s + 1), b_ptr(s + 1), 0, arow, brow);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                mfma_step<1, HB ? B_INS - B_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 1, src, b_slot(s + LA + 1),
+                                                                       kof(s + LA + 1), B_INS / 2);
+                __builtin_amdgcn_sched_barrier(0);
+            };
+            int s = 0;
+            for (; s + LA + 1 < ns; ++s) slice(s, T_{}, T_{});
+            for (; s + LA < ns; ++s) slice(s, T_{}, F_{});
+            for (; s < ns; ++s) slice(s, F_{}, F_{});
+        }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         lds_barrier();  // every wave is done with the ring before it is reused
 
