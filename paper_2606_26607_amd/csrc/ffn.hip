@@ -586,6 +586,14 @@ constexpr int BIG_BK = 64;        // K per slice
 constexpr int CPR = BIG_BK / 8;   // 16-byte chunks per LDS row
 constexpr int RPI = 64 / CPR;     // rows per DMA instruction
 static_assert(RPI == 8, "a lane's DMA row is lane / 8");
+
+// RPI consecutive row indices from a 4-byte aligned address, as one scalar
+// load (a read of metadata like ld_meta's).
+typedef int32_t rows_t __attribute__((ext_vector_type(RPI), aligned(4)));
+__device__ __forceinline__ rows_t ld_rows(const int32_t *p)
+{
+    return *(const __attribute__((address_space(4))) rows_t *)p;
+}
 constexpr int A_SLOTS = 2, B_SLOTS = 3;        // large tiles: A(s+1), B(s+2) in flight
 constexpr int SA_SLOTS = 3, SB_SLOTS = 4;      // small-row tiles: A(s+2), B(s+3) in flight
 constexpr int BIG_RING_CHUNKS = (A_SLOTS * 256 + B_SLOTS * 256) * CPR;  // 160 KB of 16-byte chunks
@@ -1048,8 +1056,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
             int32_t ri = 0;
             const int64_t rb = r0 + (int64_t)g * RPI;
             if (row_index != nullptr && rb + RPI <= cap) {
-                typedef int32_t rows_t __attribute__((ext_vector_type(RPI), aligned(4)));
-                const rows_t vj = ld_meta(reinterpret_cast<const rows_t *>(row_index + rb));  // one scalar load
+                const rows_t vj = ld_rows(row_index + rb);
 #pragma unroll
                 for (int j = 0; j < RPI; ++j) ri = lr == j ? vj[j] : ri;
             } else if (row_index != nullptr && rb < cap) {
