@@ -1631,8 +1631,9 @@ __global__ __launch_bounds__(1024) void layer_perm_sched_kernel(const int32_t *_
 // permutation's chunks), writes those whose first pair lies in the chunk
 // (every token once over the grid) and counts the chunk's pairs per local
 // expert (the permutation's histogram row c).
+constexpr int RC_THREADS = 512;  // route/count block: 512 / G tokens routed at once
 template <int G, int S, int ROUNDS>
-__global__ __launch_bounds__(256) void layer_route_count_kernel(const float *__restrict__ logits, int64_t T, int E,
+__global__ __launch_bounds__(RC_THREADS) void layer_route_count_kernel(const float *__restrict__ logits, int64_t T, int E,
                                                                 int k, int e0, int El, int32_t *__restrict__ ids,
                                                                 float *__restrict__ w,
                                                                 int32_t *__restrict__ chunk_cnt)
@@ -1646,16 +1647,16 @@ __global__ __launch_bounds__(256) void layer_route_count_kernel(const float *__r
     const int64_t p1 = p0 + CH < npairs ? p0 + CH : npairs;
     const int64_t ta = p0 / k, tb = (p1 + k - 1) / k;  // tokens [ta, tb) have pairs in the chunk
     const int sub = tid % G;
-    for (int64_t t = ta + tid / G; t < tb; t += 256 / G)
+    for (int64_t t = ta + tid / G; t < tb; t += RC_THREADS / G)
         route_dev::route_token<G, S>(logits + t * E, E, k, sub, lid + (t - ta) * k, lw + (t - ta) * k);
     if (tid < 64) hist[tid] = 0;
     __syncthreads();
     const int64_t tw = (p0 + k - 1) / k;  // the first token whose first pair lies in the chunk
-    for (int64_t q = tw * k + tid; q < tb * k; q += 256) {
+    for (int64_t q = tw * k + tid; q < tb * k; q += RC_THREADS) {
         ids[q] = lid[q - ta * k];
         w[q] = lw[q - ta * k];
     }
-    for (int64_t p = p0 + tid; p < p1; p += 256) {
+    for (int64_t p = p0 + tid; p < p1; p += RC_THREADS) {
         const int le = permute_dev::local_index(lid[p - ta * k], e0, El);
         if (le < El) atomicAdd(&hist[le], 1);
     }
@@ -1984,11 +1985,11 @@ struct LaunchRouteCount {
                          int32_t *chunk_cnt, int64_t nchunks, bool short_chunks, hipStream_t s)
     {
         if (short_chunks)
-            layer_route_count_kernel<G, S, 4><<<dim3((unsigned)nchunks), dim3(256), 0, s>>>(logits, T, E, k, e0, El,
-                                                                                              ids, w, chunk_cnt);
+            layer_route_count_kernel<G, S, 4><<<dim3((unsigned)nchunks), dim3(RC_THREADS), 0, s>>>(
+                logits, T, E, k, e0, El, ids, w, chunk_cnt);
         else
-            layer_route_count_kernel<G, S, 16><<<dim3((unsigned)nchunks), dim3(256), 0, s>>>(logits, T, E, k, e0, El,
-                                                                                               ids, w, chunk_cnt);
+            layer_route_count_kernel<G, S, 16><<<dim3((unsigned)nchunks), dim3(RC_THREADS), 0, s>>>(
+                logits, T, E, k, e0, El, ids, w, chunk_cnt);
         return hipGetLastError();
     }
 };
