@@ -174,10 +174,15 @@ struct SchedShape {
 //     dealt over all workgroups (the idle ones first) after their large
 //     tiles, when one whole tile takes less than a stream-K share plus the
 //     fixed cost of a stream-K piece (prologue and partial sums);
-//   SM_PIECES_ALL: else stream-K over all workgroups after their large tiles.
+//   SM_PIECES_ALL: else stream-K over all workgroups after their large tiles;
+//   SM_PIECES_PAIR: with no idle workgroups and at most G/2 tiles, stream-K
+//     over 2 * ts workgroups (spread over the dies) after their large tiles,
+//     so that each tile is cut into two halves of K, when that is the
+//     cheapest of the three (two pieces pay the fixed cost of a piece and
+//     one partial each, PAIR_OVH large slices in all).
 // extra = what the small-row work adds to the large tiles' rounds, in units
 // of one large-tile K-slice.
-enum SmallMode { SM_PIECES_IDLE, SM_WHOLE_IDLE, SM_WHOLE_ALL, SM_PIECES_ALL };
+enum SmallMode { SM_PIECES_IDLE, SM_WHOLE_IDLE, SM_WHOLE_ALL, SM_PIECES_ALL, SM_PIECES_PAIR };
 
 // x / g for x >= 0, in 32 bits whenever x fits (it always does in practice;
 // a 64-bit division is a long instruction sequence on the GPU)
@@ -186,6 +191,7 @@ __device__ __forceinline__ int64_t div_g(int64_t x, int g)
     return x <= 0x7fffffff ? (int64_t)((uint32_t)x / (uint32_t)g) : x / g;
 }
 constexpr float PIECE_OVH = 8.0f;  // fixed cost of a stream-K piece, in large slices
+constexpr float PAIR_OVH = 3.0f;   // fixed cost of splitting a whole small-row tile in two, in large slices
 struct SmallPlan {
     SmallMode mode;
     int idle;
@@ -211,6 +217,9 @@ __device__ __forceinline__ SmallPlan small_plan(int64_t tl, int64_t ts, int nk, 
     if (idle && (int64_t)cost_num * ts <= (int64_t)SMALL_COST_DEN * idle) return SmallPlan{SM_PIECES_IDLE, idle, 0.f};
     if (idle && ts <= (int64_t)idle * wfit) return SmallPlan{SM_WHOLE_IDLE, idle, 0.f};
     const float pieces = (float)cost_num / (float)SMALL_COST_DEN * (float)ts * (float)nk / (float)G;
+    const float pair = 0.5f * whole + PAIR_OVH;
+    if (idle == 0 && 2 * ts <= G && pair < whole && pair < pieces + PIECE_OVH)
+        return SmallPlan{SM_PIECES_PAIR, idle, pair};
     if (ts <= G && whole < pieces + PIECE_OVH) return SmallPlan{SM_WHOLE_ALL, idle, ts > idle ? whole : 0.f};
     return SmallPlan{SM_PIECES_ALL, idle, pieces};
 }
@@ -1455,6 +1464,12 @@ __device__ __forceinline__ SmallGroup small_group(int64_t tl, int64_t ts, int nk
                                    whole_time(nk, kind.whole_num));
     const bool deal = p.mode == SM_WHOLE_IDLE || p.mode == SM_WHOLE_ALL;
     if (p.mode == SM_PIECES_ALL) return SmallGroup{vx, G, false};
+    if (p.mode == SM_PIECES_PAIR) {
+        // the first 2 * ts workgroups in (workgroup within die, die) order
+        const int P = G / 8, size = (int)(2 * ts);
+        const int v = (vx % P) * 8 + vx / P;
+        return SmallGroup{v < size ? v : -1, size, false};
+    }
     // die d holds c_d = tl*(d+1)/8 - tl*d/8 whole tiles; with R rounds (the
     // busiest die's), its workgroups u < c_d - (R-1)*P are busy in the last
     // round and the others idle (G - tl % G of them in all; none, and all
