@@ -326,9 +326,9 @@ moe_status moe_kv_move(int n_src, const uint16_t *const *src_k, const uint16_t *
  * moe_policy: the switch coordinator's state (Sec. 4.5), owned by the
  *   caller; set it up with moe_policy_init and feed moe_policy_step the
  *   global in-flight request count once per decode iteration, between
- *   steps.  In TP it switches to EP as soon as the latest count exceeds
- *   t_high; in EP it switches back to TP only when the mean count over the
- *   last `window` iterations (fewer at start) falls below t_low <= t_high.
+ *   steps.  The rule has hysteresis: from TP, one sample above t_high is
+ *   enough to request EP; from EP, TP is requested once the average of
+ *   the last `window` samples (fewer at start) is under t_low <= t_high.
  *   After a switch, and after a cancelled attempt, no attempt is made for
  *   cooldown_s seconds (times are the caller's clock, e.g. seconds since
  *   start).  target_fits tells whether the other mode can hold the live
