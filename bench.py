@@ -662,7 +662,9 @@ def main():
 
     # Measured ceilings on this GPU (references, not part of the path): the
     # vendor GEMM (torch.matmul, hipBLASLt) on the dense shape of the
-    # gate-up GEMM, and a device-to-device copy.
+    # gate-up GEMM, the library's matrix-core reference loop (bf16 MFMAs
+    # with no memory traffic, on random and on zero operands), and a
+    # device-to-device copy.
     ceilings = None
     if not args.no_ceilings:
         def timed(fn, reps=20):
@@ -684,6 +686,21 @@ def main():
             ceilings["vendor_gemm_tflops"] = 2.0 * m * cfg.H * 2 * cfg.I_s / t / 1e12
             ceilings["vendor_gemm_shape"] = [m, 2 * cfg.I_s, cfg.H]
             del A, B
+            # the clock settles over the first calls of a sustained MFMA load:
+            # the best of 8 back-to-back calls of about 6 ms each
+            out = torch.empty(torch.cuda.get_device_properties(0).multi_processor_count * 512,
+                              dtype=torch.float32, device=dev)
+            for key, zero in (("mfma_loop_random_tflops", False), ("mfma_loop_zero_tflops", True)):
+                best = 0.0
+                for _ in range(8):
+                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    a.record()
+                    flops = moe.calib_mfma(out, 20000, zero_operands=zero)
+                    b.record()
+                    torch.cuda.synchronize()
+                    best = max(best, flops / (a.elapsed_time(b) * 1e-3) / 1e12)
+                ceilings[key] = best
+            del out
         src = torch.empty(256 << 20, dtype=torch.int16, device=dev).fill_(1)
         dst = torch.empty_like(src)
         t = timed(lambda: dst.copy_(src), reps=10)
@@ -692,6 +709,7 @@ def main():
         if roof is not None:
             if roof["bound"] == "mfma" and "vendor_gemm_tflops" in ceilings:
                 roof["frac_of_vendor_gemm"] = roof["achieved"] / ceilings["vendor_gemm_tflops"]
+                roof["frac_of_mfma_loop_random"] = roof["achieved"] / ceilings["mfma_loop_random_tflops"]
             if roof["bound"] == "hbm":
                 roof["frac_of_copy"] = roof["achieved"] / ceilings["copy_gbs"]
 

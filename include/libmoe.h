@@ -425,6 +425,23 @@ moe_status moe_timing_device_reset(void);
 moe_status moe_timing_device_read(int kind, double *total_ms, int64_t *launches);
 
 moe_status moe_timing_enable(int enable);
+
+/*
+ * Matrix-core reference loop for measurement, not part of the layer: the
+ * rate at which this device's bf16 matrix cores run with nothing else
+ * limiting them.  Launches `grid` workgroups of 8 waves (one per compute
+ * unit when grid is the CU count); every wave keeps 2 x 4 independent
+ * 32x32 fp32 accumulators and issues `iters` rounds of 8
+ * v_mfma_f32_32x32x16_bf16 on operands fixed at its start: hashed uniform
+ * values in [-1, 1) and [-0.02, 0.02), or zeros when zero_operands != 0
+ * (the same instruction stream without switching activity, so without the
+ * clock reduction random operands cause).  Each thread then writes the sum
+ * of its accumulators to out[b * 512 + thread] (out: grid * 512 floats,
+ * device memory owned by the caller).  One call performs
+ * grid * 8 * iters * 8 * 32768 floating-point operations.
+ * 1 <= grid <= 65536, 1 <= iters <= 2^24; otherwise MOE_ERR_INVALID_ARG.
+ */
+moe_status moe_calib_mfma(int grid, int iters, int zero_operands, float *out, void *stream);
 /* Time only the kinds whose bit (1 << kind) is set in `kinds` (0 disables);
  * bits at or above MOE_K_COUNT give MOE_ERR_INVALID_ARG. */
 moe_status moe_timing_enable_mask(uint32_t kinds);

@@ -92,6 +92,7 @@ def lib():
         "moe_timing_enable_mask": ([ctypes.c_uint32], i32),
         "moe_timing_reset": ([], i32),
         "moe_timing_read": ([i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)], i32),
+        "moe_calib_mfma": ([i32, i32, i32, vp, vp], i32),
     }
     for name, (args, res) in sigs.items():
         fn = getattr(L, name)
@@ -663,4 +664,15 @@ def timing_device_read(kind: str):
     n = ctypes.c_int64(0)
     _check(lib().moe_timing_device_read(KERNEL_KINDS[kind], ctypes.byref(ms), ctypes.byref(n)))
     return ms.value, n.value
+
+
+def calib_mfma(out: torch.Tensor, iters: int, zero_operands: bool = False, stream=None) -> float:
+    """Enqueue the matrix-core reference loop (one workgroup per 512 floats
+    of `out`) and return the floating-point operations it performs."""
+    _need(out, torch.float32, "out", 1)
+    if out.numel() == 0 or out.numel() % 512:
+        raise ValueError("calib_mfma: out must hold a positive multiple of 512 floats")
+    grid = out.numel() // 512
+    _check(lib().moe_calib_mfma(grid, int(iters), 1 if zero_operands else 0, _ptr(out), _stream(stream)))
+    return float(grid) * 8 * iters * 8 * 32768
 

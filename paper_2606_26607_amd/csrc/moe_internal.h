@@ -73,6 +73,10 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
                               int64_t shared_rows, const uint16_t *sw13, const uint16_t *sw2,
                               uint16_t *shared_y, void *ws, hipStream_t s);
 
+// Matrix-core reference loop (calib.hip): grid workgroups of 512 threads,
+// out[grid * 512].
+hipError_t launch_calib_mfma(int grid, int iters, int zero, float *out, hipStream_t s);
+
 // dir: MOE_EP_TO_TP or MOE_TP_TO_EP; src arrays are host arrays of P device
 // pointers (NULL pairs skipped).
 hipError_t launch_reshard(int dir, int P, int r, int E, int H, int I, const uint16_t *const *src_w13,

@@ -254,3 +254,10 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(binding, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(ImportError):
         binding.lib()
+
+
+@pytest.mark.parametrize("grid,iters", [(0, 1), (65537, 1), (1, 0), (1, 1 << 25)])
+def test_calib_mfma_rejects(grid, iters):
+    L = moe.lib()
+    assert L.moe_calib_mfma(grid, iters, 0, FAKE, None) == INVALID
+    assert L.moe_calib_mfma(1, 1, 0, None, None) == INVALID
