@@ -649,6 +649,14 @@ __device__ __forceinline__ void dma16(i32x4_t desc, uint32_t lds, uint32_t voff,
                  :: "s"(lds), "v"(voff), "s"(desc), "s"(soff) : "memory");
 }
 
+// The same with the non-temporal hint, for weights that are streamed
+// through once per launch.
+__device__ __forceinline__ void dma16_nt(i32x4_t desc, uint32_t lds, uint32_t voff, uint32_t soff)
+{
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen nt lds"
+                 :: "s"(lds), "v"(voff), "s"(desc), "s"(soff) : "memory");
+}
+
 // The same with an agent-coherent (sc1) load, for data another workgroup
 // (possibly on another die, behind another L2) stored with sc1.
 __device__ __forceinline__ void dma16_sc1(i32x4_t desc, uint32_t lds, uint32_t voff, uint32_t soff)
@@ -684,11 +692,12 @@ __device__ __forceinline__ void issue_a(const SliceSrc &a, uint32_t slot, int k0
     dma16(a.ra, slot + (a.wave * A_INS + q) * 1024, a.voa[q], (uint32_t)k0 * 2u);
 }
 
-template <int BNt>
+template <int BNt, bool NT>
 __device__ __forceinline__ void issue_b(const SliceSrc &a, uint32_t slot, int k0, int q)
 {
     constexpr int B_INS = BNt / RPI / GEMM_WAVES;
-    dma16(a.rb, slot + (a.wave * B_INS + q) * 1024, a.vob[q], (uint32_t)k0 * 2u);
+    if constexpr (NT) dma16_nt(a.rb, slot + (a.wave * B_INS + q) * 1024, a.vob[q], (uint32_t)k0 * 2u);
+    else dma16(a.rb, slot + (a.wave * B_INS + q) * 1024, a.vob[q], (uint32_t)k0 * 2u);
 }
 
 // Instruction q of this wave's run of NI instructions of one operand (A or
@@ -723,8 +732,9 @@ __device__ __forceinline__ void load_frags(Frags<MB, NB> &f, int sl, const uint4
 }
 
 // The MFMAs of one k-step (MB x NB blocks) with NQ loads of A (IS_B = 0) or
-// B (IS_B = 1), numbered q0 .. q0+NQ-1, spread evenly between them.
-template <int IS_B, int NQ, int MB, int NB, int BMt, int BNt>
+// B (IS_B = 1), numbered q0 .. q0+NQ-1, spread evenly between them (B with
+// the non-temporal hint when NTB).
+template <int IS_B, int NQ, int MB, int NB, int BMt, int BNt, bool NTB>
 __device__ __forceinline__ void mfma_step(f32x16_t (&acc)[MB][NB], const Frags<MB, NB> &f, int sl,
                                           const SliceSrc &src, uint32_t slot, int k0, int q0)
 {
@@ -741,7 +751,7 @@ __device__ __forceinline__ void mfma_step(f32x16_t (&acc)[MB][NB], const Frags<M
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int q = qa; q < qb; ++q) {
-                    if (IS_B) issue_b<BNt>(src, slot, k0, q0 + q);
+                    if (IS_B) issue_b<BNt, NTB>(src, slot, k0, q0 + q);
                     else issue_a<BMt>(src, slot, k0, q0 + q);
                 }
                 __builtin_amdgcn_sched_barrier(0);
@@ -920,7 +930,7 @@ struct TileClass {
 // workgroup's LDS (at least the class's ring size).  Pointers are restrict
 // parameters so that the inlined body keeps the no-alias facts of kernel
 // arguments (its loads are not reordered around the stores it makes).
-template <int BMt, int BNt, bool GATED, int WM, bool TAIL, int ASL, int BSL>
+template <int BMt, int BNt, bool GATED, int WM, bool TAIL, int ASL, int BSL, bool STREAM>
 __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restrict__ A,
                                            const int32_t *__restrict__ row_index, int kdiv, int64_t a_rows,
                                            const int32_t *__restrict__ offsets,
@@ -1191,7 +1201,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
         } else {
             // prologue: B(0), then (A(t), B(t+1)) for t < LA; wait for A(0), B(0)
     #pragma unroll
-            for (int q = 0; q < B_INS; ++q) issue_b<BNt>(src, b_slot(0), kof(0), q);
+            for (int q = 0; q < B_INS; ++q) issue_b<BNt, STREAM>(src, b_slot(0), kof(0), q);
     #pragma unroll
             for (int t = 0; t < LA; ++t) {
                 if (t < ns) {
@@ -1200,7 +1210,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                 }
                 if (t + 1 < ns) {
     #pragma unroll
-                    for (int q = 0; q < B_INS; ++q) issue_b<BNt>(src, b_slot(t + 1), kof(t + 1), q);
+                    for (int q = 0; q < B_INS; ++q) issue_b<BNt, STREAM>(src, b_slot(t + 1), kof(t + 1), q);
                 }
             }
             // issued after A(0): B(1), then the pairs 1 .. LA-1
@@ -1219,16 +1229,16 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                 const uint4 *sa = a_ptr(s), *sb = b_ptr(s);
                 load_frags(f, 1, sa, sb, 1, arow, brow);
                 __builtin_amdgcn_sched_barrier(0);
-                mfma_step<0, HA ? A_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 0, src, a_slot(s + LA), kof(s + LA), 0);
+                mfma_step<0, HA ? A_INS / 2 : 0, MB, NB, BMt, BNt, STREAM>(acc, f, 0, src, a_slot(s + LA), kof(s + LA), 0);
                 __builtin_amdgcn_sched_barrier(0);
                 load_frags(f, 0, sa, sb, 2, arow, brow);
                 __builtin_amdgcn_sched_barrier(0);
-                mfma_step<0, HA ? A_INS - A_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 1, src, a_slot(s + LA),
+                mfma_step<0, HA ? A_INS - A_INS / 2 : 0, MB, NB, BMt, BNt, STREAM>(acc, f, 1, src, a_slot(s + LA),
                                                                        kof(s + LA), A_INS / 2);
                 __builtin_amdgcn_sched_barrier(0);
                 load_frags(f, 1, sa, sb, 3, arow, brow);
                 __builtin_amdgcn_sched_barrier(0);
-                mfma_step<1, HB ? B_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 0, src, b_slot(s + LA + 1), kof(s + LA + 1),
+                mfma_step<1, HB ? B_INS / 2 : 0, MB, NB, BMt, BNt, STREAM>(acc, f, 0, src, b_slot(s + LA + 1), kof(s + LA + 1),
                                                                0);
                 __builtin_amdgcn_sched_barrier(0);
                 if (HA || s + 1 < ns) {
@@ -1240,7 +1250,7 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
                     load_frags(f, 0, a_ptr(s + 1), b_ptr(s + 1), 0, arow, brow);
                     __builtin_amdgcn_sched_barrier(0);
                 }
-                mfma_step<1, HB ? B_INS - B_INS / 2 : 0, MB, NB, BMt, BNt>(acc, f, 1, src, b_slot(s + LA + 1),
+                mfma_step<1, HB ? B_INS - B_INS / 2 : 0, MB, NB, BMt, BNt, STREAM>(acc, f, 1, src, b_slot(s + LA + 1),
                                                                        kof(s + LA + 1), B_INS / 2);
                 __builtin_amdgcn_sched_barrier(0);
             };
@@ -1515,8 +1525,10 @@ __device__ unsigned long long g_dev_ts[2][8][DEV_TS_SLOTS];  // [0]: start (min)
 // its workgroups: these stream weights, and spreading them over many CUs is
 // what reaches HBM bandwidth) in the same persistent grid.  The classes
 // cover disjoint rows, so a workgroup goes from its large tiles to its
-// small-row share without waiting for anyone.
-template <bool GATED>
+// small-row share without waiting for anyone.  STREAM: the small-row class
+// loads its weights with the non-temporal hint (launches whose weights
+// cannot stay in the last-level cache from one step to the next).
+template <bool GATED, bool STREAM>
 __global__ __attribute__((amdgpu_flat_work_group_size(GEMM_THREADS, GEMM_THREADS), amdgpu_waves_per_eu(2, 2)))
 void gemm_grouped(GemmArgs g, TileClass small, TileClass large, int tslot)
 {
@@ -1525,7 +1537,7 @@ void gemm_grouped(GemmArgs g, TileClass small, TileClass large, int tslot)
     constexpr int OUTN = GATED ? BIGN / 2 : BIGN;
     // die-major id: the hardware deals workgroups to the 8 dies round robin
     const int vx = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
-    gemm_class<BIGM, BIGN, GATED, BIG_WM, false, A_SLOTS, B_SLOTS>(
+    gemm_class<BIGM, BIGN, GATED, BIG_WM, false, A_SLOTS, B_SLOTS, false>(
         ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, large.tile_prefix, nullptr, g.El, g.ne, g.cap,
         g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh, large.tile_cnt,
         large.partials, vx, gridDim.x, false);
@@ -1538,12 +1550,12 @@ void gemm_grouped(GemmArgs g, TileClass small, TileClass large, int tslot)
                                       (int64_t)small.tile_prefix[g.ne] * n_tiles, g.K / BIG_BK, gridDim.x,
                                       tall ? SMALL128 : SMALL64, vx);
     if (tall)
-        gemm_class<SMALL128.rows, BIGN, GATED, SMALL_WM, true, S128_ASL, S128_BSL>(
+        gemm_class<SMALL128.rows, BIGN, GATED, SMALL_WM, true, S128_ASL, S128_BSL, STREAM>(
             ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, small.tile_prefix, small.mtile, g.El, g.ne, g.cap,
             g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh,
             small.tile_cnt, small.partials, sg.v, sg.size, sg.deal);
     else
-        gemm_class<SMALL64.rows, BIGN, GATED, SMALL_WM, true, SA_SLOTS, SB_SLOTS>(
+        gemm_class<SMALL64.rows, BIGN, GATED, SMALL_WM, true, SA_SLOTS, SB_SLOTS, STREAM>(
             ring, g.A, g.row_index, g.kdiv, g.a_rows, g.offsets, g.split, small.tile_prefix, small.mtile, g.El, g.ne, g.cap,
             g.shared_rows, g.shared_begin, g.N, g.K, g.W, g.w_stride, g.Wsh, g.up_off, g.C, g.Csh,
             small.tile_cnt, small.partials, sg.v, sg.size, sg.deal);
@@ -1757,6 +1769,22 @@ int device_ts_slot(int kind)
     return (int)g_dts_kind.size() - 1;
 }
 
+// Whether a grouped GEMM launch streams its weights: when the local
+// experts' weights of the GEMM (elems bf16 values) exceed half of the 256 MB
+// last-level cache, they do not stay cached from one step to the next, and
+// the small-row tiles (the decode path, one reader per weight panel) load
+// them with the non-temporal hint.  Measured on the DeepSeek-V3-shaped
+// decode slices: gate-up 285 -> 252 us (T = 64), 343 -> 301 us (T = 512),
+// down 155 -> 137 us and 188 -> 169 us.  Below the threshold the weights
+// are re-read from the cache in the next step (the Qwen-shaped slice's
+// 100 MB, prefill tail tiles sharing panels with large tiles), and the hint
+// made those launches 1-10% slower.
+constexpr int64_t STREAM_WEIGHT_BYTES = (int64_t)128 << 20;
+bool weights_streamed(int64_t elems)
+{
+    return elems * 2 > STREAM_WEIGHT_BYTES;
+}
+
 int device_cus()
 {
     int dev = 0, cus = 0;
@@ -1903,9 +1931,13 @@ hipError_t launch_gemms(const FfnCall &c, const uint16_t *x, int64_t x_rows, con
             KernelTimer timer(MOE_K_GATE_UP, s);
             const GemmArgs g{x,   row_index, kdiv, x_rows, offsets, c.split, El, ne, cap, sc, shared_begin,
                              Is,  H,         w13,  (int64_t)2 * Is * H, sw13, Is, c.h, c.h_sh};
-            gemm_grouped<true><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
-                g, TileClass{c.pre_s, c.mt_g, cs_gu, c.part_s}, TileClass{c.pre, nullptr, c_gu, c.part},
-                device_ts_slot(MOE_K_GATE_UP));
+            const TileClass sm{c.pre_s, c.mt_g, cs_gu, c.part_s}, lg{c.pre, nullptr, c_gu, c.part};
+            if (weights_streamed((int64_t)El * 2 * Is * H))
+                gemm_grouped<true, true><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
+                    g, sm, lg, device_ts_slot(MOE_K_GATE_UP));
+            else
+                gemm_grouped<true, false><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
+                    g, sm, lg, device_ts_slot(MOE_K_GATE_UP));
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         if (H / BIG_BK >= SPLIT_MIN_NK) {  // the large tiles may have been split over K
@@ -1918,9 +1950,13 @@ hipError_t launch_gemms(const FfnCall &c, const uint16_t *x, int64_t x_rows, con
             KernelTimer timer(MOE_K_DOWN, s);
             const GemmArgs g{c.h, nullptr, 1, rows, offsets, c.split_d, El, ne, cap, sc, shared_begin,
                              H,   Is,      w2, (int64_t)H * Is, sw2, 0, y, shared_y};
-            gemm_grouped<false><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
-                g, TileClass{c.pre_sd, c.mt_d, cs_dn, c.part_s}, TileClass{c.pre_ld, nullptr, c_dn, c.part},
-                device_ts_slot(MOE_K_DOWN));
+            const TileClass sm{c.pre_sd, c.mt_d, cs_dn, c.part_s}, lg{c.pre_ld, nullptr, c_dn, c.part};
+            if (weights_streamed((int64_t)El * H * Is))
+                gemm_grouped<false, true><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
+                    g, sm, lg, device_ts_slot(MOE_K_DOWN));
+            else
+                gemm_grouped<false, false><<<dim3((unsigned)L.grid), dim3(GEMM_THREADS), 0, s>>>(
+                    g, sm, lg, device_ts_slot(MOE_K_DOWN));
             if ((err = hipGetLastError()) != hipSuccess) return err;
         }
         if (Is / BIG_BK >= SPLIT_MIN_NK) {
