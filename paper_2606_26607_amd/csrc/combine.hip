@@ -30,9 +30,8 @@ __device__ __forceinline__ void add8(float acc[8], uint4 v, float s)
 
 // One work item = one token's chunk of blockDim.x 16-byte vectors (one per
 // thread), so that a small batch still spreads over the whole GPU and each
-// thread has a single row chunk in flight per source.  The token's slots are
-// read by every thread from the same address (a uniform load), so no
-// barrier is needed.
+// thread has a single row chunk in flight per source.  Every wave loads the
+// token's slots itself (one lane per slot), so no barrier is needed.
 __global__ __launch_bounds__(256) void combine_kernel(const uint16_t *__restrict__ y, int64_t y_rows,
                                                       const int32_t *__restrict__ pair_to_row,
                                                       const float *__restrict__ w, int64_t T, int k,
@@ -45,6 +44,12 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint16_t *__restrict
     for (int64_t item = blockIdx.x; item < T * chunks; item += gridDim.x) {
         const int64_t t = item / chunks;
         const int i = (int)(item - t * chunks) * (int)blockDim.x + (int)threadIdx.x;
+        // the token's k slots (k <= 16): lane j of every wave loads slot j's
+        // row and weight, and the slot loop reads them from those lanes, so
+        // the k index loads are one load instead of a chain of k
+        const int lane = (int)threadIdx.x & 63;
+        const int32_t my_r = lane < k ? pair_to_row[t * k + lane] : -1;
+        const float my_w = lane < k ? w[t * k + lane] : 0.f;
         if (i >= vecs) continue;
         const bool has_shared = shared_y != nullptr && t >= sb && t < sb + sc;
         uint4 *o = reinterpret_cast<uint4 *>(out + t * H);
@@ -52,8 +57,10 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint16_t *__restrict
         if (accumulate) add8(acc, o[i], 1.0f);
         if (has_shared) add8(acc, reinterpret_cast<const uint4 *>(shared_y + (t - sb) * H)[i], 1.0f);
         for (int j = 0; j < k; ++j) {
-            const int32_t r = pair_to_row[t * k + j];
-            if (r >= 0 && r < y_rows) add8(acc, load_last_use(reinterpret_cast<const uint4 *>(y + (int64_t)r * H) + i), w[t * k + j]);
+            const int32_t r = __builtin_amdgcn_readlane(my_r, j);
+            if (r >= 0 && r < y_rows)
+                add8(acc, load_last_use(reinterpret_cast<const uint4 *>(y + (int64_t)r * H) + i),
+                     __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_w), j)));
         }
         uint4 v;
         v.x = pack_bf16(acc[0], acc[1]);
