@@ -40,13 +40,36 @@ __device__ __forceinline__ uint32_t dpp32(uint32_t v)
     return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true);
 }
 
-// The steps that combine a group of G lanes (G <= 16 uses DPP: after the two
-// quad swaps every quad agrees, the half-row mirror joins the two quads of a
-// half row, the row mirror joins the halves).
+// Lane `src`'s value of v (a 32- or 64-bit value), the same in every lane.
+template <typename T>
+__device__ __forceinline__ T read_lane(T v, int src)
+{
+    if constexpr (sizeof(T) == 8) {
+        const uint64_t u = *reinterpret_cast<uint64_t *>(&v);
+        const uint64_t o = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, src) |
+                           ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), src) << 32);
+        return *reinterpret_cast<const T *>(&o);
+    } else {
+        const uint32_t o = (uint32_t)__builtin_amdgcn_readlane((int)*reinterpret_cast<uint32_t *>(&v), src);
+        return *reinterpret_cast<const T *>(&o);
+    }
+}
+
+// The steps that combine a group of G lanes.  Within a row of 16 lanes DPP
+// moves: after the two quad swaps every quad agrees, the half-row mirror
+// joins the two quads of a half row, the row mirror joins the halves.  Wider
+// groups (32 or 64 lanes, the whole wave active) then combine their rows'
+// results read from lanes 0, 16, 32 and 48 into scalar registers, instead of
+// cross-lane shuffles through the LDS unit, each of which costs a round trip.
 template <int G, typename T, typename Op>
 __device__ __forceinline__ T group_reduce(T v, Op op)
 {
-    if constexpr (G <= 16) {
+    if constexpr (G == 32 || G == 64) {
+        v = group_reduce<16>(v, op);
+        const T r0 = read_lane(v, 0), r1 = read_lane(v, 16), r2 = read_lane(v, 32), r3 = read_lane(v, 48);
+        if constexpr (G == 64) return op(op(r0, r1), op(r2, r3));
+        else return (threadIdx.x & 32) ? op(r2, r3) : op(r0, r1);
+    } else if constexpr (G <= 16) {
         auto step = [&](auto ctrl) {
             constexpr int C = decltype(ctrl)::value;
             if constexpr (sizeof(T) == 8) {
@@ -63,8 +86,7 @@ __device__ __forceinline__ T group_reduce(T v, Op op)
         if constexpr (G >= 8) step(std::integral_constant<int, 0x141>{});
         if constexpr (G >= 16) step(std::integral_constant<int, 0x140>{});
     } else {
-#pragma unroll
-        for (int off = G / 2; off > 0; off >>= 1) v = op(v, __shfl_xor(v, off, G));
+        static_assert(G <= 64, "a lane group lies within one wave");
     }
     return v;
 }
