@@ -1062,29 +1062,12 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
         asm volatile("" : "+s"(Kt), "+s"(kd), "+v"(ln));
         const int lr = ln >> 3;  // this lane's row within a DMA instruction
         // this lane's byte offset in A instruction g (LDS rows RPI*g ..)
-        auto a_off = [&](int g) -> uint32_t {
+        // ... given ri, the row index of this lane's row of instruction g
+        // (gathered rows; unused otherwise)
+        auto a_off_ri = [&](int g, int32_t ri) -> uint32_t {
             const int trow = g * RPI + lr;                       // row of the tile
             const int kc = (ln & 7) ^ lr ^ (g & 1);                // position ^ swz(row)
             const int64_t r = r0 + trow;
-            // Gathered rows: the RPI row indices of this instruction's rows
-            // are read with scalar loads (the rows are the same for the whole
-            // wave), so they do not wait for the output stores of the
-            // workgroup's previous tile; each lane takes its own.  Rows at or
-            // past cap (the shared expert's) take none, and the indices read
-            // are clamped into the array.
-            int32_t ri = 0;
-            const int64_t rb = r0 + (int64_t)g * RPI;
-            if (row_index != nullptr && rb + RPI <= cap) {
-                const rows_t vj = ld_rows(row_index + rb);
-#pragma unroll
-                for (int j = 0; j < RPI; ++j) ri = lr == j ? vj[j] : ri;
-            } else if (row_index != nullptr && rb < cap) {
-#pragma unroll
-                for (int j = 0; j < RPI; ++j) {
-                    const int32_t vj = ld_meta(row_index + (rb + j < cap ? rb + j : cap - 1));
-                    ri = lr == j ? vj : ri;
-                }
-            }
             int64_t off;
             if (r >= r1) off = a_bytes;                            // past the expert: zeros
             else if (row_index) {
@@ -1094,6 +1077,33 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
             }
             else off = ((int64_t)trow * Kt + kc * 8) * 2;
             return (uint32_t)off;
+        };
+        // This lane's row index in RPI indices read as one scalar load.
+        auto pick = [&](const rows_t &vj) -> int32_t {
+            int32_t ri = 0;
+#pragma unroll
+            for (int j = 0; j < RPI; ++j) ri = lr == j ? vj[j] : ri;
+            return ri;
+        };
+        auto a_off = [&](int g) -> uint32_t {
+            // Gathered rows: the RPI row indices of this instruction's rows
+            // are read with scalar loads (the rows are the same for the whole
+            // wave), so they do not wait for the output stores of the
+            // workgroup's previous tile; each lane takes its own.  Rows at or
+            // past cap (the shared expert's) take none, and the indices read
+            // are clamped into the array.
+            int32_t ri = 0;
+            const int64_t rb = r0 + (int64_t)g * RPI;
+            if (row_index != nullptr && rb + RPI <= cap) {
+                ri = pick(ld_rows(row_index + rb));
+            } else if (row_index != nullptr && rb < cap) {
+#pragma unroll
+                for (int j = 0; j < RPI; ++j) {
+                    const int32_t vj = ld_meta(row_index + (rb + j < cap ? rb + j : cap - 1));
+                    ri = lr == j ? vj : ri;
+                }
+            }
+            return a_off_ri(g, ri);
         };
         // ... in this wave's B instruction q, instruction g of the operand
         auto b_off = [&](int q, int g) -> uint32_t {
@@ -1105,8 +1115,22 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
             // one descriptor and one set of offsets: the operand this wave loads
             src.ra = loads_a ? desc_a : desc_b;
             if (loads_a) {
+                const int64_t gb = r0 + (int64_t)wave * NI * RPI;  // first row of this wave's instructions
+                // (only the gate-up GEMM gathers its rows: the down GEMM's code
+                // keeps its register allocation)
+                if (GATED && row_index != nullptr && gb + NI * RPI <= cap) {
+                    // every instruction's rows are routed rows: issue all NI
+                    // index loads before using any, so the prologue waits for
+                    // one scalar-load latency instead of NI in a row
+                    rows_t vr[NI];
 #pragma unroll
-                for (int q = 0; q < NI; ++q) src.voa[q] = a_off(wave * NI + q);
+                    for (int q = 0; q < NI; ++q) vr[q] = ld_rows(row_index + gb + q * RPI);
+#pragma unroll
+                    for (int q = 0; q < NI; ++q) src.voa[q] = a_off_ri(wave * NI + q, pick(vr[q]));
+                } else {
+#pragma unroll
+                    for (int q = 0; q < NI; ++q) src.voa[q] = a_off(wave * NI + q);
+                }
             } else {
 #pragma unroll
                 for (int q = 0; q < NI; ++q) src.voa[q] = b_off(q, wb * NI + q);
