@@ -977,11 +977,6 @@ __device__ __forceinline__ void gemm_class(uint4 *ring, const uint16_t *__restri
     const WorkSplit ws((int64_t)tile_prefix[ne] * n_tiles, nk, grp_size,
                        TAIL ? (deal ? SPLIT_NEVER : SPLIT_ALWAYS) : SPLIT_AUTO);
     if (ws.T == 0 || v < 0 || v >= grp_size) return;
-    // This lane's chunk within a DMA instruction: row lane/CPR of the
-    // instruction's rows, LDS position lane%CPR, global chunk
-    // (lane%CPR) ^ swz(row); swz depends on the instruction only through its
-    // parity, so two byte offsets cover every instruction.
-    const int lrow = lane >> 3;
     const uint32_t ring_base = lds_addr(ring);
     const uint4 *const a_ring = ring;
     const uint4 *const b_ring = ring + ASL * A_STAGE;
