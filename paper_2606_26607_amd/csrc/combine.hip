@@ -46,22 +46,51 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint16_t *__restrict
         const int i = (int)(item - t * chunks) * (int)blockDim.x + (int)threadIdx.x;
         // the token's k slots (k <= 16): lane j of every wave loads slot j's
         // row and weight, and the slot loop reads them from those lanes, so
-        // the k index loads are one load instead of a chain of k
+        // the k index loads are one load instead of a chain of k.  The
+        // ballot (taken while the whole wave is active) marks the slots with
+        // a row here; the loop visits only those, in slot order.
         const int lane = (int)threadIdx.x & 63;
         const int32_t my_r = lane < k ? pair_to_row[t * k + lane] : -1;
         const float my_w = lane < k ? w[t * k + lane] : 0.f;
+        uint64_t present = __builtin_amdgcn_ballot_w64(my_r >= 0 && my_r < y_rows);
         if (i >= vecs) continue;
         const bool has_shared = shared_y != nullptr && t >= sb && t < sb + sc;
         uint4 *o = reinterpret_cast<uint4 *>(out + t * H);
         float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-        if (accumulate) add8(acc, o[i], 1.0f);
-        if (has_shared) add8(acc, reinterpret_cast<const uint4 *>(shared_y + (t - sb) * H)[i], 1.0f);
-        for (int j = 0; j < k; ++j) {
-            const int32_t r = __builtin_amdgcn_readlane(my_r, j);
-            if (r >= 0 && r < y_rows)
-                add8(acc, load_last_use(reinterpret_cast<const uint4 *>(y + (int64_t)r * H) + i),
-                     __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_w), j)));
-        }
+        // Sources are loaded before they are added, two rows at a time (the
+        // prior output and the shared row with the first two): one memory
+        // round trip per pair of present slots instead of one per source.
+        // They are added in the same order (prior, shared, then the slots in
+        // order), so the sum is the same.
+        uint4 pv = make_uint4(0, 0, 0, 0), sv = make_uint4(0, 0, 0, 0);
+        if (accumulate) pv = o[i];
+        if (has_shared) sv = reinterpret_cast<const uint4 *>(shared_y + (t - sb) * H)[i];
+        bool first = true;
+        do {
+            int ja = -1, jb = -1;
+            if (present) {
+                ja = __builtin_ctzll(present);
+                present &= present - 1;
+            }
+            if (present) {
+                jb = __builtin_ctzll(present);
+                present &= present - 1;
+            }
+            uint4 va = make_uint4(0, 0, 0, 0), vb = make_uint4(0, 0, 0, 0);
+            if (ja >= 0)
+                va = load_last_use(reinterpret_cast<const uint4 *>(y + (int64_t)__builtin_amdgcn_readlane(my_r, ja) * H) + i);
+            if (jb >= 0)
+                vb = load_last_use(reinterpret_cast<const uint4 *>(y + (int64_t)__builtin_amdgcn_readlane(my_r, jb) * H) + i);
+            if (first) {
+                if (accumulate) add8(acc, pv, 1.0f);
+                if (has_shared) add8(acc, sv, 1.0f);
+                first = false;
+            }
+            if (ja >= 0)
+                add8(acc, va, __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_w), ja)));
+            if (jb >= 0)
+                add8(acc, vb, __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_w), jb)));
+        } while (present);
         uint4 v;
         v.x = pack_bf16(acc[0], acc[1]);
         v.y = pack_bf16(acc[2], acc[3]);

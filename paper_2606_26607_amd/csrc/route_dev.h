@@ -106,11 +106,21 @@ template <int G, int S>
 __device__ __forceinline__ void route_token(const float *__restrict__ row, int E, int k, int sub,
                                             int32_t *__restrict__ ids, float *__restrict__ w)
 {
+    // All S loads go out before the first is used: a lane past E reads
+    // logit E-1 (in bounds) and drops it.  Guarded by e < E instead, each
+    // load sat in its own branch and waited for its data before the next
+    // was issued, S memory round trips in a row.
+    float lv[S];
+#pragma unroll
+    for (int m = 0; m < S; ++m) {
+        const int e = sub + m * G;
+        lv[m] = row[e < E ? e : E - 1];
+    }
     uint64_t key[S];
 #pragma unroll
     for (int m = 0; m < S; ++m) {
-        int e = sub + m * G;
-        key[m] = e < E ? ((uint64_t)order_key(row[e]) << 32) | (uint32_t)(~e) : 0ull;
+        const int e = sub + m * G;
+        key[m] = e < E ? ((uint64_t)order_key(lv[m]) << 32) | (uint32_t)(~e) : 0ull;
     }
     // round j's winner is known to every lane of the group, so each lane
     // adds exp(l_j - l_0) in rank order: the normalising sum is the same
