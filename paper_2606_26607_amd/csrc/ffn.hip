@@ -184,11 +184,19 @@ struct SchedShape {
 // of one large-tile K-slice.
 enum SmallMode { SM_PIECES_IDLE, SM_WHOLE_IDLE, SM_WHOLE_ALL, SM_PIECES_ALL, SM_PIECES_PAIR };
 
-// x / g for x >= 0, in 32 bits whenever x fits (it always does in practice;
-// a 64-bit division is a long instruction sequence on the GPU)
+// x / g (rounded down) for 0 <= x < 2^53 and g >= 1, in 32 bits whenever x
+// fits (it always does in practice).  A wider x takes a double-precision
+// quotient, exact in its integer part to within one, corrected to the
+// floor: an integer 64-bit division expands to about a hundred instructions
+// at every use, and the schedule's code runs once per launch from a cold
+// instruction cache.
 __device__ __forceinline__ int64_t div_g(int64_t x, int g)
 {
-    return x <= 0x7fffffff ? (int64_t)((uint32_t)x / (uint32_t)g) : x / g;
+    if (x <= 0x7fffffff) return (int64_t)((uint32_t)x / (uint32_t)g);
+    int64_t q = (int64_t)((double)x / (double)g);
+    q -= q * g > x ? 1 : 0;
+    q += (q + 1) * g <= x ? 1 : 0;
+    return q;
 }
 constexpr float PIECE_OVH = 8.0f;  // fixed cost of a stream-K piece, in large slices
 constexpr float PAIR_OVH = 3.0f;   // fixed cost of splitting a whole small-row tile in two, in large slices
@@ -285,7 +293,7 @@ struct SchedOut {
     int4 *mt[2];  // per small m-tile: expert, first row, end row
 };
 
-// (A device function run by one block: one thread per expert, at least two
+// (A device function run by one block: one thread per expert, at least four
 // waves, whole waves; NE_MAX bounds the experts, the shared one included.
 // offsets may point to LDS.)
 template <int NE_MAX>
@@ -301,11 +309,10 @@ __device__ __forceinline__ void schedule_body(const int32_t *__restrict__ offset
     __shared__ int32_t tot[3 * NC];
     __shared__ int32_t ptot[4];
     __shared__ int32_t big[2];  // the largest expert and its rows
-    __shared__ unsigned long long kmin[2];
-    // one thread per expert, at least two waves, whole waves (the launch
+    __shared__ unsigned long long kmin[4];
+    // one thread per expert, at least four waves, whole waves (the launch
     // sizes the block)
     const int e = threadIdx.x, lane = e & 63, wv = e >> 6;
-    for (int64_t i = e; i < n_counters; i += blockDim.x) counters[i] = 0;
     // experts: the El routed ones, then the shared one when there are shared
     // rows; rows fit int32 (cap + shared rows < 2^31 is checked on the host)
     const int ne = El + (shared_rows > 0 ? 1 : 0);
@@ -379,24 +386,31 @@ __device__ __forceinline__ void schedule_body(const int32_t *__restrict__ offset
         }
         __syncthreads();
         L = big[0];
-        // Candidates of GEMM gi on lanes 0 .. 19 of wave gi: base
-        // candidate c = t / 2 (t = lane) with D = 0 (even t) or with the
-        // fewest moves D that save a round of large tiles (odd t; none where
-        // that takes more than ND_SCHED - 1 moves or more m-tiles than the
-        // largest expert has).  Each takes the cheaper small tile height
-        // (ties: 64 rows).  Its key is the cost's bits (non-negative floats
-        // order as integers), then the candidate as c * ND_SCHED + D (ties:
-        // the lowest: smax 96, then fewer moves), with the height in the
-        // lowest bit.
+        // Candidates of GEMM gi with small tile height tall ? 128 : 64 rows
+        // on lanes 0 .. 19 of wave 2 * gi + tall: base candidate c = t / 2
+        // (t = lane) with D = 0 (even t) or with the fewest moves D that
+        // save a round of large tiles (odd t; none where that takes more
+        // than ND_SCHED - 1 moves or more m-tiles than the largest expert
+        // has).  Its key is the cost's bits (non-negative floats order as
+        // integers), then the candidate as c * ND_SCHED + D, then the height
+        // bit, so the least key over both waves of a GEMM is its cheapest
+        // candidate and height (ties: smax 96, then fewer moves, then 64
+        // rows).  One height per wave halves each lane's work (the costing
+        // is a divergent chain of divisions and branches).
+        // (the wave index is made uniform and the GEMM's shape selected field
+        // by field, so the shape stays in scalar registers: indexed by a
+        // per-lane value it was read with vector loads from the argument
+        // segment, a memory round trip in the costing's chain)
         unsigned long long key = ~0ull;
-        const int gi = wv, t = lane;
-        if (wv < 2 && t < 2 * NC) {
+        const int wvu = __builtin_amdgcn_readfirstlane(wv);
+        const int gi = wvu >> 1, tall = wvu & 1, t = lane;
+        if (wvu < 4 && t < 2 * NC) {
             const int c = t / 2;
             const int nt = gi ? sh.nt_dn : sh.nt_gu, nk = gi ? sh.nk_dn : sh.nk_gu, g = sh.grid;
-            const int wf64 = sh.wfit[gi][0], wf128 = sh.wfit[gi][1];
-            const float wh64 = sh.whole[gi][0], wh128 = sh.whole[gi][1];
+            const int wf = gi ? (tall ? sh.wfit[1][1] : sh.wfit[1][0]) : (tall ? sh.wfit[0][1] : sh.wfit[0][0]);
+            const float wh = gi ? (tall ? sh.whole[1][1] : sh.whole[1][0]) : (tall ? sh.whole[0][1] : sh.whole[0][0]);
             const int64_t tl0 = tot[3 * c];
-            int64_t tl = tl0, t64 = tot[3 * c + 1], t128 = tot[3 * c + 2];
+            int64_t tl = tl0, ts = tot[3 * c + 1 + tall];
             int D = 0;
             bool valid = true;
             if (t & 1) {
@@ -408,33 +422,30 @@ __device__ __forceinline__ void schedule_body(const int32_t *__restrict__ offset
                     D = (int)dmin;
                     const int2 r = rows_moved(big[1], make_int2(xl, 0), D);
                     tl += r.x - xl;
-                    t64 += (r.y + 63) / 64 - vals[L][3 * c + 1];
-                    t128 += (r.y + 127) / 128 - vals[L][3 * c + 2];
+                    ts += (r.y + (tall ? 127 : 63)) / (tall ? 128 : 64) - vals[L][3 * c + 1 + tall];
                 }
             }
             if (valid) {
+                // one inlined copy of the cost model for both heights
+                const int cnum = tall ? SMALL128.cost_num : SMALL64.cost_num;
                 const float cl = large_cost(tl * nt, nk, g);
-                const float c64 = gemm_cost(cl, tl * nt, t64 * nt, nk, g, SMALL64.cost_num, wf64, wh64, false);
-                const float c128 = gemm_cost(cl, tl * nt, t128 * nt, nk, g, SMALL128.cost_num, wf128, wh128, true);
-                const float cmin = c128 < c64 ? c128 : c64;
-                key = ((unsigned long long)__float_as_uint(cmin) << 32) |
-                      ((unsigned)(c * ND_SCHED + D) << 1) | (c128 < c64);
+                const float cost = gemm_cost(cl, tl * nt, ts * nt, nk, g, cnum, wf, wh, tall != 0);
+                key = ((unsigned long long)__float_as_uint(cost) << 32) | ((unsigned)(c * ND_SCHED + D) << 1) |
+                      (unsigned)tall;
             }
         }
-        // the cheapest candidate of each GEMM: a minimum over lanes 0 .. 31 of
-        // its wave
-        if (wv < 2) {
-#pragma unroll
-            for (int off = 1; off < 32; off <<= 1) {
-                const unsigned long long o = __shfl_xor(key, off, 64);
-                key = o < key ? o : key;
-            }
-            if (t == 0) kmin[gi] = key;
+        // the cheapest of each wave: a minimum over lanes 0 .. 31 (DPP within
+        // rows, then the rows' results; the whole wave is active), then the
+        // lesser of the GEMM's two waves
+        if (wvu < 4) {
+            key = route_dev::group_reduce<32>(key, [](unsigned long long a, unsigned long long b) { return a < b ? a : b; });
+            if (t == 0) kmin[wvu] = key;
         }
         __syncthreads();
         for (int i = 0; i < 2; ++i) {
-            cand[i] = (int)((kmin[i] & 0xffffffffu) >> 1);
-            kinds |= (int)(kmin[i] & 1) << i;
+            const unsigned long long km = kmin[2 * i] < kmin[2 * i + 1] ? kmin[2 * i] : kmin[2 * i + 1];
+            cand[i] = (int)((km & 0xffffffffu) >> 1);
+            kinds |= (int)(km & 1) << i;
         }
     }
     int32_t v[4];
@@ -469,6 +480,9 @@ __device__ __forceinline__ void schedule_body(const int32_t *__restrict__ offset
             }
         }
     }
+    // the GEMMs' split-K tile counters, cleared last: before a barrier,
+    // the barrier's fence would wait for these stores to land
+    for (int64_t i = e; i < n_counters; i += blockDim.x) counters[i] = 0;
 }
 
 __global__ __launch_bounds__(1024) void schedule_kernel(const int32_t *__restrict__ offsets, int El,
@@ -1733,7 +1747,7 @@ __global__ __launch_bounds__(256) void layer_scan_sched_kernel(const int32_t *__
     // expert totals: thread t sums expert t % El over chunks t / El, + S, ...
     // (S = 256 / El column groups), then one lane per expert adds the groups
     // and the lanes scan the totals into the experts' first rows
-    constexpr int UNR = 8;
+    constexpr int UNR = 16;  // loads in flight per thread and pass (one pass for 256 chunks of 16 experts)
     __shared__ int32_t part[256];
     __shared__ int32_t soff[64 + 1];
     const int t = threadIdx.x, S = 256 / El;
@@ -2021,7 +2035,7 @@ hipError_t launch_grouped_ffn(const uint16_t *x, int64_t x_rows, const int32_t *
     if (shared_rows > 0 && !c.big) return hipErrorNotSupported;  // the host API checks this first
     {
         KernelTimer timer(MOE_K_SCHEDULE, s);
-        const unsigned threads = (unsigned)(ceil_div(c.ne > 128 ? c.ne : 128, 64) * 64);
+        const unsigned threads = (unsigned)(ceil_div(c.ne > 256 ? c.ne : 256, 64) * 64);
         schedule_kernel<<<dim3(1), dim3(threads), 0, s>>>(offsets, El, cap, shared_rows, c.bm(), c.big, c.sh, c.so,
                                                           c.cnt, c.n_cnt);
         hipError_t err = hipGetLastError();

@@ -135,7 +135,10 @@ __device__ __forceinline__ void scan_scatter_body(const int32_t *__restrict__ id
                                                   int32_t *__restrict__ row_to_pair,
                                                   int32_t *__restrict__ pair_to_row, int64_t blk)
 {
-    constexpr int CHUNK = ROUNDS * 64, UNR = 4;
+    // UNR loads in flight per thread and pass: each pass waits for its
+    // loads, so the passes are memory round trips in a row (a 256-chunk
+    // histogram of 16 experts is one pass)
+    constexpr int CHUNK = ROUNDS * 64, UNR = 16;
     __shared__ int32_t part_tot[256], part_bef[256];
     __shared__ int32_t next_row[4][64];
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
@@ -197,7 +200,12 @@ __device__ __forceinline__ void scan_scatter_body(const int32_t *__restrict__ id
     const int64_t c = c_first + wv;
     if (c >= nchunks) return;
     if (lane < El) {
-        for (int64_t cc = c_first; cc < c; ++cc) row += chunk_cnt[cc * El + lane];
+        // the counts of the block's chunks before this one (at most 3),
+        // loaded together
+        int32_t before[3];
+#pragma unroll
+        for (int q = 0; q < 3; ++q) before[q] = c_first + q < c ? chunk_cnt[(c_first + q) * El + lane] : 0;
+        row += before[0] + before[1] + before[2];
         next_row[wv][lane] = row;
     }
     __builtin_amdgcn_wave_barrier();
