@@ -219,7 +219,8 @@ moe_status moe_combine(const uint16_t *y, int64_t y_rows, const int32_t *pair_to
  * those four calls write.  Where the shapes allow it (at most 64 local
  * experts, the large-tile FFN shapes: H and I_s multiples of 64, at least
  * 128), routing, the permutation and the FFN's tile schedule run in fused
- * launches: for small inputs (at most 16384 pairs) routing, then the
+ * launches: for small inputs (pairs x (bits of the local expert index + 2)
+ * at most 16384, e.g. 2048 pairs over 32 experts) routing, then the
  * permutation with the schedule in one workgroup; for larger ones routing
  * with the permutation's histogram, then its scan and scatter with the
  * schedule: two launches instead of three or four.  Otherwise it runs the

@@ -1667,6 +1667,15 @@ __global__ __launch_bounds__(GEMM_THREADS) void splitk_reduce(const int32_t *__r
 // what its own launch computes.
 // ---------------------------------------------------------------------------
 constexpr int LAYER_NE_MAX = 128;  // experts of the fused schedule (local ones + shared), at most
+// The layer's one-workgroup permutation takes at most this many pair-steps
+// (pairs x (index bits + 2)); larger inputs take the two fused launches.
+// Measured (same-box A/B of the layer step): 4096 pairs over 32 local
+// experts (32768 pair-steps: the 512-token decode slice) 0.4971 -> 0.4952 ms
+// and 8192 pairs over one expert (32768: the Mixtral EP slice) 0.4440 ->
+// 0.4407 ms in two launches; 512 pairs over 32 experts (4096: the 64-token
+// decode slice) 0.4102 ms in one workgroup against 0.4115 in two.  The
+// threshold lies between the measured points.
+constexpr int64_t LAYER_SMALL_WORK = 16 * 1024;
 
 // Small inputs (the one-workgroup permutation), after the routing launch:
 // one block of 1024 threads permutes the pairs, then schedules the FFN's
@@ -2087,7 +2096,7 @@ bool layer_fused_prep(int64_t T, int k, int El, int H, int Is, int64_t sc)
     while ((1 << nbits) < El + 2) ++nbits;
     const bool fuse = npairs > 0 && El <= 64 && El + (sc > 0 ? 1 : 0) <= LAYER_NE_MAX &&
                       ffn_large_tiles(T, cap + sc, H, Is);
-    const bool small = npairs <= permute_dev::SMALL_PAIRS && npairs * (nbits + 2) <= permute_dev::SMALL_WORK;
+    const bool small = npairs <= permute_dev::SMALL_PAIRS && npairs * (nbits + 2) <= LAYER_SMALL_WORK;
     return fuse && (small || permute_chunks(T, k, El) <= permute_dev::SCAN_SCATTER_MAX_CHUNKS);
 }
 
@@ -2113,7 +2122,7 @@ hipError_t launch_layer(const uint16_t *x, const float *logits, int64_t T, int E
     const FfnCall c(T, true, El, cap, H, Is, sc, ws_ffn);
     int nbits = 0;
     while ((1 << nbits) < El + 2) ++nbits;
-    const bool small = npairs <= permute_dev::SMALL_PAIRS && npairs * (nbits + 2) <= permute_dev::SMALL_WORK;
+    const bool small = npairs <= permute_dev::SMALL_PAIRS && npairs * (nbits + 2) <= LAYER_SMALL_WORK;
     if (small && (err = launch_route(logits, T, E, k, ids, w, s)) != hipSuccess) return err;
     {
         KernelTimer timer(MOE_K_LAYER_PREP, s);

@@ -80,7 +80,8 @@ def test_one_call_equals_four_calls(name):
 
 
 @pytest.mark.parametrize("T,H,E,k,I,P,layout,shared,fused", [
-    (1000, 256, 16, 3, 256, 1, "replicated", False, True),    # one workgroup; 3 pairs per token
+    (700, 256, 16, 3, 256, 1, "replicated", False, True),     # one workgroup (2100 pairs); 3 pairs per token
+    (1000, 256, 16, 3, 256, 1, "replicated", False, True),    # 3000 pairs: two fused launches
     (6000, 256, 16, 3, 256, 2, "ep", False, True),            # 256-pair chunks straddled by tokens
     (7000, 128, 64, 6, 128, 1, "replicated", False, True),    # 64 local experts, 6 pairs per token
     (300000, 128, 64, 8, 128, 8, "ep", False, True),          # pairs x experts above 2^24: 1024-pair chunks
