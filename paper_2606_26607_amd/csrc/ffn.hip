@@ -396,11 +396,11 @@ __device__ __forceinline__ void schedule_body(const int32_t *__restrict__ offset
         // bit, so the least key over both waves of a GEMM is its cheapest
         // candidate and height (ties: smax 96, then fewer moves, then 64
         // rows).  One height per wave halves each lane's work (the costing
-        // is a divergent chain of divisions and branches).
-        // (the wave index is made uniform and the GEMM's shape selected field
-        // by field, so the shape stays in scalar registers: indexed by a
-        // per-lane value it was read with vector loads from the argument
-        // segment, a memory round trip in the costing's chain)
+        // is a divergent chain of divisions and branches).  The wave index
+        // is made uniform and the GEMM's shape selected field by field, so
+        // the shape stays in scalar registers: indexed by a per-lane value,
+        // it was read with vector loads from the argument segment, a memory
+        // round trip in the costing's chain.
         unsigned long long key = ~0ull;
         const int wvu = __builtin_amdgcn_readfirstlane(wv);
         const int gi = wvu >> 1, tall = wvu & 1, t = lane;
