@@ -634,7 +634,8 @@ def main():
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU's share of the layer; --gpus {args.gpus} is not "
-              "supported (the multi-GPU collectives are outside this build)", file=sys.stderr)
+              "supported (libmoe has no multi-GPU collectives: the TP all-reduce and the EP "
+              "all-to-alls are left to the caller)", file=sys.stderr)
         sys.exit(2)
 
     import torch
