@@ -23,9 +23,10 @@ __device__ __forceinline__ int local_index(int32_t id, int e0, int El)
 // wavefronts then place their pairs in order.  Same stable result as the
 // multi-kernel path.  One workgroup's time grows with the pairs and the
 // ballots per pair (bits of the local expert index) while the multi-kernel
-// path costs about two launches, so the workgroup takes at most
+// path costs about two launches, so moe_permute's workgroup takes at most
 // SMALL_WORK pair-steps (measured: 8192 pairs over 1 local expert and 4096
-// over 32 are faster here, 8192 over 8 in two launches).
+// over 32 are faster here, 8192 over 8 in two launches).  The layer forward,
+// whose two-launch path also routes and schedules, has its own threshold.
 constexpr int SMALL_PAIRS = 16 * 1024;
 constexpr int64_t SMALL_WORK = 32 * 1024;
 // (A device function run by a whole block of 1024 threads.)
